@@ -1,0 +1,188 @@
+/*
+ * svl.h -- C ABI of the budget-adapted MLLM prefill library (libsvl.so) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library runs the inference-time prefill of SmartVL ("Look Less, Think
+ * Faster: Joint Token-Compute Adaptation for Multimodal LLMs"): the token
+ * controller's per-token scores and an integer keep budget select the vision
+ * tokens to keep (Sec. 3.1 and Sec. 3.3 "Inference": the budget projection
+ * discards the lowest-confidence tokens first); the kept tokens are packed
+ * with the text tokens into one compressed, contiguous sequence per sample
+ * (Sec. 3.1); then the LLaMA decoder layers run under the compute
+ * controller's masks (Sec. 3.2): a layer with mask 0 is bypassed through its
+ * residual, an inactive head contributes nothing, and head group j also gates
+ * slice j of the FFN intermediate dimension.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Ownership.  The caller owns every buffer: weights, inputs, outputs and the
+ *   workspace.  The library keeps no per-call state and allocates no device
+ *   memory in these calls.  Host arrays (keep, masks, cu_seqlens) are read or
+ *   written before the call returns.
+ * Pointers.  "dev" pointers are HIP device pointers (16-byte aligned);
+ *   "host" pointers are ordinary host memory.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL: the null
+ *   stream).  All device work is enqueued on it; device outputs are valid once
+ *   the stream reaches that point.  No call synchronises the stream.
+ * Dtypes.  `svl_config.dtype` selects the storage type of weights and of the
+ *   vision / text hidden states: SVL_F32 (float) or SVL_BF16 (bfloat16).  The
+ *   residual stream `resid` is always float32.  SVL_BF16 runs bf16 matrix
+ *   products with float32 accumulation.
+ * Layouts.  Row-major throughout.  Linear weights use the [out][in] layout
+ *   (y = x W^T).  The packed residual holds the samples one after another:
+ *   rows cu_seqlens[b] .. cu_seqlens[b+1]-1 are sample b's sequence, kept
+ *   vision tokens (ascending original index) followed by its text tokens.
+ * Errors.  Every argument is validated before anything is enqueued, so an
+ *   error leaves the stream untouched.  A non-zero svl_status is returned and
+ *   svl_last_error() gives a message (per thread).  HIP launch errors are
+ *   reported as SVL_E_HIP; faults inside kernels surface at the caller's
+ *   next synchronisation.
+ */
+#ifndef SVL_H
+#define SVL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SVL_ABI_VERSION 1
+
+typedef enum {
+  SVL_OK = 0,
+  SVL_E_NULL = 1,       /* a required pointer is NULL */
+  SVL_E_SHAPE = 2,      /* inconsistent or unsupported sizes */
+  SVL_E_VALUE = 3,      /* a value out of range (keep budget, mask byte not 0/1) */
+  SVL_E_WORKSPACE = 4,  /* workspace smaller than svl_workspace_bytes() */
+  SVL_E_DTYPE = 5,      /* unknown dtype */
+  SVL_E_HIP = 6,        /* HIP runtime error (no device, launch failure) */
+  SVL_E_ALIGN = 7       /* a device pointer not 16-byte aligned */
+} svl_status;
+
+typedef enum { SVL_F32 = 0, SVL_BF16 = 1 } svl_dtype;
+
+/* Decoder shape (LLaMA block: pre-RMSNorm, rotate-half RoPE, causal
+ * attention with n_kv_heads K/V heads shared by n_heads/n_kv_heads query
+ * heads each, SwiGLU FFN, no biases).  n_groups is the number of head
+ * groups G of the layer-head controller (Sec. 3.2); FFN slice j is the
+ * channel range [j*d_ffn/G, (j+1)*d_ffn/G).
+ * Requirements: all sizes > 0; n_heads % n_kv_heads == 0; head_dim even;
+ * d_ffn % n_groups == 0; for SVL_BF16 also d_model % 64 == 0,
+ * head_dim in {64, 128}, d_ffn/n_groups % 64 == 0. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, n_groups;
+  float rms_eps;     /* RMSNorm epsilon */
+  float rope_theta;  /* RoPE base: pair (r, r+d/2) turns by p * theta^(-2r/d) */
+  int32_t dtype;     /* svl_dtype */
+} svl_config;
+
+/* One layer's weights (dev, config dtype).  Shapes:
+ *   attn_norm, ffn_norm [D];  wq [A*d][D];  wk, wv [KV*d][D];  wo [D][A*d];
+ *   w_gate, w_up [F][D];  w_down [D][F]. */
+typedef struct {
+  const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+} svl_layer_weights;
+
+/* Batch description: B samples, each with n_vision scored vision tokens and
+ * n_text text tokens; keep (host [B]) is each sample's keep budget k_b in
+ * [0, n_vision].  Sample b's sequence length is S_b = k_b + n_text. */
+typedef struct {
+  int32_t batch, n_vision, n_text;
+  const int32_t *keep;
+} svl_batch;
+
+/* Executed FLOPs (2 per multiply-add, matrix products only), by component:
+ * q: query projection; kv: key and value projections; o: output projection;
+ * attn: causal scores and probability-value products; ffn: gate, up, down. */
+typedef struct {
+  uint64_t q, kv, o, attn, ffn, total;
+} svl_flops;
+
+/* Token selection and packing (Sec. 3.1; Sec. 3.3 budget projection).
+ * For each sample b: keeps the keep[b] highest scores of scores[b][:]
+ * (ordering: larger score first, NaN below every number, -0 equal to +0,
+ * equal scores -> lower index first), writes the kept indices in ascending
+ * order to kept_idx[b][0..k_b) and -1 to kept_idx[b][k_b..N), and packs
+ * [vision[b][kept] ; text[b]] into resid rows cu_seqlens[b]..cu_seqlens[b+1].
+ *   scores   dev  float  [B][N]
+ *   vision   dev  dtype  [B][N][D]
+ *   text     dev  dtype  [B][T][D]
+ *   kept_idx dev  int32  [B][N]       (out)
+ *   resid    dev  float  [sum S_b][D] (out, widened exactly from dtype)
+ *   cu_seqlens host int32 [B+1]       (out; cu_seqlens[0] = 0)
+ *   ws/ws_bytes: workspace of at least svl_workspace_bytes(cfg, B, sum S_b). */
+svl_status svl_select_tokens(const svl_config *cfg, const svl_batch *batch,
+                             const float *scores, const void *vision, const void *text,
+                             int32_t *kept_idx, float *resid, int32_t *cu_seqlens,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* One decoder layer on a packed residual (Sec. 3.2), in place.
+ *   layer      index of the layer (informational; weights are passed directly)
+ *   cu_seqlens host int32 [batch+1]: the packed rows of each sample
+ *   layer_on   host uint8 [batch]: 0 = the layer is bypassed for the sample
+ *   head_mask  host uint8 [batch][A]: query-head gates (0/1); a K/V head is
+ *              computed iff one of its query heads is active
+ *   ffn_mask   host uint8 [batch][G] or NULL (FFN ungated): FFN slice gates
+ *   resid      dev float [cu_seqlens[batch]][D], updated in place
+ * Positions for RoPE are 0..S_b-1 within each sample.  Rows of samples with
+ * layer_on = 0 are not read or written. */
+svl_status svl_layer_forward(const svl_config *cfg, int32_t layer, const svl_layer_weights *w,
+                             int32_t batch, const int32_t *cu_seqlens, const uint8_t *layer_on,
+                             const uint8_t *head_mask, const uint8_t *ffn_mask, float *resid,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* The whole budget-adapted prefill: svl_select_tokens followed by every
+ * layer under the masks (Eq. (1) with the allocation given).
+ *   layers     host array of cfg->n_layers svl_layer_weights
+ *   layer_mask host uint8 [B][L];  head_mask host uint8 [B][L][A];
+ *   ffn_mask   host uint8 [B][L][G] or NULL
+ *   kept_idx, resid, cu_seqlens: as svl_select_tokens; resid holds the
+ *   residual stream after the last layer (no final norm, no LM head)
+ *   flops      host, may be NULL: executed FLOPs (same as svl_count_flops) */
+svl_status svl_prefill(const svl_config *cfg, const svl_layer_weights *layers,
+                       const svl_batch *batch, const float *scores, const void *vision,
+                       const void *text, const uint8_t *layer_mask, const uint8_t *head_mask,
+                       const uint8_t *ffn_mask, int32_t *kept_idx, float *resid,
+                       int32_t *cu_seqlens, svl_flops *flops, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* Workspace bytes any of the calls above needs for `batch` samples and at
+ * most `total_rows` packed rows (sum of S_b), for any masks.  0 on bad args. */
+size_t svl_workspace_bytes(const svl_config *cfg, int32_t batch, int32_t total_rows);
+
+/* Executed FLOPs for the given sequence lengths (host [B]) and masks, in
+ * closed form (host only, no device work; only the shape rules that do
+ * not depend on the kernels apply).  Per executed (sample, layer) with
+ * H active query heads, K active K/V heads, C active FFN channels:
+ *   q = 2 S D d H, kv = 4 S D d K, o = 2 S H d D, attn = 2 H d S (S+1),
+ *   ffn = 6 S D C.
+ * The paper's estimator Eq. (8) charges 4 D S^2 for a full score matrix; the
+ * causal products charge only the triangle. */
+svl_status svl_count_flops(const svl_config *cfg, int32_t batch, const int32_t *seqlens,
+                           const uint8_t *layer_mask, const uint8_t *head_mask,
+                           const uint8_t *ffn_mask, svl_flops *out);
+
+/* Message for the last non-OK status returned on this thread. */
+const char *svl_last_error(void);
+
+/* SVL_ABI_VERSION of the built library. */
+int32_t svl_abi_version(void);
+
+/* ---- kernel timing (instrumentation for benchmarks) ----------------------
+ * With timing on, every launch is bracketed by two hipEvents recorded on the
+ * launch's stream; svl_timing_read() waits for the recorded events and
+ * returns the summed kernel time (ms) and launch count of one kernel class,
+ * then forgets them.  Timing adds event records between launches, so time
+ * whole calls with timing off.
+ * Kernel classes: 0 select, 1 gather, 2 rmsnorm, 3 qkv gemm, 4 attention,
+ * 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope table, 9 other. */
+#define SVL_KCLASS_COUNT 10
+svl_status svl_timing_enable(int32_t on);
+svl_status svl_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SVL_H */

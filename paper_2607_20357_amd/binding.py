@@ -1,0 +1,248 @@
+"""Python binding of libsvl (ctypes): argument marshalling only.
+
+Every step of the prefill runs in the library's HIP kernels; this module
+only turns torch tensors into device pointers, numpy arrays into host
+pointers, and status codes into exceptions.  There is no fallback: if the
+library is not built or a tensor is not on the GPU, the call fails.
+
+Function names follow the C ABI (include/svl.h).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsvl.so")
+
+SVL_F32, SVL_BF16 = 0, 1
+KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
+          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "other": 9}
+STATUS = {0: "SVL_OK", 1: "SVL_E_NULL", 2: "SVL_E_SHAPE", 3: "SVL_E_VALUE", 4: "SVL_E_WORKSPACE",
+          5: "SVL_E_DTYPE", 6: "SVL_E_HIP", 7: "SVL_E_ALIGN"}
+WEIGHT_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+
+
+class SvlError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class svl_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
+                ("n_groups", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_theta", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class svl_layer_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+
+
+class svl_batch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_vision", ctypes.c_int32),
+                ("n_text", ctypes.c_int32), ("keep", ctypes.POINTER(ctypes.c_int32))]
+
+
+class svl_flops(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in ("q", "kv", "o", "attn", "ffn", "total")]
+
+    def as_dict(self) -> Dict[str, int]:
+        return {n: int(getattr(self, n)) for n, _ in self._fields_}
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libsvl.so (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i32, u64, sz = ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    cfgp = ctypes.POINTER(svl_config)
+    lib.svl_select_tokens.argtypes = [cfgp, ctypes.POINTER(svl_batch), P, P, P, P, P,
+                                      ctypes.POINTER(i32), P, sz, P]
+    lib.svl_layer_forward.argtypes = [cfgp, i32, ctypes.POINTER(svl_layer_weights), i32,
+                                      ctypes.POINTER(i32), P, P, P, P, P, sz, P]
+    lib.svl_prefill.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), ctypes.POINTER(svl_batch),
+                                P, P, P, P, P, P, P, P, ctypes.POINTER(i32),
+                                ctypes.POINTER(svl_flops), P, sz, P]
+    lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
+    lib.svl_workspace_bytes.restype = sz
+    lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
+                                    ctypes.POINTER(svl_flops)]
+    lib.svl_last_error.restype = ctypes.c_char_p
+    lib.svl_abi_version.restype = i32
+    lib.svl_timing_enable.argtypes = [i32]
+    lib.svl_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_int64)]
+    for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
+              "svl_timing_enable", "svl_timing_read"):
+        getattr(lib, f).restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise SvlError(status, load_library().svl_last_error().decode())
+
+
+# ------------------------------------------------------------------ marshalling helpers
+def make_config(shape=None, **kw) -> svl_config:
+    """svl_config from an object with the decoder-shape attributes (or keywords)."""
+    get = (lambda n, d=None: kw.get(n, getattr(shape, n, d))) if shape is not None else kw.get
+    dtype = get("dtype", "bf16")
+    if isinstance(dtype, str):
+        dtype = SVL_BF16 if dtype == "bf16" else SVL_F32
+    return svl_config(int(get("n_layers")), int(get("d_model")), int(get("n_heads")),
+                      int(get("n_kv_heads")), int(get("head_dim")), int(get("d_ffn")),
+                      int(get("n_groups", 4)), float(get("rms_eps", 1e-6)),
+                      float(get("rope_theta", 10000.0)), int(dtype))
+
+
+def _dev(t: Optional[torch.Tensor], name: str) -> int:
+    """Device pointer of a GPU tensor; an empty tensor passes NULL (the library
+    checks whether the argument may be empty)."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.numel() == 0:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (no CPU path exists)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _host_u8(a, name: str):
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.uint8))
+    return arr, arr.ctypes.data_as(ctypes.c_void_p)
+
+
+def _host_i32(a):
+    arr = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        stream = stream.cuda_stream
+    return ctypes.c_void_p(int(stream))
+
+
+def layer_weights(w: Dict[str, torch.Tensor]) -> svl_layer_weights:
+    return svl_layer_weights(*[_dev(w[n], n) for n in WEIGHT_FIELDS])
+
+
+# ------------------------------------------------------------------ entry points
+def svl_abi_version() -> int:
+    return int(load_library().svl_abi_version())
+
+
+def svl_workspace_bytes(cfg: svl_config, batch: int, total_rows: int) -> int:
+    n = load_library().svl_workspace_bytes(ctypes.byref(cfg), int(batch), int(total_rows))
+    if n == 0:
+        raise SvlError(2, "svl_workspace_bytes: invalid configuration")
+    return int(n)
+
+
+def alloc_workspace(cfg: svl_config, batch: int, total_rows: int, device="cuda") -> torch.Tensor:
+    """Caller-owned workspace (torch provides the device memory)."""
+    return torch.empty(svl_workspace_bytes(cfg, batch, total_rows), dtype=torch.uint8, device=device)
+
+
+def svl_count_flops(cfg: svl_config, seqlens, layer_mask, head_mask, ffn_mask=None) -> Dict[str, int]:
+    sq, sqp = _host_i32(seqlens)
+    lm, lmp = _host_u8(layer_mask, "layer_mask")
+    hm, hmp = _host_u8(head_mask, "head_mask")
+    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    out = svl_flops()
+    _check(load_library().svl_count_flops(ctypes.byref(cfg), int(sq.shape[0]), sqp, lmp, hmp, fmp,
+                                          ctypes.byref(out)))
+    return out.as_dict()
+
+
+def svl_select_tokens(cfg: svl_config, keep, scores: torch.Tensor, vision: torch.Tensor,
+                      text: torch.Tensor, kept_idx: torch.Tensor, resid: torch.Tensor,
+                      ws: torch.Tensor, stream=None) -> np.ndarray:
+    """Top-k selection and packing; returns cu_seqlens (host int32 [B+1])."""
+    kp, kpp = _host_i32(keep)
+    B, N = scores.shape
+    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
+    cu = np.zeros(B + 1, dtype=np.int32)
+    _check(load_library().svl_select_tokens(
+        ctypes.byref(cfg), ctypes.byref(batch), _dev(scores, "scores"), _dev(vision, "vision"),
+        _dev(text, "text"), _dev(kept_idx, "kept_idx"), _dev(resid, "resid"),
+        cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), _dev(ws, "ws"), ws.numel(),
+        _stream(stream)))
+    return cu
+
+
+def svl_layer_forward(cfg: svl_config, layer: int, weights: Dict[str, torch.Tensor], cu_seqlens,
+                      layer_on, head_mask, ffn_mask, resid: torch.Tensor, ws: torch.Tensor,
+                      stream=None) -> None:
+    cu, cup = _host_i32(cu_seqlens)
+    lo, lop = _host_u8(layer_on, "layer_on")
+    hm, hmp = _host_u8(head_mask, "head_mask")
+    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    w = layer_weights(weights)
+    _check(load_library().svl_layer_forward(
+        ctypes.byref(cfg), int(layer), ctypes.byref(w), int(cu.shape[0] - 1), cup, lop, hmp, fmp,
+        _dev(resid, "resid"), _dev(ws, "ws"), ws.numel(), _stream(stream)))
+
+
+class LayerTable:
+    """Host array of svl_layer_weights for svl_prefill (built once, reused)."""
+
+    def __init__(self, layers: Sequence[Dict[str, torch.Tensor]]):
+        self.layers = list(layers)         # keeps the tensors alive
+        self.array = (svl_layer_weights * len(self.layers))(*[layer_weights(w) for w in self.layers])
+
+
+def svl_prefill(cfg: svl_config, layers, keep, scores: torch.Tensor, vision: torch.Tensor,
+                text: torch.Tensor, layer_mask, head_mask, ffn_mask, kept_idx: torch.Tensor,
+                resid: torch.Tensor, ws: torch.Tensor, stream=None, want_flops: bool = True):
+    """The whole budget-adapted prefill; returns (cu_seqlens, flops dict or None).
+
+    `layers` is a LayerTable or a list of per-layer weight dicts."""
+    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
+    kp, kpp = _host_i32(keep)
+    B, N = scores.shape
+    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
+    lm, lmp = _host_u8(layer_mask, "layer_mask")
+    hm, hmp = _host_u8(head_mask, "head_mask")
+    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    cu = np.zeros(B + 1, dtype=np.int32)
+    fl = svl_flops()
+    _check(load_library().svl_prefill(
+        ctypes.byref(cfg), table.array, ctypes.byref(batch), _dev(scores, "scores"),
+        _dev(vision, "vision"), _dev(text, "text"), lmp, hmp, fmp, _dev(kept_idx, "kept_idx"),
+        _dev(resid, "resid"), cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
+    return cu, (fl.as_dict() if want_flops else None)
+
+
+def svl_timing_enable(on: bool) -> None:
+    _check(load_library().svl_timing_enable(1 if on else 0))
+
+
+def svl_timing_read(kernel_class: str):
+    """(total ms, launches) recorded for a kernel class since the last read."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(load_library().svl_timing_read(KCLASS[kernel_class], ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

@@ -1,0 +1,511 @@
+// C ABI of libsvl: argument validation (all of it before anything is
+// enqueued), workspace layout, one host-to-device copy of the plan per call,
+// and the launch sequence of the prefill.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/svl.h"
+#include "plan.h"
+#include "svl_internal.h"
+
+namespace svl {
+namespace {
+
+thread_local std::string g_err;
+
+svl_status fail(svl_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+// ------------------------------------------------------------------ timing
+struct TimingRec {
+  int cls;
+  hipEvent_t a, b;
+};
+struct Timing {
+  std::mutex mu;
+  bool on = false;
+  std::vector<TimingRec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t take() {
+    if (!pool.empty()) { hipEvent_t e = pool.back(); pool.pop_back(); return e; }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Timing g_timing;
+
+template <class F>
+hipError_t timed(int cls, hipStream_t st, F&& f) {
+  if (!g_timing.on) return f();
+  hipEvent_t a, b;
+  {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    a = g_timing.take();
+    b = g_timing.take();
+  }
+  if (!a || !b) return f();
+  hipEventRecord(a, st);
+  hipError_t r = f();
+  hipEventRecord(b, st);
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.recs.push_back({cls, a, b});
+  return r;
+}
+
+enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_OTHER };
+
+// ------------------------------------------------------------------ validation
+svl_status check_config(const svl_config* c, bool for_kernels = true) {
+  if (!c) return fail(SVL_E_NULL, "config is NULL");
+  if (c->dtype != SVL_F32 && c->dtype != SVL_BF16) return fail(SVL_E_DTYPE, "unknown dtype %d", c->dtype);
+  if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->d_ffn <= 0 || c->n_groups <= 0)
+    return fail(SVL_E_SHAPE, "every size in the config must be positive");
+  if (c->n_heads % c->n_kv_heads) return fail(SVL_E_SHAPE, "n_heads %% n_kv_heads != 0");
+  if (c->head_dim % 2) return fail(SVL_E_SHAPE, "head_dim must be even (RoPE pairs)");
+  if (c->d_ffn % c->n_groups) return fail(SVL_E_SHAPE, "d_ffn %% n_groups != 0");
+  if (!(c->rms_eps >= 0.f)) return fail(SVL_E_VALUE, "rms_eps must be >= 0");
+  if (!(c->rope_theta > 0.f)) return fail(SVL_E_VALUE, "rope_theta must be > 0");
+  if (!for_kernels) return SVL_OK;
+  if (c->dtype == SVL_BF16) {
+    if (c->d_model % 64) return fail(SVL_E_SHAPE, "bf16 path: d_model %% 64 != 0");
+    if (c->head_dim != 64 && c->head_dim != 128)
+      return fail(SVL_E_SHAPE, "bf16 path: head_dim must be 64 or 128");
+    if ((c->d_ffn / c->n_groups) % 64) return fail(SVL_E_SHAPE, "bf16 path: d_ffn/n_groups %% 64 != 0");
+  } else {
+    if (c->d_model % 4) return fail(SVL_E_SHAPE, "f32 path: d_model %% 4 != 0");
+    if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+      return fail(SVL_E_SHAPE, "f32 path: head_dim must be 32, 64 or 128");
+  }
+  return SVL_OK;
+}
+
+svl_status check_mask(const uint8_t* m, int64_t n, const char* what) {
+  for (int64_t i = 0; i < n; ++i)
+    if (m[i] > 1) return fail(SVL_E_VALUE, "%s[%lld] = %u is not 0 or 1", what, (long long)i, m[i]);
+  return SVL_OK;
+}
+
+// ------------------------------------------------------------------ workspace
+struct WsLayout {
+  int64_t plan, rope, counters, partial, xn, qkv, attn_out, h, total;
+};
+
+WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
+  const int64_t es = c.dtype == SVL_BF16 ? 2 : 4;
+  const int64_t rows = R > 0 ? R : 1;
+  WsLayout L{};
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    int64_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  L.plan = take(plan_bytes_bound(c, B, c.n_layers));
+  L.rope = take(rows * (c.head_dim / 2) * 8);
+  L.counters = take((int64_t)kSplitTarget * 4);
+  L.partial = take(c.dtype == SVL_BF16 ? (int64_t)kSplitTarget * SPLITK_SLOT_FLOATS * 4 : 0);
+  L.xn = take(rows * c.d_model * es);
+  L.qkv = take(rows * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
+  L.attn_out = take(rows * (int64_t)c.n_heads * c.head_dim * es);
+  L.h = take(rows * (int64_t)c.d_ffn * es);
+  L.total = off;
+  return L;
+}
+
+// ------------------------------------------------------------------ execution
+struct Exec {
+  const svl_config& c;
+  hipStream_t st;
+  uint8_t* ws;
+  WsLayout L;
+  const Plan& plan;
+  float* resid;
+
+  template <class T>
+  const T* at(int64_t off) const { return reinterpret_cast<const T*>(ws + L.plan + off); }
+
+  hipError_t gemm(const GemmLaunch& g, const KChunk* chunks, const void* A, int lda, const void* W0,
+                  const void* W1, const void* W2, int ldw, int nb1, int nb2, void* out, int ldo,
+                  int epi, int cls) {
+    if (g.ntiles == 0) return hipSuccess;
+    GemmArgs a{};
+    a.groups = at<GemmGroup>(g.groups_off);
+    a.ngroups = g.ngroups;
+    a.ntiles = g.ntiles;
+    a.chunks = chunks;
+    a.A = A; a.lda = lda;
+    a.W0 = W0; a.W1 = W1; a.W2 = W2; a.ldw = ldw; a.nb1 = nb1; a.nb2 = nb2;
+    a.out = out; a.ldo = ldo;
+    a.partial = reinterpret_cast<float*>(ws + L.partial);
+    a.counters = reinterpret_cast<int32_t*>(ws + L.counters);
+    const bool bf16 = c.dtype == SVL_BF16;
+    return timed(cls, st, [&] { return bf16 ? launch_gemm_bf16(a, epi, st) : launch_gemm_f32(a, epi, st); });
+  }
+
+  hipError_t norm(const NormLaunch& n, const void* gain) {
+    if (n.nrows == 0) return hipSuccess;
+    NormArgs a{};
+    a.segs = at<Seg>(n.segs_off);
+    a.nsegs = n.nsegs;
+    a.nrows = n.nrows;
+    a.x = resid;
+    a.gain = gain;
+    a.out = ws + L.xn;
+    a.D = c.d_model;
+    a.eps = c.rms_eps;
+    return timed(K_NORM, st, [&] { return launch_rmsnorm(a, c.dtype, st); });
+  }
+
+  hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) {
+    const int A = c.n_heads, KV = c.n_kv_heads, d = c.head_dim, D = c.d_model, F = c.d_ffn;
+    const int qkv_w = (A + 2 * KV) * d;
+    const KChunk* chunks = at<KChunk>(P.chunks_off);
+    hipError_t e = hipSuccess;
+    if (P.norm_attn.nrows > 0) {
+      if ((e = norm(P.norm_attn, w.attn_norm)) != hipSuccess) return e;
+      if ((e = gemm(P.qkv, chunks, ws + L.xn, D, w.wq, w.wk, w.wv, D, A * d, (A + KV) * d,
+                    ws + L.qkv, qkv_w, EPI_STORE, K_QKV)) != hipSuccess)
+        return e;
+      AttnArgs a{};
+      a.groups = at<AttnGroup>(P.attn.groups_off);
+      a.ngroups = P.attn.ngroups;
+      a.ntiles = P.attn.ntiles;
+      a.head_table = at<int32_t>(P.attn.heads_off);
+      a.qkv = ws + L.qkv;
+      a.ldq = qkv_w;
+      a.n_heads = A;
+      a.n_kv_heads = KV;
+      a.out = ws + L.attn_out;
+      a.ldo = A * d;
+      a.rope = reinterpret_cast<const float2*>(ws + L.rope);
+      a.scale = 1.0f / std::sqrt((float)d);
+      e = timed(K_ATTN, st, [&] {
+        return c.dtype == SVL_BF16 ? launch_attn_bf16(a, d, st) : launch_attn_f32(a, d, st);
+      });
+      if (e != hipSuccess) return e;
+      if ((e = gemm(P.o, chunks, ws + L.attn_out, A * d, w.wo, nullptr, nullptr, A * d, 0, 0, resid,
+                    D, EPI_RESID, K_O)) != hipSuccess)
+        return e;
+    }
+    if (P.norm_ffn.nrows > 0) {
+      if ((e = norm(P.norm_ffn, w.ffn_norm)) != hipSuccess) return e;
+      if ((e = gemm(P.gu, chunks, ws + L.xn, D, w.w_gate, w.w_up, nullptr, D, 0, 0, ws + L.h, F,
+                    EPI_SWIGLU, K_GU)) != hipSuccess)
+        return e;
+      if ((e = gemm(P.down, chunks, ws + L.h, F, w.w_down, nullptr, nullptr, F, 0, 0, resid, D,
+                    EPI_RESID, K_DOWN)) != hipSuccess)
+        return e;
+    }
+    return hipSuccess;
+  }
+};
+
+thread_local Plan t_plan;
+
+svl_status hip_fail(hipError_t e, const char* where) {
+  return fail(SVL_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// Copies the plan image, clears the split-K counters and builds the RoPE table.
+svl_status stage(const Exec& ex, bool need_layers) {
+  if ((int64_t)ex.plan.image.size() > ex.L.rope - ex.L.plan)
+    return fail(SVL_E_SHAPE, "internal: plan image exceeds its workspace region");
+  hipError_t e = hipMemcpyAsync(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(),
+                                hipMemcpyHostToDevice, ex.st);
+  if (e != hipSuccess) return hip_fail(e, "plan upload");
+  if (need_layers) {
+    e = timed(K_OTHER, ex.st, [&] {
+      return launch_fill_i32(reinterpret_cast<int32_t*>(ex.ws + ex.L.counters), 0, kSplitTarget, ex.st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "counter clear");
+    e = timed(K_ROPE, ex.st, [&] {
+      return launch_rope_table(reinterpret_cast<float2*>(ex.ws + ex.L.rope), ex.plan.max_seq,
+                               ex.c.head_dim, ex.c.rope_theta, ex.st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "rope table");
+  }
+  return SVL_OK;
+}
+
+svl_status check_batch(const svl_config& c, const svl_batch* b) {
+  if (!b) return fail(SVL_E_NULL, "batch is NULL");
+  if (b->batch <= 0) return fail(SVL_E_SHAPE, "batch must be positive");
+  if (b->n_vision < 0 || b->n_text < 0) return fail(SVL_E_SHAPE, "negative token counts");
+  if (!b->keep) return fail(SVL_E_NULL, "keep is NULL");
+  int64_t total = 0;
+  for (int32_t i = 0; i < b->batch; ++i) {
+    if (b->keep[i] < 0 || b->keep[i] > b->n_vision)
+      return fail(SVL_E_VALUE, "keep[%d] = %d outside [0, %d]", i, b->keep[i], b->n_vision);
+    total += b->keep[i] + b->n_text;
+  }
+  if (total > INT32_MAX) return fail(SVL_E_SHAPE, "too many packed rows");
+  (void)c;
+  return SVL_OK;
+}
+
+svl_status check_ws(const svl_config& c, int32_t B, int32_t R, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(SVL_E_NULL, "workspace is NULL");
+  if (!aligned16(ws)) return fail(SVL_E_ALIGN, "workspace not 16-byte aligned");
+  const WsLayout L = ws_layout(c, B, R);
+  if ((int64_t)ws_bytes < L.total)
+    return fail(SVL_E_WORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)L.total);
+  return SVL_OK;
+}
+
+// Data pointers: scores, vision and kept_idx are needed when there are vision
+// tokens, text when there are text tokens, resid when there are packed rows.
+svl_status check_data(const svl_batch& b, int32_t R, const void* scores, const void* vision,
+                      const void* text, const void* kept_idx, const void* resid) {
+  if (b.n_vision > 0 && (!scores || !vision || !kept_idx))
+    return fail(SVL_E_NULL, "scores, vision and kept_idx are required when n_vision > 0");
+  if (b.n_text > 0 && !text) return fail(SVL_E_NULL, "text is required when n_text > 0");
+  if (R > 0 && !resid) return fail(SVL_E_NULL, "resid is required when there are packed rows");
+  for (const void* p : {scores, vision, text, kept_idx, resid})
+    if (p && !aligned16(p)) return fail(SVL_E_ALIGN, "device pointers must be 16-byte aligned");
+  return SVL_OK;
+}
+
+svl_status select_and_gather(const Exec& ex, const svl_batch& b, const float* scores,
+                             const void* vision, const void* text, int32_t* kept_idx, int32_t R) {
+  const int32_t* keep_dev = ex.at<int32_t>(ex.plan.keep_off);
+  const int32_t* cu_dev = ex.at<int32_t>(ex.plan.cu_off);
+  hipError_t e = timed(K_SELECT, ex.st, [&] {
+    return launch_select(scores, b.batch, b.n_vision, keep_dev, kept_idx, ex.st);
+  });
+  if (e != hipSuccess) return hip_fail(e, "select");
+  e = timed(K_GATHER, ex.st, [&] {
+    return launch_gather(kept_idx, keep_dev, cu_dev, b.batch, b.n_vision, b.n_text, ex.c.d_model, R,
+                         vision, text, ex.c.dtype, ex.resid, ex.st);
+  });
+  if (e != hipSuccess) return hip_fail(e, "gather");
+  return SVL_OK;
+}
+
+void closed_form(const svl_config& c, int64_t S, const uint8_t* hm, const uint8_t* fm, svl_flops* f) {
+  const int64_t D = c.d_model, d = c.head_dim, A = c.n_heads, KV = c.n_kv_heads, G = c.n_groups;
+  const int64_t rep = A / KV;
+  int64_t H = 0, K = 0, C = 0;
+  for (int64_t h = 0; h < A; ++h) H += hm[h] ? 1 : 0;
+  for (int64_t g = 0; g < KV; ++g) {
+    bool on = false;
+    for (int64_t h = g * rep; h < (g + 1) * rep; ++h) on = on || hm[h];
+    K += on ? 1 : 0;
+  }
+  if (fm) { for (int64_t j = 0; j < G; ++j) C += fm[j] ? c.d_ffn / G : 0; } else { C = c.d_ffn; }
+  f->q += 2 * S * D * d * H;
+  f->kv += 4 * S * D * d * K;
+  f->o += 2 * S * H * d * D;
+  f->attn += 2 * H * d * S * (S + 1);
+  f->ffn += 6 * S * D * C;
+}
+
+}  // namespace
+}  // namespace svl
+
+using namespace svl;
+
+extern "C" {
+
+const char* svl_last_error(void) { return g_err.c_str(); }
+
+int32_t svl_abi_version(void) { return SVL_ABI_VERSION; }
+
+size_t svl_workspace_bytes(const svl_config* cfg, int32_t batch, int32_t total_rows) {
+  if (check_config(cfg) != SVL_OK || batch <= 0 || total_rows < 0) return 0;
+  return (size_t)ws_layout(*cfg, batch, total_rows).total;
+}
+
+svl_status svl_count_flops(const svl_config* cfg, int32_t batch, const int32_t* seqlens,
+                           const uint8_t* layer_mask, const uint8_t* head_mask,
+                           const uint8_t* ffn_mask, svl_flops* out) {
+  svl_status s = check_config(cfg, false);
+  if (s != SVL_OK) return s;
+  if (batch <= 0) return fail(SVL_E_SHAPE, "batch must be positive");
+  if (!seqlens || !layer_mask || !head_mask || !out) return fail(SVL_E_NULL, "NULL argument");
+  const int64_t L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
+  if ((s = check_mask(layer_mask, batch * L, "layer_mask")) != SVL_OK) return s;
+  if ((s = check_mask(head_mask, batch * L * A, "head_mask")) != SVL_OK) return s;
+  if (ffn_mask && (s = check_mask(ffn_mask, batch * L * G, "ffn_mask")) != SVL_OK) return s;
+  svl_flops f{};
+  for (int64_t b = 0; b < batch; ++b) {
+    if (seqlens[b] < 0) return fail(SVL_E_VALUE, "negative sequence length");
+    for (int64_t l = 0; l < L; ++l)
+      if (layer_mask[b * L + l])
+        closed_form(*cfg, seqlens[b], head_mask + (b * L + l) * A,
+                    ffn_mask ? ffn_mask + (b * L + l) * G : nullptr, &f);
+  }
+  f.total = f.q + f.kv + f.o + f.attn + f.ffn;
+  *out = f;
+  return SVL_OK;
+}
+
+svl_status svl_select_tokens(const svl_config* cfg, const svl_batch* batch, const float* scores,
+                             const void* vision, const void* text, int32_t* kept_idx, float* resid,
+                             int32_t* cu_seqlens, void* ws, size_t ws_bytes, void* stream) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  if ((s = check_batch(*cfg, batch)) != SVL_OK) return s;
+  const int32_t B = batch->batch;
+  std::vector<int32_t> seq(B);
+  int32_t R = 0;
+  for (int32_t b = 0; b < B; ++b) { seq[b] = batch->keep[b] + batch->n_text; R += seq[b]; }
+  if (!cu_seqlens) return fail(SVL_E_NULL, "cu_seqlens is NULL");
+  if ((s = check_data(*batch, R, scores, vision, text, kept_idx, resid)) != SVL_OK) return s;
+  if ((s = check_ws(*cfg, B, R, ws, ws_bytes)) != SVL_OK) return s;
+  std::string err;
+  if (!build_plan(*cfg, B, batch->keep, seq.data(), 0, nullptr, &t_plan, &err))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  cu_seqlens[0] = 0;
+  for (int32_t b = 0; b < B; ++b) cu_seqlens[b + 1] = cu_seqlens[b] + seq[b];
+  Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), ws_layout(*cfg, B, R), t_plan, resid};
+  if ((s = stage(ex, false)) != SVL_OK) return s;
+  return select_and_gather(ex, *batch, scores, vision, text, kept_idx, R);
+}
+
+svl_status svl_layer_forward(const svl_config* cfg, int32_t layer, const svl_layer_weights* w,
+                             int32_t batch, const int32_t* cu_seqlens, const uint8_t* layer_on,
+                             const uint8_t* head_mask, const uint8_t* ffn_mask, float* resid,
+                             void* ws, size_t ws_bytes, void* stream) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  if (layer < 0 || layer >= cfg->n_layers) return fail(SVL_E_VALUE, "layer index out of range");
+  if (batch <= 0) return fail(SVL_E_SHAPE, "batch must be positive");
+  if (!w || !cu_seqlens || !layer_on || !head_mask || !resid) return fail(SVL_E_NULL, "NULL argument");
+  const void* wp[9] = {w->attn_norm, w->wq, w->wk, w->wv, w->wo, w->ffn_norm, w->w_gate, w->w_up, w->w_down};
+  for (const void* p : wp) {
+    if (!p) return fail(SVL_E_NULL, "NULL weight pointer");
+    if (!aligned16(p)) return fail(SVL_E_ALIGN, "weight pointers must be 16-byte aligned");
+  }
+  if (!aligned16(resid)) return fail(SVL_E_ALIGN, "resid must be 16-byte aligned");
+  if (cu_seqlens[0] != 0) return fail(SVL_E_VALUE, "cu_seqlens[0] must be 0");
+  std::vector<int32_t> seq(batch);
+  for (int32_t b = 0; b < batch; ++b) {
+    seq[b] = cu_seqlens[b + 1] - cu_seqlens[b];
+    if (seq[b] < 0) return fail(SVL_E_VALUE, "cu_seqlens must be non-decreasing");
+  }
+  const int32_t R = cu_seqlens[batch];
+  if ((s = check_mask(layer_on, batch, "layer_on")) != SVL_OK) return s;
+  if ((s = check_mask(head_mask, (int64_t)batch * cfg->n_heads, "head_mask")) != SVL_OK) return s;
+  if (ffn_mask && (s = check_mask(ffn_mask, (int64_t)batch * cfg->n_groups, "ffn_mask")) != SVL_OK)
+    return s;
+  if ((s = check_ws(*cfg, batch, R, ws, ws_bytes)) != SVL_OK) return s;
+  LayerMasks m{layer_on, head_mask, cfg->n_heads, ffn_mask, cfg->n_groups};
+  std::string err;
+  if (!build_plan(*cfg, batch, nullptr, seq.data(), 1, &m, &t_plan, &err))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), ws_layout(*cfg, batch, R), t_plan, resid};
+  if ((s = stage(ex, true)) != SVL_OK) return s;
+  hipError_t e = ex.layer(t_plan.layers[0], *w);
+  if (e != hipSuccess) return hip_fail(e, "layer launch");
+  return SVL_OK;
+}
+
+svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, const svl_batch* batch,
+                       const float* scores, const void* vision, const void* text,
+                       const uint8_t* layer_mask, const uint8_t* head_mask, const uint8_t* ffn_mask,
+                       int32_t* kept_idx, float* resid, int32_t* cu_seqlens, svl_flops* flops,
+                       void* ws, size_t ws_bytes, void* stream) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  if ((s = check_batch(*cfg, batch)) != SVL_OK) return s;
+  if (!layers || !layer_mask || !head_mask || !cu_seqlens) return fail(SVL_E_NULL, "NULL argument");
+  const int32_t B = batch->batch, L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
+  std::vector<int32_t> seq(B);
+  int32_t R = 0;
+  for (int32_t b = 0; b < B; ++b) { seq[b] = batch->keep[b] + batch->n_text; R += seq[b]; }
+  if ((s = check_data(*batch, R, scores, vision, text, kept_idx, resid)) != SVL_OK) return s;
+  for (int32_t l = 0; l < L; ++l) {
+    const svl_layer_weights& w = layers[l];
+    const void* wp[9] = {w.attn_norm, w.wq, w.wk, w.wv, w.wo, w.ffn_norm, w.w_gate, w.w_up, w.w_down};
+    for (const void* p : wp) {
+      if (!p) return fail(SVL_E_NULL, "NULL weight pointer in layer %d", l);
+      if (!aligned16(p)) return fail(SVL_E_ALIGN, "weight pointer of layer %d not 16-byte aligned", l);
+    }
+  }
+  if ((s = check_mask(layer_mask, (int64_t)B * L, "layer_mask")) != SVL_OK) return s;
+  if ((s = check_mask(head_mask, (int64_t)B * L * A, "head_mask")) != SVL_OK) return s;
+  if (ffn_mask && (s = check_mask(ffn_mask, (int64_t)B * L * G, "ffn_mask")) != SVL_OK) return s;
+  if ((s = check_ws(*cfg, B, R, ws, ws_bytes)) != SVL_OK) return s;
+  std::vector<LayerMasks> masks(L);
+  for (int32_t l = 0; l < L; ++l) {
+    // host masks are [B][L][...]: row b of layer l starts at (b*L + l) * width
+    masks[l].layer_on = nullptr;
+    masks[l].head_mask = head_mask + (int64_t)l * A;
+    masks[l].head_stride = (int64_t)L * A;
+    masks[l].ffn_mask = ffn_mask ? ffn_mask + (int64_t)l * G : nullptr;
+    masks[l].ffn_stride = (int64_t)L * G;
+  }
+  std::vector<uint8_t> lon((size_t)L * B);
+  for (int32_t l = 0; l < L; ++l) {
+    for (int32_t b = 0; b < B; ++b) lon[(size_t)l * B + b] = layer_mask[(int64_t)b * L + l];
+    masks[l].layer_on = lon.data() + (size_t)l * B;
+  }
+  std::string err;
+  if (!build_plan(*cfg, B, batch->keep, seq.data(), L, masks.data(), &t_plan, &err))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  cu_seqlens[0] = 0;
+  for (int32_t b = 0; b < B; ++b) cu_seqlens[b + 1] = cu_seqlens[b] + seq[b];
+  if (flops) {
+    svl_status fs = svl_count_flops(cfg, B, seq.data(), layer_mask, head_mask, ffn_mask, flops);
+    if (fs != SVL_OK) return fs;
+  }
+  Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), ws_layout(*cfg, B, R), t_plan, resid};
+  if ((s = stage(ex, true)) != SVL_OK) return s;
+  if ((s = select_and_gather(ex, *batch, scores, vision, text, kept_idx, R)) != SVL_OK) return s;
+  for (int32_t l = 0; l < L; ++l) {
+    hipError_t e = ex.layer(t_plan.layers[l], layers[l]);
+    if (e != hipSuccess) return hip_fail(e, "layer launch");
+  }
+  return SVL_OK;
+}
+
+svl_status svl_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.on = on != 0;
+  return SVL_OK;
+}
+
+svl_status svl_timing_read(int32_t kernel_class, double* total_ms, int64_t* launches) {
+  if (kernel_class < 0 || kernel_class >= SVL_KCLASS_COUNT) return fail(SVL_E_VALUE, "bad kernel class");
+  if (!total_ms || !launches) return fail(SVL_E_NULL, "NULL argument");
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double sum = 0.0;
+  int64_t n = 0;
+  std::vector<TimingRec> keep;
+  for (auto& r : g_timing.recs) {
+    if (r.cls != kernel_class) { keep.push_back(r); continue; }
+    hipError_t e = hipEventSynchronize(r.b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return hip_fail(e, "timing read");
+    sum += ms;
+    ++n;
+    g_timing.pool.push_back(r.a);
+    g_timing.pool.push_back(r.b);
+  }
+  g_timing.recs.swap(keep);
+  *total_ms = sum;
+  *launches = n;
+  return SVL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,168 @@
+// Token selection (top-k by score, kept indices ascending) and the packing of
+// kept vision rows and text rows into the float32 residual stream.
+//
+// Selection, one workgroup per sample:
+//   1. every score is mapped to an unsigned key whose order is the required
+//      order: larger score -> larger key, -0 and +0 -> one key, NaN -> 0
+//      (below -inf, whose key is 0x007fffff);
+//   2. a 4-pass radix select (8 bits per pass, 256-bin LDS histogram) finds
+//      the k-th largest key T and how many keys equal to T are kept;
+//   3. one ordered pass over the indices keeps key > T, and key == T while
+//      fewer than the needed number of equal keys have been seen (ties go to
+//      the lower index); wave ballots give the prefix counts, so the kept
+//      indices come out in ascending order.
+// Gather: one workgroup per packed row, 16-byte loads, exact widening of
+// bf16 to float32.
+#include "svl_internal.h"
+#include "device_util.h"
+
+namespace svl {
+namespace {
+
+constexpr int NT = 256;
+
+__device__ __forceinline__ uint32_t score_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;  // NaN
+  if (u == 0x80000000u) u = 0u;                      // -0 -> +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive count of `p` over the workgroup's threads in thread order, and
+// the total.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int block_excl_count(bool p, int* s_wave, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const unsigned long long m = __ballot(p);
+  const int below = __popcll(m & ((1ull << lane) - 1ull));
+  if (lane == 0) s_wave[w] = __popcll(m);
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) {
+    off += (i < w) ? s_wave[i] : 0;
+    tot += s_wave[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return off + below;
+}
+
+__global__ __launch_bounds__(NT) void select_kernel(const float* scores, int N, const int32_t* keep,
+                                                    int32_t* kept_idx) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_digit, s_remaining;
+  __shared__ int s_wave[NT / 64];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const float* s = scores + (size_t)b * N;
+  int32_t* out = kept_idx + (size_t)b * N;
+  const int k = keep[b];
+
+  if (k > 0 && k < N) {
+    uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      hist[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < N; i += NT) {
+        const uint32_t key = score_key(s[i]);
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t cum = 0;
+        int d = 255;
+        for (; d > 0; --d) {
+          if (cum + hist[d] >= remaining) break;
+          cum += hist[d];
+        }
+        s_digit = (uint32_t)d;
+        s_remaining = remaining - cum;
+      }
+      __syncthreads();
+      prefix |= s_digit << shift;
+      mask |= 255u << shift;
+      remaining = s_remaining;
+      __syncthreads();
+    }
+    const uint32_t T = prefix;
+    const int need_eq = (int)remaining;
+    int eq_seen = 0, written = 0;
+    for (int c0 = 0; c0 < N; c0 += NT) {
+      const int i = c0 + tid;
+      const uint32_t key = i < N ? score_key(s[i]) : 0u;
+      const bool gt = i < N && key > T;
+      const bool eq = i < N && key == T;
+      int eq_tot, keep_tot;
+      const int eq_rank = eq_seen + block_excl_count(eq, s_wave, &eq_tot);
+      const bool kp = gt || (eq && eq_rank < need_eq);
+      const int pos = written + block_excl_count(kp, s_wave, &keep_tot);
+      if (kp) out[pos] = i;
+      eq_seen += eq_tot;
+      written += keep_tot;
+    }
+  } else if (k == N) {
+    for (int i = tid; i < N; i += NT) out[i] = i;
+  }
+  for (int i = k + tid; i < N; i += NT) out[i] = -1;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(NT) void gather_kernel(const int32_t* kept_idx, const int32_t* keep,
+                                                    const int32_t* cu, int B, int N, int T, int D,
+                                                    const void* vision, const void* text,
+                                                    float* resid) {
+  const int r = blockIdx.x;
+  int lo = 0, hi = B - 1;   // sample b with cu[b] <= r < cu[b+1]
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo, i = r - cu[b], k = keep[b];
+  size_t src_row;
+  const void* src;
+  if (i < k) {
+    src = vision;
+    src_row = (size_t)b * N + min(max(kept_idx[(size_t)b * N + i], 0), N - 1);
+  }
+  else { src = text; src_row = (size_t)b * T + (i - k); }
+  float* dst = resid + (size_t)r * D;
+  if constexpr (BF16) {
+    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(src) + src_row * D);
+    for (int c = threadIdx.x; c < D / 8; c += NT) {
+      const uint4 v = p[c];
+      float4 f0 = make_float4(bf16_bits_to_f32(v.x & 0xffffu), bf16_bits_to_f32(v.x >> 16),
+                              bf16_bits_to_f32(v.y & 0xffffu), bf16_bits_to_f32(v.y >> 16));
+      float4 f1 = make_float4(bf16_bits_to_f32(v.z & 0xffffu), bf16_bits_to_f32(v.z >> 16),
+                              bf16_bits_to_f32(v.w & 0xffffu), bf16_bits_to_f32(v.w >> 16));
+      reinterpret_cast<float4*>(dst)[2 * c] = f0;
+      reinterpret_cast<float4*>(dst)[2 * c + 1] = f1;
+    }
+  } else {
+    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(src) + src_row * D);
+    for (int c = threadIdx.x; c < D / 4; c += NT) reinterpret_cast<float4*>(dst)[c] = p[c];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* scores, int32_t B, int32_t N, const int32_t* keep_dev,
+                         int32_t* kept_idx, hipStream_t st) {
+  if (B <= 0 || N <= 0) return hipSuccess;
+  select_kernel<<<B, NT, 0, st>>>(scores, N, keep_dev, kept_idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const int32_t* cu_dev,
+                         int32_t B, int32_t N, int32_t T, int32_t D, int32_t total_rows,
+                         const void* vision, const void* text, int32_t dtype, float* resid,
+                         hipStream_t st) {
+  if (total_rows <= 0) return hipSuccess;
+  if (dtype == SVL_BF16)
+    gather_kernel<true><<<total_rows, NT, 0, st>>>(kept_idx, keep_dev, cu_dev, B, N, T, D, vision,
+                                                    text, resid);
+  else
+    gather_kernel<false><<<total_rows, NT, 0, st>>>(kept_idx, keep_dev, cu_dev, B, N, T, D, vision,
+                                                     text, resid);
+  return hipGetLastError();
+}
+
+}  // namespace svl

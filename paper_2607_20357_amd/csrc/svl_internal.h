@@ -1,0 +1,77 @@
+// Internal declarations of libsvl: plan descriptors shared by the host
+// planner and the kernels, kernel launchers, and small device helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <stdint.h>
+
+#include "../../include/svl.h"
+#include "plan_types.h"
+
+namespace svl {
+
+enum Epilogue : int32_t {
+  EPI_STORE = 0,   // out[row][col] = acc (activation dtype)
+  EPI_RESID = 1,   // resid[row][col] += acc (float32)
+  EPI_SWIGLU = 2,  // out[row][ch] = silu(gate) * up, gate/up tiles paired
+};
+
+struct GemmArgs {
+  const GemmGroup* groups;
+  int32_t ngroups, ntiles;
+  const KChunk* chunks;
+  const void* A;       // activations [rows][lda]
+  int32_t lda;
+  const void* W0;      // weight row sources ([out][in] layout, row stride ldw)
+  const void* W1;
+  const void* W2;
+  int32_t ldw;
+  int32_t nb1, nb2;    // EPI_STORE: columns < nb1 -> W0, < nb2 -> W1, else W2
+  void* out;           // output / residual, row stride ldo
+  int32_t ldo;
+  float* partial;      // split-K partial tiles
+  int32_t* counters;   // split-K arrival counters (zero between launches)
+};
+
+struct AttnArgs {
+  const AttnGroup* groups;
+  int32_t ngroups, ntiles;
+  const int32_t* head_table;
+  const void* qkv;     // [rows][(A + 2 KV) d]: Q heads, then K heads, then V heads
+  int32_t ldq;         // row stride of qkv
+  int32_t n_heads, n_kv_heads;
+  void* out;           // [rows][A d]
+  int32_t ldo;
+  const float2* rope;  // (cos, sin)[pos][d/2]
+  float scale;         // 1/sqrt(d)
+};
+
+struct NormArgs {
+  const Seg* segs;
+  int32_t nsegs, nrows;
+  const float* x;      // residual [rows][D]
+  const void* gain;    // [D], weight dtype
+  void* out;           // [rows][D], activation dtype
+  int32_t D;
+  float eps;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (each returns hipSuccess or the launch error).
+hipError_t launch_select(const float* scores, int32_t B, int32_t N, const int32_t* keep_dev,
+                         int32_t* kept_idx, hipStream_t st);
+hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const int32_t* cu_dev,
+                         int32_t B, int32_t N, int32_t T, int32_t D, int32_t total_rows,
+                         const void* vision, const void* text, int32_t dtype, float* resid,
+                         hipStream_t st);
+hipError_t launch_rmsnorm(const NormArgs& a, int32_t dtype, hipStream_t st);
+hipError_t launch_gemm_bf16(const GemmArgs& a, int32_t epi, hipStream_t st);
+hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
+hipError_t launch_attn_bf16(const AttnArgs& a, int32_t head_dim, hipStream_t st);
+hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);
+hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, float theta,
+                             hipStream_t st);
+hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t st);
+
+}  // namespace svl

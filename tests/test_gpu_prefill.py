@@ -1,0 +1,210 @@
+"""GPU parity of the whole budget-adapted prefill (svl_prefill) and of one
+layer (svl_layer_forward) against the CPU oracle.
+
+Bars: kept indices and cu_seqlens bit-exact; FLOP count exact; hidden
+states within max relative error (per sample, max|gpu - oracle| / max|oracle|)
+1e-4 for float32 workloads and 2e-2 for bf16 workloads (oracle in float64)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_20357_amd as svl
+import workloads as W
+from gpu_helpers import gpu_prefill, host_layer, oracle_prefill, rel_err_per_sample, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_prefill(w, seed=0, samples_for_oracle=None):
+    print(f"prefill {w.name} seed={seed}", flush=True)
+    inp = W.draw_inputs(w, seed, device="cuda")
+    layers = [W.draw_layer_weights(w, l, seed, device="cuda") for l in range(w.shape.n_layers)]
+    kept, cu, resid, flops = gpu_prefill(w, inp, layers)
+    ref = oracle_prefill(w, inp, layers, samples_for_oracle)
+    samples = list(range(w.batch)) if samples_for_oracle is None else list(samples_for_oracle)
+    for j, b in enumerate(samples):
+        np.testing.assert_array_equal(kept[b], ref.kept_idx[j])
+        assert cu[b + 1] - cu[b] == ref.cu_seqlens[j + 1] - ref.cu_seqlens[j]
+    rows = np.concatenate([np.arange(cu[b], cu[b + 1]) for b in samples])
+    errs = rel_err_per_sample(resid[rows], ref.resid, ref.cu_seqlens)
+    print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+    if samples_for_oracle is None:
+        assert flops["total"] == ref.flops.total
+        for k in ("q", "kv", "o", "attn", "ffn"):
+            assert flops[k] == getattr(ref.flops, k), k
+    return errs
+
+
+def test_prefill_tiny_f32():
+    _check_prefill(W.get_workload("tiny_f32"))
+
+
+def test_prefill_tiny_f32_other_seeds():
+    for seed in (1, 2):
+        _check_prefill(W.get_workload("tiny_f32"), seed)
+
+
+def test_prefill_llava7b_headline_full_size():
+    """The benchmarked workload at its real shape: 32 layers, d 4096, keep 144."""
+    _check_prefill(W.get_workload("llava7b_b1_keep25"))
+
+
+def test_prefill_scaled_ragged_batch():
+    w = W.scaled(W.get_workload("llava7b_b8_ragged"), n_layers=6, d_model=1024, n_heads=8,
+                 n_kv_heads=8, d_ffn=2816, name="ragged_b8_small")
+    _check_prefill(w)
+
+
+def test_prefill_scaled_gqa():
+    w = W.scaled(W.get_workload("gqa7b_hires_b2"), n_layers=4, d_model=1024, n_heads=8,
+                 n_kv_heads=4, d_ffn=2048, layers_skipped=1, name="gqa_small")
+    _check_prefill(w)
+
+
+def test_prefill_scaled_video():
+    w = W.scaled(W.get_workload("llava13b_video_b4"), n_layers=4, d_model=1024, n_heads=8,
+                 n_kv_heads=8, d_ffn=2048, layers_skipped=1, name="video_small")
+    _check_prefill(w)
+
+
+def _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask, seed=3):
+    dev = "cuda"
+    cfg = svl.make_config(shape)
+    R = int(np.sum(seqlens))
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+    g = torch.Generator(device=dev).manual_seed(seed)
+    x0 = torch.randn(R, shape.d_model, generator=g, device=dev)
+    wl = W.Workload(name="layer", shape=shape, batch=len(seqlens), n_vision=0, n_text=0)
+    weights = W.draw_layer_weights(wl, 0, seed, device=dev)
+    resid = x0.clone()
+    ws = svl.alloc_workspace(cfg, len(seqlens), R, dev)
+    svl.svl_layer_forward(cfg, 0, weights, cu, layer_on, head_mask, ffn_mask, resid, ws)
+    torch.cuda.synchronize()
+    got = resid.cpu().numpy()
+    x = x0.cpu().numpy().astype(np.float64)
+    Wh = host_layer(weights)
+    ref = np.empty_like(x)
+    for b in range(len(seqlens)):
+        rows = slice(cu[b], cu[b + 1])
+        if layer_on[b]:
+            ref[rows] = oracle.decoder_layer(x[rows], Wh, shape, head_mask[b],
+                                             None if ffn_mask is None else ffn_mask[b])
+        else:
+            ref[rows] = x[rows]
+            # a bypassed sample's rows are not touched at all
+            np.testing.assert_array_equal(got[rows], x0.cpu().numpy()[rows])
+    return rel_err_per_sample(got, ref, cu)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_masks_and_edges(dtype):
+    """Per-head masks (not only whole groups), FFN coupled / ungated / all
+    off, a bypassed sample, an empty sample and a one-row sample."""
+    hd = 64
+    shape = W.ModelShape(n_layers=1, d_model=512, n_heads=8, n_kv_heads=4, head_dim=hd,
+                         d_ffn=1024, n_groups=4, dtype=dtype)
+    seqlens = np.array([70, 0, 1, 129, 200], np.int32)
+    B = len(seqlens)
+    rng = np.random.default_rng(0)
+    head_mask = (rng.random((B, 8)) > 0.4).astype(np.uint8)
+    head_mask[3] = 0                 # attention block off entirely
+    head_mask[4] = 1
+    ffn_mask = (rng.random((B, 4)) > 0.4).astype(np.uint8)
+    ffn_mask[4] = 0                  # FFN block off entirely
+    layer_on = np.array([1, 1, 1, 1, 0], np.uint8)
+    tol = tol_for(shape)
+    for fm in (ffn_mask, None):
+        print(f"layer edges dtype={dtype} ffn={'coupled' if fm is not None else 'ungated'}",
+              flush=True)
+        errs = _layer_case(shape, seqlens, layer_on, head_mask, fm)
+        assert max(errs) <= tol, errs
+
+
+@pytest.mark.parametrize("name", ["llava7b_b1_keep25", "llava7b_b8_ragged", "gqa7b_hires_b2",
+                                  "llava13b_video_b4"])
+def test_layer_full_size(name):
+    """One decoder layer at each workload's real width, sequence lengths and
+    masks (first non-prefix layer of the seed-0 draw)."""
+    w = W.get_workload(name)
+    keep, lm, hm, fm = W.draw_masks(w, 0)
+    l = w.shape.prefix
+    seqlens = (keep + w.n_text).astype(np.int32)
+    print(f"layer full size {name} seqlens={seqlens.tolist()}", flush=True)
+    errs = _layer_case(w.shape, seqlens, lm[:, l], hm[:, l], None if fm is None else fm[:, l])
+    print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+
+
+def test_prefill_deterministic_and_flops():
+    w = W.get_workload("llava7b_b8_ragged")
+    w = W.scaled(w, n_layers=3, d_model=512, n_heads=4, n_kv_heads=4, d_ffn=1024, name="det")
+    inp = W.draw_inputs(w, 4, device="cuda")
+    layers = [W.draw_layer_weights(w, l, 4, device="cuda") for l in range(w.shape.n_layers)]
+    a = gpu_prefill(w, inp, layers)
+    b = gpu_prefill(w, inp, layers)
+    np.testing.assert_array_equal(a[2], b[2])
+    cfg = svl.make_config(w.shape)
+    f = svl.svl_count_flops(cfg, inp.keep + w.n_text, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    assert f == a[3]
+
+
+def test_prefill_edge_batches():
+    """keep = 0, keep = N, no text tokens, every layer skipped for a sample,
+    all heads and FFN slices off in a layer (alpha = 0)."""
+    base = W.Workload(name="edges", shape=W.ModelShape(n_layers=3, d_model=256, n_heads=4,
+                                                        n_kv_heads=2, head_dim=64, d_ffn=512,
+                                                        n_groups=2, dtype="bf16"),
+                      batch=4, n_vision=40, n_text=0, keep_ratio=0.5)
+    for T in (0, 5):
+        w = W.Workload(**{**base.__dict__, "n_text": T})
+        inp = W.draw_inputs(w, 1, device="cuda")
+        inp.keep[:] = [0, 40, 13, 1]
+        inp.layer_mask[2, :] = 0
+        inp.head_mask[1, 1, :] = 0
+        inp.ffn_mask[1, 1, :] = 0
+        layers = [W.draw_layer_weights(w, l, 1, device="cuda") for l in range(3)]
+        print(f"edge batch T={T} keep={inp.keep.tolist()}", flush=True)
+        kept, cu, resid, flops = gpu_prefill(w, inp, layers)
+        ref = oracle_prefill(w, inp, layers)
+        np.testing.assert_array_equal(kept, ref.kept_idx)
+        np.testing.assert_array_equal(cu, ref.cu_seqlens)
+        errs = rel_err_per_sample(resid, ref.resid, cu)
+        assert max(errs) <= tol_for(w.shape), errs
+        # the sample that skips every layer is its packed input, exactly
+        rows = slice(cu[2], cu[3])
+        np.testing.assert_array_equal(resid[rows], ref.resid[rows].astype(np.float32))
+        assert flops["total"] == ref.flops.total
+
+
+def test_gated_weights_are_never_read():
+    """NaN in every weight row / column of inactive heads and FFN slices, and
+    in every weight of a layer no sample runs, leaves the output bit-identical."""
+    w = W.scaled(W.get_workload("llava7b_b1_keep25"), n_layers=4, d_model=512, n_heads=4,
+                 n_kv_heads=4, d_ffn=1024, layers_skipped=1, name="poison")
+    inp = W.draw_inputs(w, 2, device="cuda")
+    layers = [W.draw_layer_weights(w, l, 2, device="cuda") for l in range(4)]
+    clean = gpu_prefill(w, inp, layers)[2]
+    d, F, G = w.shape.head_dim, w.shape.d_ffn, w.shape.n_groups
+    poisoned = []
+    for l, lw in enumerate(layers):
+        lw = {k: v.clone() for k, v in lw.items()}
+        if not inp.layer_mask[0, l]:
+            for v in lw.values():
+                v.fill_(float("nan"))
+        else:
+            for h in range(w.shape.n_heads):
+                if not inp.head_mask[0, l, h]:
+                    for n in ("wq", "wk", "wv"):
+                        lw[n][h * d:(h + 1) * d] = float("nan")
+                    lw["wo"][:, h * d:(h + 1) * d] = float("nan")
+            for j in range(G):
+                if not inp.ffn_mask[0, l, j]:
+                    sl = slice(j * F // G, (j + 1) * F // G)
+                    lw["w_gate"][sl] = float("nan")
+                    lw["w_up"][sl] = float("nan")
+                    lw["w_down"][:, sl] = float("nan")
+        poisoned.append(lw)
+    got = gpu_prefill(w, inp, poisoned)[2]
+    np.testing.assert_array_equal(got, clean)
