@@ -1,0 +1,236 @@
+"""Benchmark of the budget-adapted prefill on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = one svl_prefill call over one batch of seeded synthetic inputs
+already resident in HBM: top-k selection and packing of the vision tokens,
+then every decoder layer under the layer / head / FFN masks.  The default
+workload is the LLaVA-1.5-7B-shaped batch-1 prefill with keep ratio 0.25
+(576 vision + 64 text tokens, 144 kept; 8 of 32 heads and the matching FFN
+slice off per layer; 8 of 32 layers skipped; bf16 weights and activations,
+float32 accumulation and residual).
+
+Prints one JSON line.  `value` is effective prefill tokens/s = B*(N+T) per
+step time (tokens the prefill stands for, before pruning).  The `roofline`
+object covers the dominant kernel (the gate/up GEMM), timed with HIP events
+recorded by the library on the launch stream in a second pass of the same
+steps; `cpu_baseline` times the CPU oracle on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default=None)
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-layers", type=int, default=3,
+                   help="executed layers the CPU-baseline sample runs")
+    return p.parse_args()
+
+
+def gemm_bytes(shape, seqlens, layer_mask, head_mask, ffn_mask):
+    """Algorithmic HBM bytes of each GEMM class over one step: active weight
+    bytes + activation operand + output, bf16 (2 B) activations/weights and
+    float32 residual read-modify-write for the output / down projections."""
+    D, A, KV, d, F, G = (shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+                         shape.d_ffn, shape.n_groups)
+    rep = A // KV
+    out = {"qkv": 0, "o": 0, "gu": 0, "down": 0}
+    launches = {"qkv": 0, "o": 0, "gu": 0, "down": 0}
+    B, L = layer_mask.shape
+    for l in range(L):
+        rows_a = rows_f = 0
+        qkv_cols = o_k = f_ch = 0
+        for b in range(B):
+            if not layer_mask[b, l] or seqlens[b] == 0:
+                continue
+            hm = head_mask[b, l]
+            H = int(hm.sum())
+            K = sum(int(hm[g * rep:(g + 1) * rep].any()) for g in range(KV))
+            C = F if ffn_mask is None else int(ffn_mask[b, l].sum()) * (F // G)
+            if H:
+                rows_a += seqlens[b]
+                # weights read once per launch when every sample shares the
+                # mask (the headline case); per sample otherwise
+                qkv_cols = max(qkv_cols, (H + 2 * K) * d)
+                o_k = max(o_k, H * d)
+            if C:
+                rows_f += seqlens[b]
+                f_ch = max(f_ch, C)
+        if rows_a:
+            out["qkv"] += qkv_cols * D * 2 + rows_a * D * 2 + rows_a * qkv_cols * 2
+            out["o"] += D * o_k * 2 + rows_a * o_k * 2 + rows_a * D * 8
+            launches["qkv"] += 1
+            launches["o"] += 1
+        if rows_f:
+            out["gu"] += 2 * f_ch * D * 2 + rows_f * D * 2 + rows_f * f_ch * 2
+            out["down"] += D * f_ch * 2 + rows_f * f_ch * 2 + rows_f * D * 8
+            launches["gu"] += 1
+            launches["down"] += 1
+    return out, launches
+
+
+def cpu_baseline(w, inp, layers, n_exec_layers):
+    """The CPU oracle on the first `n_exec_layers` executed layers of the same
+    inputs (selection and packing included); the rate is scaled to the whole
+    prefill by the executed-layer count."""
+    import oracle
+    import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    B = w.batch
+    executed = [l for l in range(w.shape.n_layers) if inp.layer_mask[:, l].any()]
+    sample = executed[:n_exec_layers]
+    host = {}
+    for l in sample:
+        host[l] = {k: W.as_f32(v) for k, v in layers[l].items()}
+    vis, txt = W.as_f32(inp.vision), W.as_f32(inp.text)
+    t0 = time.perf_counter()
+    oracle.prefill(w.shape, lambda l: host[l], inp.scores, inp.keep, vis, txt, inp.layer_mask,
+                   inp.head_mask, inp.ffn_mask, layers=sample)
+    dt = time.perf_counter() - t0
+    est = dt * len(executed) / max(1, len(sample))
+    tokens = B * (w.n_vision + w.n_text)
+    return {"value": tokens / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(sample)} of {len(executed)} executed layers (float64 numpy oracle, "
+                      f"selection and packing included), {dt:.1f} s, rate scaled by "
+                      f"{len(executed)}/{len(sample)}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; multi-GPU runs are not part of "
+                                   "it (samples would shard data-parallel, see DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    w = W.get_workload(args.workload or W.HEADLINE)
+    shape = w.shape
+    print(f"# workload {w.name}: {w.description}", file=sys.stderr, flush=True)
+    inp = W.draw_inputs(w, args.seed, device=dev)
+    layers = [W.draw_layer_weights(w, l, args.seed, device=dev) for l in range(shape.n_layers)]
+    table = svl.LayerTable(layers)
+    cfg = svl.make_config(shape)
+    B, N = inp.scores.shape
+    seqlens = (inp.keep + w.n_text).astype(np.int64)
+    R = int(seqlens.sum())
+    scores = torch.from_numpy(inp.scores).to(dev)
+    kept = torch.empty((B, N), dtype=torch.int32, device=dev)
+    resid = torch.empty((R, shape.d_model), dtype=torch.float32, device=dev)
+    ws = svl.alloc_workspace(cfg, B, R, dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
+                        inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
+                        want_flops=False)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+    print(f"# timed {args.steps} steps: {ms:.4f} ms/step (wall {1e3 * t_wall / args.steps:.4f})",
+          file=sys.stderr, flush=True)
+
+    # second pass, same steps, every launch bracketed by HIP events on `stream`
+    svl.svl_timing_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    svl.svl_timing_enable(False)
+    ktime = {k: svl.svl_timing_read(k) for k in svl.KCLASS}
+
+    flops = svl.svl_count_flops(cfg, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
+    gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / args.steps
+    attn_ms = ktime["attention"][0] / args.steps
+    tokens = B * (w.n_vision + w.n_text)
+    value = tokens / (ms * 1e-3)
+
+    bytes_, launches = gemm_bytes(shape, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    gu_ms, gu_n = ktime["gemm_gate_up"]
+    gu_avg_ms = gu_ms / max(1, gu_n)
+    gu_bytes_per_launch = bytes_["gu"] / max(1, launches["gu"])
+    achieved = gu_bytes_per_launch / (gu_avg_ms * 1e-3) / 1e9
+    per_kernel = {k: {"ms_per_step": v[0] / args.steps, "launches_per_step": v[1] / args.steps}
+                  for k, v in ktime.items() if v[1]}
+
+    result = {
+        "metric": "effective prefill tokens/s + MFMA util (% peak), 7B-shaped, keep 0.25",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if shape.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "n_vision": w.n_vision, "n_text": w.n_text,
+                   "keep": [int(k) for k in inp.keep], "kept_tokens": R,
+                   "layers_executed_per_sample": [int(x) for x in inp.layer_mask.sum(1)],
+                   "n_layers": shape.n_layers, "d_model": shape.d_model,
+                   "heads": shape.n_heads, "kv_heads": shape.n_kv_heads,
+                   "d_ffn": shape.d_ffn, "parallelism": "none (1 GPU)"},
+        "kept_tokens_per_s": round(R / (ms * 1e-3), 1),
+        "executed_tflops": round(flops["total"] / (ms * 1e-3) / 1e12, 2),
+        "executed_flops_per_step": flops["total"],
+        "mfma_util_gemm_pct": round(100 * gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2),
+        "mfma_util_attn_pct": round(100 * flops["attn"] / (attn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 3)
+        if attn_ms > 0 else None,
+        "gemm_ms_per_step": round(gemm_ms, 4),
+        "per_kernel": per_kernel,
+        "roofline": {
+            "kernel": "gemm_bf16_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "avg_launch_ms": round(gu_avg_ms, 5),
+            "algorithmic_bytes_per_launch": int(gu_bytes_per_launch),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, inp, layers, args.cpu_layers)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

@@ -145,7 +145,7 @@ struct Exec {
 
   hipError_t gemm(const GemmLaunch& g, const KChunk* chunks, const void* A, int lda, const void* W0,
                   const void* W1, const void* W2, int ldw, int nb1, int nb2, void* out, int ldo,
-                  int epi, int cls) {
+                  int epi, int cls) const {
     if (g.ntiles == 0) return hipSuccess;
     GemmArgs a{};
     a.groups = at<GemmGroup>(g.groups_off);
@@ -157,11 +157,14 @@ struct Exec {
     a.out = out; a.ldo = ldo;
     a.partial = reinterpret_cast<float*>(ws + L.partial);
     a.counters = reinterpret_cast<int32_t*>(ws + L.counters);
+    a.rope = reinterpret_cast<const float2*>(ws + L.rope);
+    a.head_dim = c.head_dim;
+    a.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim;
     const bool bf16 = c.dtype == SVL_BF16;
     return timed(cls, st, [&] { return bf16 ? launch_gemm_bf16(a, epi, st) : launch_gemm_f32(a, epi, st); });
   }
 
-  hipError_t norm(const NormLaunch& n, const void* gain) {
+  hipError_t norm(const NormLaunch& n, const void* gain) const {
     if (n.nrows == 0) return hipSuccess;
     NormArgs a{};
     a.segs = at<Seg>(n.segs_off);
@@ -175,7 +178,7 @@ struct Exec {
     return timed(K_NORM, st, [&] { return launch_rmsnorm(a, c.dtype, st); });
   }
 
-  hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) {
+  hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) const {
     const int A = c.n_heads, KV = c.n_kv_heads, d = c.head_dim, D = c.d_model, F = c.d_ffn;
     const int qkv_w = (A + 2 * KV) * d;
     const KChunk* chunks = at<KChunk>(P.chunks_off);
@@ -183,7 +186,8 @@ struct Exec {
     if (P.norm_attn.nrows > 0) {
       if ((e = norm(P.norm_attn, w.attn_norm)) != hipSuccess) return e;
       if ((e = gemm(P.qkv, chunks, ws + L.xn, D, w.wq, w.wk, w.wv, D, A * d, (A + KV) * d,
-                    ws + L.qkv, qkv_w, EPI_STORE, K_QKV)) != hipSuccess)
+                    ws + L.qkv, qkv_w, c.dtype == SVL_BF16 ? EPI_QKV : EPI_STORE, K_QKV)) !=
+          hipSuccess)
         return e;
       AttnArgs a{};
       a.groups = at<AttnGroup>(P.attn.groups_off);

@@ -12,10 +12,9 @@
 // 4g..4g+3 and 16+4g..16+4g+3 of each 32-row step), which leaves the sum
 // unchanged.
 //
-// RoPE is applied while loading: Q fragments and the K tile are rotated in
-// float32 with the (cos, sin) table of each row's position inside its
-// sample (0..S-1, the compacted sequence) and rounded to bf16 once.
-// K and V tiles of 64 rows go through LDS; V is stored transposed.
+// Q and K arrive already rotated by RoPE (the QKV projection's epilogue
+// rotates them at each row's position inside its sample).  K and V tiles of
+// 64 rows go through LDS; V is stored transposed.
 #include "svl_internal.h"
 #include "device_util.h"
 
@@ -24,18 +23,6 @@ namespace {
 
 constexpr int BQ = ATTN_BQ, BKV = 64, NT = 256;
 constexpr float NEG_BIG = -1.0e30f;
-
-__device__ __forceinline__ void unpack8(const uint4& v, float* f) {
-  f[0] = bf16_bits_to_f32(v.x & 0xffffu); f[1] = bf16_bits_to_f32(v.x >> 16);
-  f[2] = bf16_bits_to_f32(v.y & 0xffffu); f[3] = bf16_bits_to_f32(v.y >> 16);
-  f[4] = bf16_bits_to_f32(v.z & 0xffffu); f[5] = bf16_bits_to_f32(v.z >> 16);
-  f[6] = bf16_bits_to_f32(v.w & 0xffffu); f[7] = bf16_bits_to_f32(v.w >> 16);
-}
-
-__device__ __forceinline__ uint4 pack8(const float* f) {
-  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
-                    pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7]));
-}
 
 template <int D>
 __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
@@ -62,31 +49,17 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
   const uint16_t* base = qkv + (size_t)g.row0 * ldq;
   const int qcol = h * D, kcol = (a.n_heads + kvh) * D, vcol = (a.n_heads + a.n_kv_heads + kvh) * D;
 
-  // Query fragments, rotated: lane holds Q[qi][32 s + 8 gq + j].
+  // Query fragments: lane holds Q[qi][32 s + 8 gq + j].
   const int qi = q0 + wave * 16 + lq;
   const bool qvalid = qi < S;
   bf16x8_t qf[NS];
   {
-    const int qrow = qvalid ? qi : 0;
-    const uint16_t* qp = base + (size_t)qrow * ldq + qcol;
-    float qv[NS][8];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) unpack8(*reinterpret_cast<const uint4*>(qp + 32 * s + 8 * gq), qv[s]);
-    const float2* cs = a.rope + (size_t)qrow * (D / 2);
-#pragma unroll
-    for (int s = 0; s < NS / 2; ++s)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float2 c = cs[32 * s + 8 * gq + j];
-        const float x1 = qv[s][j], x2 = qv[s + NS / 2][j];
-        qv[s][j] = x1 * c.x - x2 * c.y;
-        qv[s + NS / 2][j] = x2 * c.x + x1 * c.y;
-      }
+    const uint16_t* qp = base + (size_t)(qvalid ? qi : 0) * ldq + qcol;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      uint4 p = pack8(qv[s]);
-      if (!qvalid) p = make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8_t, p);
+      uint4 v = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * gq);
+      if (!qvalid) v = make_uint4(0, 0, 0, 0);
+      qf[s] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 
@@ -99,27 +72,13 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
 
   for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
     __syncthreads();
-    // K tile, rotated: task = (row, chunk c of the first half, and its partner).
-    for (int task = tid; task < BKV * (D / 16); task += NT) {
-      const int row = task / (D / 16), c = task % (D / 16);
+    // K tile: task = (row, 16-byte chunk).
+    for (int task = tid; task < BKV * (D / 8); task += NT) {
+      const int row = task / (D / 8), c = task % (D / 8);
       const int kv = kv0 + row;
-      const bool ok = kv < S;
-      const uint16_t* kp = base + (size_t)(ok ? kv : 0) * ldq + kcol;
-      float x1[8], x2[8];
-      unpack8(*reinterpret_cast<const uint4*>(kp + 8 * c), x1);
-      unpack8(*reinterpret_cast<const uint4*>(kp + D / 2 + 8 * c), x2);
-      const float2* cs = a.rope + (size_t)(ok ? kv : 0) * (D / 2) + 8 * c;
-      float y1[8], y2[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float2 cc = cs[j];
-        y1[j] = x1[j] * cc.x - x2[j] * cc.y;
-        y2[j] = x2[j] * cc.x + x1[j] * cc.y;
-      }
-      uint4 p1 = pack8(y1), p2 = pack8(y2);
-      if (!ok) { p1 = make_uint4(0, 0, 0, 0); p2 = p1; }
-      *reinterpret_cast<uint4*>(&Ks[row * KS + 8 * c]) = p1;
-      *reinterpret_cast<uint4*>(&Ks[row * KS + D / 2 + 8 * c]) = p2;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (kv < S) v = *reinterpret_cast<const uint4*>(base + (size_t)kv * ldq + kcol + 8 * c);
+      *reinterpret_cast<uint4*>(&Ks[row * KS + 8 * c]) = v;
     }
     // V tile, transposed: task = (row pair, 8-column chunk).
     for (int task = tid; task < (BKV / 2) * (D / 8); task += NT) {

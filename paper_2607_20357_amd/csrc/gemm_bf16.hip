@@ -19,10 +19,16 @@
 // arrival counter) adds the pieces in split order, so the result does not
 // depend on arrival order, and runs the epilogue.
 //
-// Epilogues: store as bf16 (Q/K/V), add into the float32 residual (output
-// and down projections), or SwiGLU: the tile's 128 weight rows are 64 gate
-// rows and the 64 matching up rows, interleaved so that one lane holds both
-// the gate and the up value of a channel, and silu(gate) * up is stored.
+// Epilogues:
+//   QKV: store as bf16; query and key columns are first rotated by RoPE at
+//     the row's position inside its sample (the float32 accumulators are
+//     rotated, so Q and K are rounded to bf16 once).  Rotation pairs dims
+//     (r, r + d/2) of a head; for d = 128 the tile's weight rows are
+//     interleaved so that one lane holds both members of each pair;
+//   RESID: add into the float32 residual (output and down projections);
+//   SWIGLU: the tile's 128 weight rows are 64 gate rows and the 64 matching
+//     up rows, interleaved so that one lane holds both the gate and the up
+//     value of a channel, and silu(gate) * up is stored.
 #include "svl_internal.h"
 #include "device_util.h"
 
@@ -77,9 +83,12 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
       b_ok[i] = ch < ncnt;
       src = static_cast<const uint16_t*>((j >> 1) ? a.W1 : a.W0);
       wrow = n0 + (b_ok[i] ? ch : 0);
-    } else if constexpr (EPI == EPI_STORE) {
-      b_ok[i] = r < ncnt;
-      const int col = n0 + (b_ok[i] ? r : 0);
+    } else if constexpr (EPI == EPI_QKV) {
+      // tile row r -> head dim: d = 128 interleaves the two rotation halves
+      const int half = r >> 6, j = (r & 63) >> 4;
+      const int tr = (a.head_dim == 128) ? (j >> 1) * 64 + half * 32 + (j & 1) * 16 + (r & 15) : r;
+      b_ok[i] = tr < ncnt;
+      const int col = n0 + (b_ok[i] ? tr : 0);
       if (n0 < a.nb1) { src = static_cast<const uint16_t*>(a.W0); wrow = col; }
       else if (n0 < a.nb2) { src = static_cast<const uint16_t*>(a.W1); wrow = col - a.nb1; }
       else { src = static_cast<const uint16_t*>(a.W2); wrow = col - a.nb2; }
@@ -189,18 +198,37 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
 
   // Epilogue.  acc[i][j][r] is C[wm*64 + i*16 + 4*(lane/16) + r][wn*64 + j*16 + lane%16].
   const int rbase = wm * 64 + (lane >> 4) * 4;
-  if constexpr (EPI == EPI_STORE) {
+  if constexpr (EPI == EPI_QKV) {
     uint16_t* out = static_cast<uint16_t*>(a.out);
+    const bool rot = n0 < a.rope_cols;
+    const int hd = a.head_dim, half = hd >> 1;
+    // d = 128: this wave holds dims wn*32 + [0,32) (blocks 0,1) and the same
+    // dims + 64 (blocks 2,3).  d = 64: this wave holds head wn of the tile,
+    // dims [0,32) (blocks 0,1) and [32,64) (blocks 2,3).
+    const int cbase = (hd == 128) ? wn * 32 : wn * 64;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rbase + i * 16 + r;
-        uint16_t* orow = out + (size_t)(mrow0 + min(row, mcnt - 1)) * a.ldo + n0;
+        const int rowc = min(row, mcnt - 1);
+        const int pos = (mrow0 - g.row0) + rowc;
+        uint16_t* orow = out + (size_t)(mrow0 + rowc) * a.ldo + n0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = wn * 64 + j * 16 + (lane & 15);
-          if (row < mcnt && col < ncnt) orow[col] = f32_to_bf16_bits(acc[i][j][r]);
+        for (int j = 0; j < 2; ++j) {
+          const int dim = j * 16 + (lane & 15) + ((hd == 128) ? wn * 32 : 0);  // in [0, d/2)
+          const int c1 = (hd == 128) ? dim : cbase + dim;
+          const int c2 = c1 + half;
+          float v1 = acc[i][j][r], v2 = acc[i][j + 2][r];
+          if (rot) {
+            const float2 cs = a.rope[(size_t)pos * half + dim];
+            const float o1 = v1 * cs.x - v2 * cs.y;
+            const float o2 = v2 * cs.x + v1 * cs.y;
+            v1 = o1;
+            v2 = o2;
+          }
+          if (row < mcnt && c1 < ncnt) orow[c1] = f32_to_bf16_bits(v1);
+          if (row < mcnt && c2 < ncnt) orow[c2] = f32_to_bf16_bits(v2);
         }
       }
   } else if constexpr (EPI == EPI_RESID) {
@@ -241,7 +269,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int32_t epi, hipStream_t st) {
   if (a.ntiles <= 0) return hipSuccess;
   const unsigned grid = (unsigned)((a.ntiles + 7) / 8 * 8);
   switch (epi) {
-    case EPI_STORE: gemm_bf16_kernel<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
+    case EPI_QKV: gemm_bf16_kernel<EPI_QKV><<<grid, NT, 0, st>>>(a); break;
     case EPI_RESID: gemm_bf16_kernel<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
     default: gemm_bf16_kernel<EPI_SWIGLU><<<grid, NT, 0, st>>>(a); break;
   }

@@ -15,6 +15,7 @@ enum Epilogue : int32_t {
   EPI_STORE = 0,   // out[row][col] = acc (activation dtype)
   EPI_RESID = 1,   // resid[row][col] += acc (float32)
   EPI_SWIGLU = 2,  // out[row][ch] = silu(gate) * up, gate/up tiles paired
+  EPI_QKV = 3,     // EPI_STORE, with RoPE applied to query / key columns
 };
 
 struct GemmArgs {
@@ -32,6 +33,9 @@ struct GemmArgs {
   int32_t ldo;
   float* partial;      // split-K partial tiles
   int32_t* counters;   // split-K arrival counters (zero between launches)
+  const float2* rope;  // EPI_QKV: (cos, sin)[pos][head_dim/2]
+  int32_t head_dim;    // EPI_QKV: 64 or 128
+  int32_t rope_cols;   // EPI_QKV: columns < rope_cols are rotated (Q and K heads)
 };
 
 struct AttnArgs {
@@ -43,7 +47,7 @@ struct AttnArgs {
   int32_t n_heads, n_kv_heads;
   void* out;           // [rows][A d]
   int32_t ldo;
-  const float2* rope;  // (cos, sin)[pos][d/2]
+  const float2* rope;  // (cos, sin)[pos][d/2]; used by kernels that rotate on load
   float scale;         // 1/sqrt(d)
 };
 
