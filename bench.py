@@ -203,7 +203,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if shape.dtype == "bf16" else "f32",
+        "dtype": "f16" if shape.dtype == "bf16" else "f32",
+        "storage_dtype": shape.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "batch": B, "n_vision": w.n_vision, "n_text": w.n_text,
                    "keep": [int(k) for k in inp.keep], "kept_tokens": R,
@@ -220,7 +221,7 @@ def main():
         "gemm_ms_per_step": round(gemm_ms, 4),
         "per_kernel": per_kernel,
         "roofline": {
-            "kernel": "gemm_bf16_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU)",
+            "kernel": "gemm_mfma_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
             "avg_launch_ms": round(gu_avg_ms, 5),

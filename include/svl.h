@@ -26,8 +26,9 @@
  *   the stream reaches that point.  No call synchronises the stream.
  * Dtypes.  `svl_config.dtype` selects the storage type of weights and of the
  *   vision / text hidden states: SVL_F32 (float) or SVL_BF16 (bfloat16).  The
- *   residual stream `resid` is always float32.  SVL_BF16 runs bf16 matrix
- *   products with float32 accumulation.
+ *   residual stream `resid` is always float32.  SVL_BF16 runs 16-bit MFMA
+ *   matrix products (fp16 or bf16 inputs, see svl_compute) with float32
+ *   accumulation.
  * Layouts.  Row-major throughout.  Linear weights use the [out][in] layout
  *   (y = x W^T).  The packed residual holds the samples one after another:
  *   rows cu_seqlens[b] .. cu_seqlens[b+1]-1 are sample b's sequence, kept
@@ -63,6 +64,17 @@ typedef enum {
 
 typedef enum { SVL_F32 = 0, SVL_BF16 = 1 } svl_dtype;
 
+/* Type of the activations between kernels and of the matrix-product inputs
+ * when the storage dtype is SVL_BF16 (ignored for SVL_F32, which computes in
+ * float32).  SVL_COMPUTE_F16 widens each bf16 weight to fp16 inside the
+ * matrix-product kernels (exact for magnitudes in [2^-14, 65504]; smaller
+ * ones become fp16 subnormals, absolute error at most 2^-25) and keeps
+ * activations in fp16 (11-bit significand): weights and activations must lie
+ * inside the fp16 range.  SVL_COMPUTE_BF16 keeps bf16 activations (8-bit
+ * significand, full bf16 range).  Both accumulate in float32 and keep the
+ * residual stream in float32. */
+typedef enum { SVL_COMPUTE_F16 = 0, SVL_COMPUTE_BF16 = 1 } svl_compute;
+
 /* Decoder shape (LLaMA block: pre-RMSNorm, rotate-half RoPE, causal
  * attention with n_kv_heads K/V heads shared by n_heads/n_kv_heads query
  * heads each, SwiGLU FFN, no biases).  n_groups is the number of head
@@ -75,7 +87,8 @@ typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, n_groups;
   float rms_eps;     /* RMSNorm epsilon */
   float rope_theta;  /* RoPE base: pair (r, r+d/2) turns by p * theta^(-2r/d) */
-  int32_t dtype;     /* svl_dtype */
+  int32_t dtype;     /* svl_dtype: storage of weights and hidden inputs */
+  int32_t compute;   /* svl_compute (SVL_BF16 storage only; 0 = SVL_COMPUTE_F16) */
 } svl_config;
 
 /* One layer's weights (dev, config dtype).  Shapes:

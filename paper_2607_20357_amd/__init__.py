@@ -5,7 +5,7 @@ behind a C ABI, see include/svl.h); `binding` marshals torch tensors and
 numpy arrays into its calls.
 """
 from .binding import (  # noqa: F401
-    KCLASS, SVL_BF16, SVL_F32, LayerTable, SvlError, alloc_workspace, layer_weights,
+    KCLASS, SVL_BF16, SVL_COMPUTE_BF16, SVL_COMPUTE_F16, SVL_F32, LayerTable, SvlError, alloc_workspace, layer_weights,
     load_library, make_config, svl_abi_version, svl_count_flops, svl_layer_forward, svl_prefill,
     svl_select_tokens, svl_timing_enable, svl_timing_read, svl_workspace_bytes,
 )

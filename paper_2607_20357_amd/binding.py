@@ -20,6 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsvl.so")
 
 SVL_F32, SVL_BF16 = 0, 1
+SVL_COMPUTE_F16, SVL_COMPUTE_BF16 = 0, 1
 KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
           "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "other": 9}
 STATUS = {0: "SVL_OK", 1: "SVL_E_NULL", 2: "SVL_E_SHAPE", 3: "SVL_E_VALUE", 4: "SVL_E_WORKSPACE",
@@ -38,7 +39,8 @@ class svl_config(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
                 ("n_groups", ctypes.c_int32), ("rms_eps", ctypes.c_float),
-                ("rope_theta", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("rope_theta", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("compute", ctypes.c_int32)]
 
 
 class svl_layer_weights(ctypes.Structure):
@@ -101,15 +103,21 @@ def _check(status: int) -> None:
 
 # ------------------------------------------------------------------ marshalling helpers
 def make_config(shape=None, **kw) -> svl_config:
-    """svl_config from an object with the decoder-shape attributes (or keywords)."""
+    """svl_config from an object with the decoder-shape attributes (or keywords).
+
+    compute: "f16" (default) or "bf16", the activation / matrix-input type of
+    bf16-stored workloads."""
     get = (lambda n, d=None: kw.get(n, getattr(shape, n, d))) if shape is not None else kw.get
     dtype = get("dtype", "bf16")
     if isinstance(dtype, str):
         dtype = SVL_BF16 if dtype == "bf16" else SVL_F32
+    compute = kw.get("compute", "f16")
+    if isinstance(compute, str):
+        compute = SVL_COMPUTE_BF16 if compute == "bf16" else SVL_COMPUTE_F16
     return svl_config(int(get("n_layers")), int(get("d_model")), int(get("n_heads")),
                       int(get("n_kv_heads")), int(get("head_dim")), int(get("d_ffn")),
                       int(get("n_groups", 4)), float(get("rms_eps", 1e-6)),
-                      float(get("rope_theta", 10000.0)), int(dtype))
+                      float(get("rope_theta", 10000.0)), int(dtype), int(compute))
 
 
 def _dev(t: Optional[torch.Tensor], name: str) -> int:

@@ -19,8 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libsvl.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["abi.cpp", "plan.cpp", "select_gather.hip", "norm_misc.hip", "gemm_bf16.hip",
-           "attn_bf16.hip", "fp32_path.hip"]
+SOURCES = ["abi.cpp", "plan.cpp", "select_gather.hip", "norm_misc.hip", "gemm_mfma.hip",
+           "attn_mfma.hip", "fp32_path.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -84,12 +84,16 @@ svl_status check_config(const svl_config* c, bool for_kernels = true) {
   if (c->d_ffn % c->n_groups) return fail(SVL_E_SHAPE, "d_ffn %% n_groups != 0");
   if (!(c->rms_eps >= 0.f)) return fail(SVL_E_VALUE, "rms_eps must be >= 0");
   if (!(c->rope_theta > 0.f)) return fail(SVL_E_VALUE, "rope_theta must be > 0");
+  if (c->compute != SVL_COMPUTE_F16 && c->compute != SVL_COMPUTE_BF16)
+    return fail(SVL_E_DTYPE, "unknown compute type %d", c->compute);
   if (!for_kernels) return SVL_OK;
   if (c->dtype == SVL_BF16) {
     if (c->d_model % 64) return fail(SVL_E_SHAPE, "bf16 path: d_model %% 64 != 0");
     if (c->head_dim != 64 && c->head_dim != 128)
       return fail(SVL_E_SHAPE, "bf16 path: head_dim must be 64 or 128");
     if ((c->d_ffn / c->n_groups) % 64) return fail(SVL_E_SHAPE, "bf16 path: d_ffn/n_groups %% 64 != 0");
+    if (c->d_model > 65536 || c->d_ffn > 65536 || c->n_heads * c->head_dim > 65536)
+      return fail(SVL_E_SHAPE, "bf16 path: reduction dimensions above 65536");
   } else {
     if (c->d_model % 4) return fail(SVL_E_SHAPE, "f32 path: d_model %% 4 != 0");
     if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
@@ -106,7 +110,7 @@ svl_status check_mask(const uint8_t* m, int64_t n, const char* what) {
 
 // ------------------------------------------------------------------ workspace
 struct WsLayout {
-  int64_t plan, rope, counters, partial, xn, qkv, attn_out, h, total;
+  int64_t plan, rope, xn, qkv, attn_out, h, total;
 };
 
 WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
@@ -121,8 +125,6 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
   };
   L.plan = take(plan_bytes_bound(c, B, c.n_layers));
   L.rope = take(rows * (c.head_dim / 2) * 8);
-  L.counters = take((int64_t)kSplitTarget * 4);
-  L.partial = take(c.dtype == SVL_BF16 ? (int64_t)kSplitTarget * SPLITK_SLOT_FLOATS * 4 : 0);
   L.xn = take(rows * c.d_model * es);
   L.qkv = take(rows * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
   L.attn_out = take(rows * (int64_t)c.n_heads * c.head_dim * es);
@@ -155,13 +157,14 @@ struct Exec {
     a.A = A; a.lda = lda;
     a.W0 = W0; a.W1 = W1; a.W2 = W2; a.ldw = ldw; a.nb1 = nb1; a.nb2 = nb2;
     a.out = out; a.ldo = ldo;
-    a.partial = reinterpret_cast<float*>(ws + L.partial);
-    a.counters = reinterpret_cast<int32_t*>(ws + L.counters);
     a.rope = reinterpret_cast<const float2*>(ws + L.rope);
     a.head_dim = c.head_dim;
     a.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim;
     const bool bf16 = c.dtype == SVL_BF16;
-    return timed(cls, st, [&] { return bf16 ? launch_gemm_bf16(a, epi, st) : launch_gemm_f32(a, epi, st); });
+    return timed(cls, st, [&] {
+      return bf16 ? launch_gemm_mfma(a, epi, g.bn, c.compute == SVL_COMPUTE_F16, st)
+                  : launch_gemm_f32(a, epi, st);
+    });
   }
 
   hipError_t norm(const NormLaunch& n, const void* gain) const {
@@ -175,7 +178,8 @@ struct Exec {
     a.out = ws + L.xn;
     a.D = c.d_model;
     a.eps = c.rms_eps;
-    return timed(K_NORM, st, [&] { return launch_rmsnorm(a, c.dtype, st); });
+    const int out_kind = c.dtype != SVL_BF16 ? 0 : (c.compute == SVL_COMPUTE_F16 ? 2 : 1);
+    return timed(K_NORM, st, [&] { return launch_rmsnorm(a, out_kind, st); });
   }
 
   hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) const {
@@ -203,7 +207,8 @@ struct Exec {
       a.rope = reinterpret_cast<const float2*>(ws + L.rope);
       a.scale = 1.0f / std::sqrt((float)d);
       e = timed(K_ATTN, st, [&] {
-        return c.dtype == SVL_BF16 ? launch_attn_bf16(a, d, st) : launch_attn_f32(a, d, st);
+        return c.dtype == SVL_BF16 ? launch_attn_mfma(a, d, c.compute == SVL_COMPUTE_F16, st)
+                                   : launch_attn_f32(a, d, st);
       });
       if (e != hipSuccess) return e;
       if ((e = gemm(P.o, chunks, ws + L.attn_out, A * d, w.wo, nullptr, nullptr, A * d, 0, 0, resid,
@@ -229,7 +234,7 @@ svl_status hip_fail(hipError_t e, const char* where) {
   return fail(SVL_E_HIP, "%s: %s", where, hipGetErrorString(e));
 }
 
-// Copies the plan image, clears the split-K counters and builds the RoPE table.
+// Copies the plan image and builds the RoPE table.
 svl_status stage(const Exec& ex, bool need_layers) {
   if ((int64_t)ex.plan.image.size() > ex.L.rope - ex.L.plan)
     return fail(SVL_E_SHAPE, "internal: plan image exceeds its workspace region");
@@ -237,10 +242,6 @@ svl_status stage(const Exec& ex, bool need_layers) {
                                 hipMemcpyHostToDevice, ex.st);
   if (e != hipSuccess) return hip_fail(e, "plan upload");
   if (need_layers) {
-    e = timed(K_OTHER, ex.st, [&] {
-      return launch_fill_i32(reinterpret_cast<int32_t*>(ex.ws + ex.L.counters), 0, kSplitTarget, ex.st);
-    });
-    if (e != hipSuccess) return hip_fail(e, "counter clear");
     e = timed(K_ROPE, ex.st, [&] {
       return launch_rope_table(reinterpret_cast<float2*>(ex.ws + ex.L.rope), ex.plan.max_seq,
                                ex.c.head_dim, ex.c.rope_theta, ex.st);

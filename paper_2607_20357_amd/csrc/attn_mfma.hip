@@ -1,5 +1,7 @@
 // Causal flash attention over the packed ragged batch, active heads only,
-// on bf16 MFMA (gfx950 v_mfma_f32_16x16x32_bf16).
+// on 16-bit MFMA (gfx950 v_mfma_f32_16x16x32_{f16,bf16}); Q, K, V, the
+// probabilities and the output are fp16 or bf16 (the activation type),
+// scores, softmax statistics and accumulators float32.
 //
 // One workgroup = one (sample, active query head, 64-row query tile); the
 // launch lists only active heads, so inactive heads are never read or
@@ -24,8 +26,8 @@ namespace {
 constexpr int BQ = ATTN_BQ, BKV = 64, NT = 256;
 constexpr float NEG_BIG = -1.0e30f;
 
-template <int D>
-__global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
+template <int D, bool F16>
+__global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D + 8;      // K tile row stride (elements)
   constexpr int VS = BKV + 8;    // transposed V tile row stride (elements)
   constexpr int NS = D / 32;     // MFMA k-steps over the head dimension
@@ -52,14 +54,14 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
   // Query fragments: lane holds Q[qi][32 s + 8 gq + j].
   const int qi = q0 + wave * 16 + lq;
   const bool qvalid = qi < S;
-  bf16x8_t qf[NS];
+  uint4 qf[NS];
   {
     const uint16_t* qp = base + (size_t)(qvalid ? qi : 0) * ldq + qcol;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       uint4 v = *reinterpret_cast<const uint4*>(qp + 32 * s + 8 * gq);
       if (!qvalid) v = make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8_t, v);
+      qf[s] = v;
     }
   }
 
@@ -105,8 +107,8 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
       st[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(&Ks[(16 * i + lq) * KS + 32 * s + 8 * gq]);
-        st[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[i], 0, 0, 0);
+        const uint4 kf = *reinterpret_cast<const uint4*>(&Ks[(16 * i + lq) * KS + 32 * s + 8 * gq]);
+        st[i] = mfma16x16x32<F16>(kf, qf[s], st[i]);
       }
     }
     // Causal mask (kv <= q) and online softmax, per query = per lane.
@@ -141,18 +143,16 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
     // O^T += V^T P^T, two 32-row kv steps.
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
-      const uint4 pp = make_uint4(pack_bf16x2(st[2 * t2][0], st[2 * t2][1]),
-                                  pack_bf16x2(st[2 * t2][2], st[2 * t2][3]),
-                                  pack_bf16x2(st[2 * t2 + 1][0], st[2 * t2 + 1][1]),
-                                  pack_bf16x2(st[2 * t2 + 1][2], st[2 * t2 + 1][3]));
-      const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pp);
+      const uint4 pb = make_uint4(pack_act2<F16>(st[2 * t2][0], st[2 * t2][1]),
+                                  pack_act2<F16>(st[2 * t2][2], st[2 * t2][3]),
+                                  pack_act2<F16>(st[2 * t2 + 1][0], st[2 * t2 + 1][1]),
+                                  pack_act2<F16>(st[2 * t2 + 1][2], st[2 * t2 + 1][3]));
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const uint16_t* vr = &Vt[(16 * b + lq) * VS + 32 * t2 + 4 * gq];
         const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
         const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 16);
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, make_uint4(v0.x, v0.y, v1.x, v1.y));
-        o[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[b], 0, 0, 0);
+        o[b] = mfma16x16x32<F16>(make_uint4(v0.x, v0.y, v1.x, v1.y), pb, o[b]);
       }
     }
   }
@@ -164,8 +164,8 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
     uint16_t* orow = static_cast<uint16_t*>(a.out) + (size_t)(g.row0 + qi) * a.ldo + h * D;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const uint2 w = make_uint2(pack_bf16x2(o[b][0] * inv, o[b][1] * inv),
-                                 pack_bf16x2(o[b][2] * inv, o[b][3] * inv));
+      const uint2 w = make_uint2(pack_act2<F16>(o[b][0] * inv, o[b][1] * inv),
+                                 pack_act2<F16>(o[b][2] * inv, o[b][3] * inv));
       *reinterpret_cast<uint2*>(orow + 16 * b + 4 * gq) = w;
     }
   }
@@ -173,11 +173,17 @@ __global__ __launch_bounds__(NT) void attn_bf16_kernel(AttnArgs a) {
 
 }  // namespace
 
-hipError_t launch_attn_bf16(const AttnArgs& a, int32_t head_dim, hipStream_t st) {
+hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st) {
   if (a.ntiles <= 0) return hipSuccess;
-  if (head_dim == 128) attn_bf16_kernel<128><<<a.ntiles, NT, 0, st>>>(a);
-  else if (head_dim == 64) attn_bf16_kernel<64><<<a.ntiles, NT, 0, st>>>(a);
-  else return hipErrorInvalidValue;
+  if (head_dim == 128) {
+    if (f16) attn_mfma_kernel<128, true><<<a.ntiles, NT, 0, st>>>(a);
+    else attn_mfma_kernel<128, false><<<a.ntiles, NT, 0, st>>>(a);
+  } else if (head_dim == 64) {
+    if (f16) attn_mfma_kernel<64, true><<<a.ntiles, NT, 0, st>>>(a);
+    else attn_mfma_kernel<64, false><<<a.ntiles, NT, 0, st>>>(a);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -53,3 +53,54 @@ __device__ __forceinline__ float warp_sum(float v) {
 }
 
 }  // namespace svl
+
+namespace svl {
+
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
+// Float -> 16-bit activation bits (fp16 or bf16, round to nearest even).
+template <bool F16>
+__device__ __forceinline__ uint16_t f32_to_act_bits(float f) {
+  if constexpr (F16) {
+    _Float16 h = static_cast<_Float16>(f);
+    return __builtin_bit_cast(uint16_t, h);
+  } else {
+    return f32_to_bf16_bits(f);
+  }
+}
+
+template <bool F16>
+__device__ __forceinline__ float act_bits_to_f32(uint32_t h) {
+  if constexpr (F16) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, (uint16_t)h));
+  } else {
+    return bf16_bits_to_f32(h);
+  }
+}
+
+template <bool F16>
+__device__ __forceinline__ uint32_t pack_act2(float lo, float hi) {
+  return (uint32_t)f32_to_act_bits<F16>(lo) | ((uint32_t)f32_to_act_bits<F16>(hi) << 16);
+}
+
+// Two bf16 values (one 32-bit word) -> the same two values as fp16.  Exact
+// for magnitudes in [2^-14, 65504]; smaller ones become fp16 subnormals
+// (absolute error at most 2^-25).
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+  const float lo = __uint_as_float(w << 16), hi = __uint_as_float(w & 0xffff0000u);
+  return pack_act2<true>(lo, hi);
+}
+
+// 16 x 16 x 32 MFMA on 8-element fragments of 16-bit activations.
+template <bool F16>
+__device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, const floatx4& c) {
+  if constexpr (F16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+}
+
+}  // namespace svl

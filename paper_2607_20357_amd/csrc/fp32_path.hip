@@ -23,7 +23,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   if (t >= a.ntiles) return;
   const GemmGroup g = a.groups[find_group(a.groups, a.ngroups, t)];
   constexpr int BNO = (EPI == EPI_SWIGLU) ? F32_SWIGLU_CH : BN;
-  const int local = t - g.tile0;   // nsplit is 1 on this path
+  const int local = t - g.tile0;
   const int nm = (g.nrows + BM - 1) / BM;
   const int mt = local % nm, nt = local / nm;
   const int mrow0 = g.row0 + mt * BM;

@@ -3,7 +3,8 @@
 //
 // RMSNorm: one workgroup per row, float32 statistics over the float32
 // residual, output y = x * rsqrt(mean(x^2) + eps) * gain in the activation
-// dtype (bf16 for the MFMA path).  Only rows of samples that execute the
+// type (fp16 or bf16 for the MFMA path, float32 for the float32 path); the
+// gain is stored in the weight dtype.  Only rows of samples that execute the
 // sub-block are listed, so skipped samples are neither read nor written.
 #include "svl_internal.h"
 #include "device_util.h"
@@ -13,7 +14,8 @@ namespace {
 
 constexpr int NT = 256;
 
-template <bool BF16>
+// OUT: 0 float32 (float32 gain), 1 bf16, 2 fp16 (bf16 gain)
+template <int OUT>
 __global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
   __shared__ float s_part[NT / 64];
   const int r = blockIdx.x;
@@ -38,7 +40,7 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
 #pragma unroll
   for (int i = 0; i < NT / 64; ++i) tot += s_part[i];
   const float inv = rsqrtf(tot / (float)D + a.eps);
-  if constexpr (BF16) {
+  if constexpr (OUT != 0) {
     const uint2* gain = reinterpret_cast<const uint2*>(a.gain);
     uint2* out = reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + row * D);
     for (int c = tid; c < D / 4; c += NT) {
@@ -46,8 +48,8 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
       const uint2 gw = gain[c];
       const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
       const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
-      out[c] = make_uint2(pack_bf16x2(v.x * inv * g0, v.y * inv * g1),
-                          pack_bf16x2(v.z * inv * g2, v.w * inv * g3));
+      out[c] = make_uint2(pack_act2<OUT == 2>(v.x * inv * g0, v.y * inv * g1),
+                          pack_act2<OUT == 2>(v.z * inv * g2, v.w * inv * g3));
     }
   } else {
     const float4* gain = reinterpret_cast<const float4*>(a.gain);
@@ -77,10 +79,11 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
 
 }  // namespace
 
-hipError_t launch_rmsnorm(const NormArgs& a, int32_t dtype, hipStream_t st) {
+hipError_t launch_rmsnorm(const NormArgs& a, int32_t out_kind, hipStream_t st) {
   if (a.nrows <= 0) return hipSuccess;
-  if (dtype == SVL_BF16) rmsnorm_kernel<true><<<a.nrows, NT, 0, st>>>(a);
-  else rmsnorm_kernel<false><<<a.nrows, NT, 0, st>>>(a);
+  if (out_kind == 2) rmsnorm_kernel<2><<<a.nrows, NT, 0, st>>>(a);
+  else if (out_kind == 1) rmsnorm_kernel<1><<<a.nrows, NT, 0, st>>>(a);
+  else rmsnorm_kernel<0><<<a.nrows, NT, 0, st>>>(a);
   return hipGetLastError();
 }
 

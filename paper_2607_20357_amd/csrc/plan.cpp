@@ -5,8 +5,9 @@
 //   * the active K chunks of the output and down projections (only active
 //     heads' / slices' weight columns are ever read);
 //   * the active heads of the attention launch.
-// It also picks the split-K factor of each GEMM launch so that the launch
-// has enough workgroups to cover the 256 CUs.
+// It also picks the bf16 GEMM tile width of each launch: narrow tiles for
+// skinny samples, so that a launch has enough workgroups for the 256 CUs
+// without splitting K.
 #include "plan.h"
 
 #include <algorithm>
@@ -50,40 +51,28 @@ int32_t cdiv(int32_t a, int32_t b) { return (a + b - 1) / b; }
 
 struct GemmBuild {
   std::vector<GemmGroup> groups;
-  int32_t min_chunks = 1 << 30;
+  int32_t max_rows = 0;
   void add(int32_t row0, int32_t nrows, int32_t n0, int32_t n1, int32_t kc_off, int32_t kc_cnt) {
     if (nrows <= 0 || n1 <= n0 || kc_cnt <= 0) return;
     GemmGroup g{};
     g.row0 = row0; g.nrows = nrows; g.n0 = n0; g.n1 = n1;
-    g.kc_off = kc_off; g.kc_cnt = kc_cnt; g.nsplit = 1;
+    g.kc_off = kc_off; g.kc_cnt = kc_cnt;
     groups.push_back(g);
-    min_chunks = std::min(min_chunks, kc_cnt);
+    max_rows = std::max(max_rows, nrows);
   }
-  // Fixes split factor and tile numbering; returns the launch description.
-  GemmLaunch finish(ImageWriter& w, int32_t BM, int32_t BN, bool allow_split) {
+  // Numbers the tiles (M tile fastest) for tiles of BM rows x BNO output
+  // columns; bn is the tile width in weight rows recorded for the launch.
+  GemmLaunch finish(ImageWriter& w, int32_t BM, int32_t BNO, int32_t bn) {
     GemmLaunch L;
-    int32_t base = 0;
-    for (auto& g : groups) base += cdiv(g.nrows, BM) * cdiv(g.n1 - g.n0, BN);
-    int32_t ns = 1;
-    if (allow_split && base > 0 && base < kSplitTarget) {
-      ns = std::max(1, kSplitTarget / base);
-      ns = std::min(ns, kMaxSplit);
-      ns = std::min(ns, std::max(1, min_chunks / 4));   // >= 4 chunks per split
-    }
-    int32_t tile = 0, ctr = 0;
+    int32_t tile = 0;
     for (auto& g : groups) {
-      int32_t out_tiles = cdiv(g.nrows, BM) * cdiv(g.n1 - g.n0, BN);
-      g.nsplit = ns;
       g.tile0 = tile;
-      g.ctr0 = ctr;
-      tile += out_tiles * ns;
-      ctr += out_tiles;
+      tile += cdiv(g.nrows, BM) * cdiv(g.n1 - g.n0, BNO);
     }
     L.groups_off = w.append(groups);
     L.ngroups = (int32_t)groups.size();
     L.ntiles = tile;
-    L.out_tiles = ctr;
-    L.nsplit = ns;
+    L.bn = bn;
     return L;
   }
 };
@@ -121,15 +110,11 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
   const int32_t A = cfg.n_heads, KV = cfg.n_kv_heads, G = cfg.n_groups, d = cfg.head_dim;
   const int32_t D = cfg.d_model, F = cfg.d_ffn, rep = A / KV, slice = F / G;
   const int32_t BM = bf16 ? BF16_BM : F32_BM;
-  const int32_t BN = bf16 ? BF16_BN : F32_BN;
-  const int32_t BNSW = bf16 ? BF16_SWIGLU_CH : F32_SWIGLU_CH;
   const int32_t bk = 64;
 
   plan->image.clear();
   plan->layers.assign(nlayers, LayerPlan{});
   plan->max_seq = 0;
-  plan->max_counters = 0;
-  plan->max_partial_floats = 0;
   ImageWriter w{&plan->image};
 
   std::vector<int32_t> cu(B + 1, 0);
@@ -209,22 +194,25 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     LP.norm_ffn.segs_off = w.append(seg_f);
     LP.norm_ffn.nsegs = (int32_t)seg_f.size();
     LP.norm_ffn.nrows = seg_rows(seg_f);
-    LP.qkv = qkv.finish(w, BM, BN, bf16);
-    LP.o = o.finish(w, BM, BN, bf16);
-    LP.gu = gu.finish(w, BM, BNSW, bf16);
-    LP.down = down.finish(w, BM, BN, bf16);
+    if (bf16) {
+      // narrow tiles for skinny samples: enough workgroups without split-K
+      const int32_t bn_od = std::max(o.max_rows, down.max_rows) <= kSkinnyRows ? 32 : 64;
+      const int32_t bn_gu = gu.max_rows <= kSkinnyRows ? 64 : 128;
+      LP.qkv = qkv.finish(w, BM, 64, 64);
+      LP.o = o.finish(w, BM, bn_od, bn_od);
+      LP.gu = gu.finish(w, BM, bn_gu / 2, bn_gu);
+      LP.down = down.finish(w, BM, bn_od, bn_od);
+    } else {
+      LP.qkv = qkv.finish(w, BM, F32_BN, F32_BN);
+      LP.o = o.finish(w, BM, F32_BN, F32_BN);
+      LP.gu = gu.finish(w, BM, F32_SWIGLU_CH, F32_BN);
+      LP.down = down.finish(w, BM, F32_BN, F32_BN);
+    }
     LP.attn.groups_off = w.append(ag);
     LP.attn.heads_off = w.append(heads);
     LP.attn.ngroups = (int32_t)ag.size();
     LP.attn.ntiles = attn_tiles;
     LP.chunks_off = w.append(chunks);
-    for (const GemmLaunch* g : {&LP.qkv, &LP.o, &LP.gu, &LP.down}) {
-      if (g->nsplit > 1) {
-        plan->max_counters = std::max(plan->max_counters, g->out_tiles);
-        plan->max_partial_floats = std::max(plan->max_partial_floats,
-                                            (int64_t)g->ntiles * SPLITK_SLOT_FLOATS);
-      }
-    }
   }
   (void)bf16;
   return true;

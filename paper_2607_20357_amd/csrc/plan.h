@@ -15,9 +15,8 @@ namespace svl {
 struct GemmLaunch {
   int64_t groups_off = 0;   // byte offset of the GemmGroup array in the plan image
   int32_t ngroups = 0;
-  int32_t ntiles = 0;       // tiles including split-K copies
-  int32_t out_tiles = 0;    // output tiles (split-K counters needed)
-  int32_t nsplit = 1;
+  int32_t ntiles = 0;
+  int32_t bn = 0;           // weight rows per tile (bf16 kernels: 32, 64 or 128)
 };
 
 struct AttnLaunch {
@@ -45,8 +44,6 @@ struct Plan {
   std::vector<LayerPlan> layers;
   int64_t keep_off = 0, cu_off = 0;
   int32_t max_seq = 0;            // longest sequence (RoPE table rows)
-  int32_t max_counters = 0;       // split-K counters any launch needs
-  int64_t max_partial_floats = 0; // split-K partial storage any launch needs
 };
 
 struct LayerMasks {
@@ -57,9 +54,8 @@ struct LayerMasks {
   int64_t ffn_stride;
 };
 
-// Target number of workgroups a split-K launch aims for (two per CU).
-constexpr int32_t kSplitTarget = 512;
-constexpr int32_t kMaxSplit = 8;
+// Rows of a sample up to which the bf16 GEMMs use their narrow tiles.
+constexpr int32_t kSkinnyRows = 256;
 
 // Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks(l)
 // gives layer l's masks.  Returns false with a message on inconsistency.

@@ -19,17 +19,15 @@ struct Seg {
 };
 
 // One (sample, output-column range) pair of a GEMM launch.  Its tiles are
-// ceil(nrows/BM) x ceil((n1-n0)/BN) x nsplit, enumerated split fastest, then
-// M tile, then N tile, starting at tile index tile0 of the launch.
+// ceil(nrows/BM) x ceil((n1-n0)/BNO), enumerated M tile fastest, starting at
+// tile index tile0 of the launch (BNO: output columns per tile).
 struct GemmGroup {
   int32_t row0, nrows;  // rows of A (and of the output) in the packed space
   int32_t n0, n1;       // output columns [n0, n1)
   int32_t kc_off;       // first entry of this group's K chunks in the chunk table
   int32_t kc_cnt;       // number of K chunks
-  int32_t nsplit;       // split-K factor (1: no split)
   int32_t tile0;        // first tile index of the group
-  int32_t ctr0;         // first split-K counter (one per output tile)
-  int32_t pad0, pad1, pad2;
+  int32_t pad0;
 };
 
 // One sample of an attention launch: one workgroup per (active head, q tile).
@@ -48,11 +46,11 @@ struct KChunk {
 
 // ---------------------------------------------------------------------------
 // Tile sizes (the planner and the kernels must agree).
-constexpr int BF16_BM = 128, BF16_BN = 128, BF16_BK = 64;
-constexpr int BF16_SWIGLU_CH = 64;   // channels per gate/up tile (64 gate + 64 up rows)
+// bf16: 128-row tiles; the tile width BN (weight rows per tile) is chosen per
+// launch from {32, 64, 128} (gate/up tiles hold BN/2 channels).
+constexpr int BF16_BM = 128, BF16_BK = 64;
 constexpr int F32_BM = 64, F32_BN = 64, F32_BK = 16;
 constexpr int F32_SWIGLU_CH = 32;
 constexpr int ATTN_BQ = 64;          // query rows per attention workgroup
-constexpr int SPLITK_SLOT_FLOATS = BF16_BM * BF16_BN;  // one partial tile
 
 }  // namespace svl

@@ -31,8 +31,6 @@ struct GemmArgs {
   int32_t nb1, nb2;    // EPI_STORE: columns < nb1 -> W0, < nb2 -> W1, else W2
   void* out;           // output / residual, row stride ldo
   int32_t ldo;
-  float* partial;      // split-K partial tiles
-  int32_t* counters;   // split-K arrival counters (zero between launches)
   const float2* rope;  // EPI_QKV: (cos, sin)[pos][head_dim/2]
   int32_t head_dim;    // EPI_QKV: 64 or 128
   int32_t rope_cols;   // EPI_QKV: columns < rope_cols are rotated (Q and K heads)
@@ -69,10 +67,11 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
                          int32_t B, int32_t N, int32_t T, int32_t D, int32_t total_rows,
                          const void* vision, const void* text, int32_t dtype, float* resid,
                          hipStream_t st);
-hipError_t launch_rmsnorm(const NormArgs& a, int32_t dtype, hipStream_t st);
-hipError_t launch_gemm_bf16(const GemmArgs& a, int32_t epi, hipStream_t st);
+// out_kind: 0 float32, 1 bf16, 2 fp16
+hipError_t launch_rmsnorm(const NormArgs& a, int32_t out_kind, hipStream_t st);
+hipError_t launch_gemm_mfma(const GemmArgs& a, int32_t epi, int32_t bn, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
-hipError_t launch_attn_bf16(const AttnArgs& a, int32_t head_dim, hipStream_t st);
+hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);
 hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, float theta,
                              hipStream_t st);

@@ -69,9 +69,9 @@ def test_prefill_scaled_video():
     _check_prefill(w)
 
 
-def _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask, seed=3):
+def _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask, seed=3, compute="f16"):
     dev = "cuda"
-    cfg = svl.make_config(shape)
+    cfg = svl.make_config(shape, compute=compute)
     R = int(np.sum(seqlens))
     cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
     g = torch.Generator(device=dev).manual_seed(seed)
@@ -98,10 +98,11 @@ def _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask, seed=3):
     return rel_err_per_sample(got, ref, cu)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_layer_masks_and_edges(dtype):
+@pytest.mark.parametrize("dtype,compute", [("f32", "f16"), ("bf16", "f16"), ("bf16", "bf16")])
+def test_layer_masks_and_edges(dtype, compute):
     """Per-head masks (not only whole groups), FFN coupled / ungated / all
-    off, a bypassed sample, an empty sample and a one-row sample."""
+    off, a bypassed sample, an empty sample and a one-row sample; both
+    activation types of bf16-stored weights."""
     hd = 64
     shape = W.ModelShape(n_layers=1, d_model=512, n_heads=8, n_kv_heads=4, head_dim=hd,
                          d_ffn=1024, n_groups=4, dtype=dtype)
@@ -116,23 +117,26 @@ def test_layer_masks_and_edges(dtype):
     layer_on = np.array([1, 1, 1, 1, 0], np.uint8)
     tol = tol_for(shape)
     for fm in (ffn_mask, None):
-        print(f"layer edges dtype={dtype} ffn={'coupled' if fm is not None else 'ungated'}",
-              flush=True)
-        errs = _layer_case(shape, seqlens, layer_on, head_mask, fm)
+        print(f"layer edges dtype={dtype} compute={compute} "
+              f"ffn={'coupled' if fm is not None else 'ungated'}", flush=True)
+        errs = _layer_case(shape, seqlens, layer_on, head_mask, fm, compute=compute)
+        print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
         assert max(errs) <= tol, errs
 
 
-@pytest.mark.parametrize("name", ["llava7b_b1_keep25", "llava7b_b8_ragged", "gqa7b_hires_b2",
-                                  "llava13b_video_b4"])
-def test_layer_full_size(name):
+@pytest.mark.parametrize("name,compute", [("llava7b_b1_keep25", "f16"), ("llava7b_b1_keep25", "bf16"),
+                                          ("llava7b_b8_ragged", "f16"), ("gqa7b_hires_b2", "f16"),
+                                          ("llava13b_video_b4", "f16")])
+def test_layer_full_size(name, compute):
     """One decoder layer at each workload's real width, sequence lengths and
     masks (first non-prefix layer of the seed-0 draw)."""
     w = W.get_workload(name)
     keep, lm, hm, fm = W.draw_masks(w, 0)
     l = w.shape.prefix
     seqlens = (keep + w.n_text).astype(np.int32)
-    print(f"layer full size {name} seqlens={seqlens.tolist()}", flush=True)
-    errs = _layer_case(w.shape, seqlens, lm[:, l], hm[:, l], None if fm is None else fm[:, l])
+    print(f"layer full size {name} compute={compute} seqlens={seqlens.tolist()}", flush=True)
+    errs = _layer_case(w.shape, seqlens, lm[:, l], hm[:, l], None if fm is None else fm[:, l],
+                       compute=compute)
     print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
     assert max(errs) <= tol_for(w.shape), errs
 
