@@ -3,6 +3,7 @@
 // and the launch sequence of the prefill.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -110,12 +111,15 @@ svl_status check_mask(const uint8_t* m, int64_t n, const char* what) {
 
 // ------------------------------------------------------------------ workspace
 struct WsLayout {
-  int64_t plan, rope, xn, qkv, attn_out, h, total;
+  int64_t plan, rope, partial, xn, qkv, attn_out, h, total;
+  int64_t partial_slice;   // floats per split-K slice (R x d_model)
 };
 
+// Activation buffers use the padded row space (16-row blocks per sample on
+// the 16-bit MFMA path); the partial region holds the float32 split-K slices.
 WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
   const int64_t es = c.dtype == SVL_BF16 ? 2 : 4;
-  const int64_t rows = R > 0 ? R : 1;
+  const int64_t prow = std::max<int64_t>(padded_rows_bound(c, B, R), 16);
   WsLayout L{};
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
@@ -124,11 +128,13 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
     return o;
   };
   L.plan = take(plan_bytes_bound(c, B, c.n_layers));
-  L.rope = take(rows * (c.head_dim / 2) * 8);
-  L.xn = take(rows * c.d_model * es);
-  L.qkv = take(rows * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
-  L.attn_out = take(rows * (int64_t)c.n_heads * c.head_dim * es);
-  L.h = take(rows * (int64_t)c.d_ffn * es);
+  L.rope = take(std::max<int64_t>(R, 1) * (c.head_dim / 2) * 8);
+  L.partial = take(partial_rows_bound(c, R) * c.d_model * 4);
+  L.partial_slice = (int64_t)R * c.d_model;
+  L.xn = take(prow * c.d_model * es);
+  L.qkv = take(prow * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
+  L.attn_out = take(prow * (int64_t)c.n_heads * c.head_dim * es);
+  L.h = take(prow * (int64_t)c.d_ffn * es);
   L.total = off;
   return L;
 }
@@ -160,6 +166,8 @@ struct Exec {
     a.rope = reinterpret_cast<const float2*>(ws + L.rope);
     a.head_dim = c.head_dim;
     a.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim;
+    a.partial = reinterpret_cast<float*>(ws + L.partial);
+    a.pslice = L.partial_slice;
     const bool bf16 = c.dtype == SVL_BF16;
     return timed(cls, st, [&] {
       return bf16 ? launch_gemm_mfma(a, epi, g.bn, c.compute == SVL_COMPUTE_F16, st)
@@ -170,28 +178,35 @@ struct Exec {
   hipError_t norm(const NormLaunch& n, const void* gain) const {
     if (n.nrows == 0) return hipSuccess;
     NormArgs a{};
-    a.segs = at<Seg>(n.segs_off);
+    a.segs = at<NormSeg>(n.segs_off);
     a.nsegs = n.nsegs;
     a.nrows = n.nrows;
     a.x = resid;
+    a.partial = reinterpret_cast<const float*>(ws + L.partial);
+    a.nsplit = n.nsplit;
+    a.pslice = L.partial_slice;
     a.gain = gain;
     a.out = ws + L.xn;
     a.D = c.d_model;
     a.eps = c.rms_eps;
     const int out_kind = c.dtype != SVL_BF16 ? 0 : (c.compute == SVL_COMPUTE_F16 ? 2 : 1);
-    return timed(K_NORM, st, [&] { return launch_rmsnorm(a, out_kind, st); });
+    return timed(K_NORM, st, [&] { return launch_resid_norm(a, out_kind, st); });
   }
+
+  // Output / down projection: straight into the residual, or split-K
+  // pieces into the partial slices the next residual-finish launch adds.
+  static int resid_epi(const GemmLaunch& g) { return g.nsplit > 1 ? EPI_PARTIAL : EPI_RESID; }
 
   hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) const {
     const int A = c.n_heads, KV = c.n_kv_heads, d = c.head_dim, D = c.d_model, F = c.d_ffn;
     const int qkv_w = (A + 2 * KV) * d;
+    const bool mfma = c.dtype == SVL_BF16;
     const KChunk* chunks = at<KChunk>(P.chunks_off);
     hipError_t e = hipSuccess;
-    if (P.norm_attn.nrows > 0) {
-      if ((e = norm(P.norm_attn, w.attn_norm)) != hipSuccess) return e;
+    if ((e = norm(P.norm_attn, w.attn_norm)) != hipSuccess) return e;
+    if (P.qkv.ntiles > 0) {
       if ((e = gemm(P.qkv, chunks, ws + L.xn, D, w.wq, w.wk, w.wv, D, A * d, (A + KV) * d,
-                    ws + L.qkv, qkv_w, c.dtype == SVL_BF16 ? EPI_QKV : EPI_STORE, K_QKV)) !=
-          hipSuccess)
+                    ws + L.qkv, qkv_w, mfma ? EPI_QKV : EPI_STORE, K_QKV)) != hipSuccess)
         return e;
       AttnArgs a{};
       a.groups = at<AttnGroup>(P.attn.groups_off);
@@ -207,21 +222,21 @@ struct Exec {
       a.rope = reinterpret_cast<const float2*>(ws + L.rope);
       a.scale = 1.0f / std::sqrt((float)d);
       e = timed(K_ATTN, st, [&] {
-        return c.dtype == SVL_BF16 ? launch_attn_mfma(a, d, c.compute == SVL_COMPUTE_F16, st)
-                                   : launch_attn_f32(a, d, st);
+        return mfma ? launch_attn_mfma(a, d, c.compute == SVL_COMPUTE_F16, st)
+                    : launch_attn_f32(a, d, st);
       });
       if (e != hipSuccess) return e;
       if ((e = gemm(P.o, chunks, ws + L.attn_out, A * d, w.wo, nullptr, nullptr, A * d, 0, 0, resid,
-                    D, EPI_RESID, K_O)) != hipSuccess)
+                    D, resid_epi(P.o), K_O)) != hipSuccess)
         return e;
     }
-    if (P.norm_ffn.nrows > 0) {
-      if ((e = norm(P.norm_ffn, w.ffn_norm)) != hipSuccess) return e;
+    if ((e = norm(P.norm_ffn, w.ffn_norm)) != hipSuccess) return e;
+    if (P.gu.ntiles > 0) {
       if ((e = gemm(P.gu, chunks, ws + L.xn, D, w.w_gate, w.w_up, nullptr, D, 0, 0, ws + L.h, F,
                     EPI_SWIGLU, K_GU)) != hipSuccess)
         return e;
       if ((e = gemm(P.down, chunks, ws + L.h, F, w.w_down, nullptr, nullptr, F, 0, 0, resid, D,
-                    EPI_RESID, K_DOWN)) != hipSuccess)
+                    resid_epi(P.down), K_DOWN)) != hipSuccess)
         return e;
     }
     return hipSuccess;
@@ -420,6 +435,7 @@ svl_status svl_layer_forward(const svl_config* cfg, int32_t layer, const svl_lay
   Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), ws_layout(*cfg, batch, R), t_plan, resid};
   if ((s = stage(ex, true)) != SVL_OK) return s;
   hipError_t e = ex.layer(t_plan.layers[0], *w);
+  if (e == hipSuccess) e = ex.norm(t_plan.final_norm, nullptr);
   if (e != hipSuccess) return hip_fail(e, "layer launch");
   return SVL_OK;
 }
@@ -480,6 +496,8 @@ svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, c
     hipError_t e = ex.layer(t_plan.layers[l], layers[l]);
     if (e != hipSuccess) return hip_fail(e, "layer launch");
   }
+  hipError_t e = ex.norm(t_plan.final_norm, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "final residual launch");
   return SVL_OK;
 }
 

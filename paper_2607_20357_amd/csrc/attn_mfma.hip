@@ -16,7 +16,8 @@
 //
 // Q and K arrive already rotated by RoPE (the QKV projection's epilogue
 // rotates them at each row's position inside its sample).  K and V tiles of
-// 64 rows go through LDS; V is stored transposed.
+// 64 rows go through LDS; V is stored transposed.  The output is written in
+// the fragment-packed layout the output projection reads.
 #include "svl_internal.h"
 #include "device_util.h"
 
@@ -160,13 +161,16 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   l_i += __shfl_xor(l_i, 16, 64);
   l_i += __shfl_xor(l_i, 32, 64);
   if (qvalid) {
+    // fragment-packed output for the output projection: the lane's 4
+    // consecutive dims 16 b + 4 gq + [0, 4) are contiguous in the layout
     const float inv = 1.0f / l_i;
-    uint16_t* orow = static_cast<uint16_t*>(a.out) + (size_t)(g.row0 + qi) * a.ldo + h * D;
+    uint16_t* out = static_cast<uint16_t*>(a.out);
+    const int64_t row = (int64_t)g.row0 + qi;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const uint2 w = make_uint2(pack_act2<F16>(o[b][0] * inv, o[b][1] * inv),
                                  pack_act2<F16>(o[b][2] * inv, o[b][3] * inv));
-      *reinterpret_cast<uint2*>(orow + 16 * b + 4 * gq) = w;
+      *reinterpret_cast<uint2*>(out + packed_index(row, h * D + 16 * b + 4 * gq, a.ldo)) = w;
     }
   }
 }

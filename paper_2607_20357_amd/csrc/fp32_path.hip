@@ -26,7 +26,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const int local = t - g.tile0;
   const int nm = (g.nrows + BM - 1) / BM;
   const int mt = local % nm, nt = local / nm;
-  const int mrow0 = g.row0 + mt * BM;
+  const int arow0 = g.arow0 + mt * BM, orow0 = g.orow0 + mt * BM;
   const int mcnt = min(BM, g.nrows - mt * BM);
   const int n0 = g.n0 + nt * BNO;
   const int ncnt = min(BNO, g.n1 - n0);
@@ -53,7 +53,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   };
   // Loader: element e of thread tid covers row (tid*4+e)/16, k (tid*4+e)%16.
   const int lrow = tid >> 2, lk = (tid & 3) * 4;
-  const float* arow = lrow < mcnt ? A + (size_t)(mrow0 + lrow) * a.lda : nullptr;
+  const float* arow = lrow < mcnt ? A + (size_t)(arow0 + lrow) * a.lda : nullptr;
   const float* brow = wrow(lrow);
   // Output columns of this thread (tile columns).
   int cols[4];
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     const int row = ty * 4 + i;
     if (row >= mcnt) continue;
     if constexpr (EPI == EPI_SWIGLU) {
-      float* orow = static_cast<float*>(a.out) + (size_t)(mrow0 + row) * a.ldo + n0;
+      float* orow = static_cast<float*>(a.out) + (size_t)(orow0 + row) * a.ldo + n0;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int ch = cols[j];
@@ -102,12 +102,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
         if (ch < ncnt) orow[ch] = gt / (1.0f + expf(-gt)) * up;
       }
     } else if constexpr (EPI == EPI_STORE) {
-      float* orow = static_cast<float*>(a.out) + (size_t)(mrow0 + row) * a.ldo + n0;
+      float* orow = static_cast<float*>(a.out) + (size_t)(orow0 + row) * a.ldo + n0;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (cols[j] < ncnt) orow[cols[j]] = acc[i][j];
     } else {
-      float* orow = static_cast<float*>(a.out) + (size_t)(mrow0 + row) * a.ldo + n0;
+      float* orow = static_cast<float*>(a.out) + (size_t)(orow0 + row) * a.ldo + n0;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (cols[j] < ncnt) orow[cols[j]] += acc[i][j];

@@ -1,11 +1,14 @@
-// RMSNorm of the residual rows that run a sub-block, the RoPE (cos, sin)
-// table, and a fill kernel.
+// Residual finish + RMSNorm, the RoPE (cos, sin) table, and a fill kernel.
 //
-// RMSNorm: one workgroup per row, float32 statistics over the float32
-// residual, output y = x * rsqrt(mean(x^2) + eps) * gain in the activation
-// type (fp16 or bf16 for the MFMA path, float32 for the float32 path); the
-// gain is stored in the weight dtype.  Only rows of samples that execute the
-// sub-block are listed, so skipped samples are neither read nor written.
+// Residual finish + RMSNorm: one workgroup per listed row.  Rows flagged
+// NORM_ADD_PARTIALS first receive the pending split-K partial slices of the
+// previous output / down projection, added in slice order (a fixed order:
+// the result does not depend on scheduling), and are written back.  Rows
+// flagged NORM_WRITE_OUT are then normed with float32 statistics,
+// y = x * rsqrt(mean(x^2) + eps) * gain, and stored in the activation type:
+// fragment-packed fp16 / bf16 for the 16-bit MFMA GEMMs (16-byte stores of
+// 8-column groups), row-major float32 on the float32 path.  Rows of samples
+// that do not run the sub-block are not listed.
 #include "svl_internal.h"
 #include "device_util.h"
 
@@ -14,9 +17,9 @@ namespace {
 
 constexpr int NT = 256;
 
-// OUT: 0 float32 (float32 gain), 1 bf16, 2 fp16 (bf16 gain)
+// OUT: 0 float32 row-major (float32 gain), 1 bf16 packed, 2 fp16 packed (bf16 gain)
 template <int OUT>
-__global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
+__global__ __launch_bounds__(NT) void resid_norm_kernel(NormArgs a) {
   __shared__ float s_part[NT / 64];
   const int r = blockIdx.x;
   int lo = 0, hi = a.nsegs - 1;
@@ -24,15 +27,25 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
     const int mid = (lo + hi + 1) >> 1;
     if (a.segs[mid].prefix <= r) lo = mid; else hi = mid - 1;
   }
-  const Seg sg = a.segs[lo];
+  const NormSeg sg = a.segs[lo];
   const size_t row = (size_t)sg.row0 + (r - sg.prefix);
+  const size_t prow = (size_t)sg.prow0 + (r - sg.prefix);
   const int D = a.D, tid = threadIdx.x;
-  const float4* x = reinterpret_cast<const float4*>(a.x + row * D);
+  float4* x = reinterpret_cast<float4*>(a.x + row * D);
+  const bool add = (sg.flags & NORM_ADD_PARTIALS) != 0;
   float ss = 0.f;
   for (int c = tid; c < D / 4; c += NT) {
-    const float4 v = x[c];
+    float4 v = x[c];
+    if (add) {
+      for (int p = 0; p < a.nsplit; ++p) {
+        const float4 q = reinterpret_cast<const float4*>(a.partial + p * a.pslice + row * D)[c];
+        v.x += q.x; v.y += q.y; v.z += q.z; v.w += q.w;
+      }
+      x[c] = v;
+    }
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
+  if (!(sg.flags & NORM_WRITE_OUT)) return;   // uniform across the workgroup
   ss = warp_sum(ss);
   if ((tid & 63) == 0) s_part[tid >> 6] = ss;
   __syncthreads();
@@ -41,19 +54,24 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(NormArgs a) {
   for (int i = 0; i < NT / 64; ++i) tot += s_part[i];
   const float inv = rsqrtf(tot / (float)D + a.eps);
   if constexpr (OUT != 0) {
-    const uint2* gain = reinterpret_cast<const uint2*>(a.gain);
-    uint2* out = reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + row * D);
-    for (int c = tid; c < D / 4; c += NT) {
-      const float4 v = x[c];
-      const uint2 gw = gain[c];
-      const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
-      const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
-      out[c] = make_uint2(pack_act2<OUT == 2>(v.x * inv * g0, v.y * inv * g1),
-                          pack_act2<OUT == 2>(v.z * inv * g2, v.w * inv * g3));
+    const uint4* gain = reinterpret_cast<const uint4*>(a.gain);
+    uint16_t* out = static_cast<uint16_t*>(a.out);
+    for (int c = tid; c < D / 8; c += NT) {
+      const float4 v0 = x[2 * c], v1 = x[2 * c + 1];
+      const uint4 gw = gain[c];
+      const float g[8] = {bf16_bits_to_f32(gw.x & 0xffffu), bf16_bits_to_f32(gw.x >> 16),
+                          bf16_bits_to_f32(gw.y & 0xffffu), bf16_bits_to_f32(gw.y >> 16),
+                          bf16_bits_to_f32(gw.z & 0xffffu), bf16_bits_to_f32(gw.z >> 16),
+                          bf16_bits_to_f32(gw.w & 0xffffu), bf16_bits_to_f32(gw.w >> 16)};
+      const uint4 o = make_uint4(pack_act2<OUT == 2>(v0.x * inv * g[0], v0.y * inv * g[1]),
+                                 pack_act2<OUT == 2>(v0.z * inv * g[2], v0.w * inv * g[3]),
+                                 pack_act2<OUT == 2>(v1.x * inv * g[4], v1.y * inv * g[5]),
+                                 pack_act2<OUT == 2>(v1.z * inv * g[6], v1.w * inv * g[7]));
+      *reinterpret_cast<uint4*>(out + packed_index((int64_t)prow, 8 * c, D)) = o;
     }
   } else {
     const float4* gain = reinterpret_cast<const float4*>(a.gain);
-    float4* out = reinterpret_cast<float4*>(static_cast<float*>(a.out) + row * D);
+    float4* out = reinterpret_cast<float4*>(static_cast<float*>(a.out) + prow * D);
     for (int c = tid; c < D / 4; c += NT) {
       const float4 v = x[c], g = gain[c];
       out[c] = make_float4(v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z, v.w * inv * g.w);
@@ -79,11 +97,11 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
 
 }  // namespace
 
-hipError_t launch_rmsnorm(const NormArgs& a, int32_t out_kind, hipStream_t st) {
+hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st) {
   if (a.nrows <= 0) return hipSuccess;
-  if (out_kind == 2) rmsnorm_kernel<2><<<a.nrows, NT, 0, st>>>(a);
-  else if (out_kind == 1) rmsnorm_kernel<1><<<a.nrows, NT, 0, st>>>(a);
-  else rmsnorm_kernel<0><<<a.nrows, NT, 0, st>>>(a);
+  if (out_kind == 2) resid_norm_kernel<2><<<a.nrows, NT, 0, st>>>(a);
+  else if (out_kind == 1) resid_norm_kernel<1><<<a.nrows, NT, 0, st>>>(a);
+  else resid_norm_kernel<0><<<a.nrows, NT, 0, st>>>(a);
   return hipGetLastError();
 }
 

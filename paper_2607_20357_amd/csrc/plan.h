@@ -16,7 +16,8 @@ struct GemmLaunch {
   int64_t groups_off = 0;   // byte offset of the GemmGroup array in the plan image
   int32_t ngroups = 0;
   int32_t ntiles = 0;
-  int32_t bn = 0;           // weight rows per tile (bf16 kernels: 32, 64 or 128)
+  int32_t bn = 0;           // weight rows per tile (16-bit MFMA kernels: 64 or 128)
+  int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
 };
 
 struct AttnLaunch {
@@ -24,9 +25,14 @@ struct AttnLaunch {
   int32_t ngroups = 0, ntiles = 0;
 };
 
+// A residual / RMSNorm launch: adds pending split-K partials (nsplit slices)
+// into the residual rows flagged for it, and writes the normed rows flagged
+// for it.
 struct NormLaunch {
   int64_t segs_off = 0;
   int32_t nsegs = 0, nrows = 0;
+  int32_t nsplit = 0;       // partial slices to add (0: none pending)
+  bool write_out = false;   // some segment writes normed rows
 };
 
 struct LayerPlan {
@@ -42,8 +48,10 @@ struct LayerPlan {
 struct Plan {
   std::vector<uint8_t> image;
   std::vector<LayerPlan> layers;
+  NormLaunch final_norm;          // adds the last layer's pending partials
   int64_t keep_off = 0, cu_off = 0;
   int32_t max_seq = 0;            // longest sequence (RoPE table rows)
+  int32_t padded_rows = 0;        // rows of the activation buffers
 };
 
 struct LayerMasks {
@@ -54,15 +62,31 @@ struct LayerMasks {
   int64_t ffn_stride;
 };
 
-// Rows of a sample up to which the bf16 GEMMs use their narrow tiles.
-constexpr int32_t kSkinnyRows = 256;
+// Rows of a sample up to which the 16-bit MFMA GEMMs count a sample as
+// skinny (one M tile): the output and down projections then split K so the
+// launch still covers the CUs.
+constexpr int32_t kSkinnyRows = MFMA_BM;
+// Workgroups a launch aims for (one per CU).
+constexpr int32_t kTargetTiles = 256;
 
-// Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks(l)
+// Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks[l]
 // gives layer l's masks.  Returns false with a message on inconsistency.
 bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int32_t* seqlens,
                 int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err);
 
 // Upper bound of the plan image for any masks.
 int64_t plan_bytes_bound(const svl_config& cfg, int32_t B, int32_t nlayers);
+
+// Upper bound of the padded activation rows for B samples and R packed rows.
+inline int64_t padded_rows_bound(const svl_config& cfg, int32_t B, int32_t R) {
+  return cfg.dtype == SVL_BF16 ? (int64_t)R + 15 * (int64_t)B : (int64_t)R;
+}
+
+// Rows of float32 partial slices the workspace holds (split pieces x rows).
+inline int64_t partial_rows_bound(const svl_config& cfg, int32_t R) {
+  if (cfg.dtype != SVL_BF16) return 0;
+  const int64_t r = (int64_t)R * MFMA_MAX_SPLIT;
+  return r < MFMA_PARTIAL_ROWS ? r : MFMA_PARTIAL_ROWS;
+}
 
 }  // namespace svl

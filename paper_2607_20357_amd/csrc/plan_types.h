@@ -9,30 +9,48 @@ namespace svl {
 // ---------------------------------------------------------------------------
 // Plan descriptors (built on the host, copied once per call into the
 // workspace, read by the kernels).
+//
+// Row spaces.  The residual stream uses the caller's packed rows (sample b
+// at rows cu[b] .. cu[b+1]-1).  On the 16-bit MFMA path the activation
+// buffers of the workspace (normed input, Q/K/V, attention output, FFN
+// hidden) give every sample a whole number of 16-row blocks: sample b starts
+// at padded row pcu[b] = sum over earlier samples of round_up(S, 16).  On the
+// float32 path both spaces coincide.
 
-// A run of packed rows belonging to one sample.
-struct Seg {
-  int32_t row0;    // first packed row
-  int32_t nrows;   // rows in the run
-  int32_t prefix;  // sum of nrows of the earlier runs in the same list
-  int32_t pos0;    // RoPE position of the first row (0: a whole sample)
+// Rows of one sample handled by a residual / RMSNorm launch.
+enum NormFlags : int32_t {
+  NORM_ADD_PARTIALS = 1,   // resid += the split-K partial slices, written back
+  NORM_WRITE_OUT = 2,      // write the normed rows
+};
+struct NormSeg {
+  int32_t row0;    // first residual row
+  int32_t prow0;   // first activation row (padded space)
+  int32_t nrows;
+  int32_t prefix;  // sum of nrows of the earlier segments of the launch
+  int32_t flags;   // NormFlags
+  int32_t pad0, pad1, pad2;
 };
 
 // One (sample, output-column range) pair of a GEMM launch.  Its tiles are
-// ceil(nrows/BM) x ceil((n1-n0)/BNO), enumerated M tile fastest, starting at
-// tile index tile0 of the launch (BNO: output columns per tile).
+// nsplit x ceil(nrows/BM) x ceil((n1-n0)/BNO), enumerated split fastest, then
+// M tile, then N tile, starting at tile index tile0 of the launch (BNO:
+// output columns per tile).
 struct GemmGroup {
-  int32_t row0, nrows;  // rows of A (and of the output) in the packed space
+  int32_t arow0;        // first row of A (activation row space)
+  int32_t orow0;        // first output row (residual rows for RESID / PARTIAL,
+                        // activation rows otherwise)
+  int32_t nrows;
   int32_t n0, n1;       // output columns [n0, n1)
   int32_t kc_off;       // first entry of this group's K chunks in the chunk table
   int32_t kc_cnt;       // number of K chunks
+  int32_t nsplit;       // split-K pieces (PARTIAL epilogue only)
   int32_t tile0;        // first tile index of the group
-  int32_t pad0;
+  int32_t pad0, pad1, pad2;
 };
 
 // One sample of an attention launch: one workgroup per (active head, q tile).
 struct AttnGroup {
-  int32_t row0, S;      // packed rows of the sample, sequence length
+  int32_t row0, S;      // first activation row of the sample, sequence length
   int32_t h_off, h_cnt; // active query heads: head_table[h_off .. h_off+h_cnt)
   int32_t nqt;          // query tiles
   int32_t tile0;        // first workgroup index of the group
@@ -46,11 +64,26 @@ struct KChunk {
 
 // ---------------------------------------------------------------------------
 // Tile sizes (the planner and the kernels must agree).
-// bf16: 128-row tiles; the tile width BN (weight rows per tile) is chosen per
-// launch from {32, 64, 128} (gate/up tiles hold BN/2 channels).
-constexpr int BF16_BM = 128, BF16_BK = 64;
+// 16-bit MFMA path: 256-row tiles (8 waves x 32 rows); the tile width BN
+// (weight rows per tile) is chosen per launch from {64, 128} (gate/up tiles
+// hold BN/2 channels); K walks in chunks of 64.
+constexpr int MFMA_BM = 256, MFMA_BK = 64;
+constexpr int MFMA_MAX_SPLIT = 8;
+constexpr int MFMA_PARTIAL_ROWS = 4096;   // split pieces x rows the partial buffer holds
 constexpr int F32_BM = 64, F32_BN = 64, F32_BK = 16;
 constexpr int F32_SWIGLU_CH = 32;
 constexpr int ATTN_BQ = 64;          // query rows per attention workgroup
+
+// Fragment-packed activation layout (16-bit MFMA path).  A matrix with K
+// columns (K % 64 == 0) is stored as blocks of 16 rows x 64 columns, 2 KB
+// each, block (row/16, k/64) at block index (row/16) * (K/64) + k/64.  Inside
+// a block, the element (r, k) sits at
+//   ((k / 8) % 2) * 512 + (((k / 16) % 4) * 16 + r % 16) * 8 + k % 8,
+// i.e. the first halves of the MFMA fragments of all 64 lanes, then the
+// second halves: one 16-byte load per lane reads 1 KB contiguously.
+inline constexpr int64_t packed_index(int64_t r, int64_t k, int64_t K) {
+  return ((r >> 4) * (K >> 6) + (k >> 6)) * 1024 + ((k >> 3) & 1) * 512 +
+         (((k >> 4) & 3) * 16 + (r & 15)) * 8 + (k & 7);
+}
 
 }  // namespace svl

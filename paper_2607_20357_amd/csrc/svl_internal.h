@@ -12,10 +12,11 @@
 namespace svl {
 
 enum Epilogue : int32_t {
-  EPI_STORE = 0,   // out[row][col] = acc (activation dtype)
-  EPI_RESID = 1,   // resid[row][col] += acc (float32)
-  EPI_SWIGLU = 2,  // out[row][ch] = silu(gate) * up, gate/up tiles paired
-  EPI_QKV = 3,     // EPI_STORE, with RoPE applied to query / key columns
+  EPI_STORE = 0,    // out[row][col] = acc (float32 path)
+  EPI_RESID = 1,    // resid[row][col] += acc (float32)
+  EPI_SWIGLU = 2,   // out[row][ch] = silu(gate) * up, gate/up tiles paired
+  EPI_QKV = 3,      // store, with RoPE applied to query / key columns
+  EPI_PARTIAL = 4,  // split-K piece p: partial[p][row][col] = acc (float32)
 };
 
 struct GemmArgs {
@@ -34,6 +35,8 @@ struct GemmArgs {
   const float2* rope;  // EPI_QKV: (cos, sin)[pos][head_dim/2]
   int32_t head_dim;    // EPI_QKV: 64 or 128
   int32_t rope_cols;   // EPI_QKV: columns < rope_cols are rotated (Q and K heads)
+  float* partial;      // EPI_PARTIAL: split-K slices, slice p at partial + p * pslice
+  int64_t pslice;
 };
 
 struct AttnArgs {
@@ -43,18 +46,21 @@ struct AttnArgs {
   const void* qkv;     // [rows][(A + 2 KV) d]: Q heads, then K heads, then V heads
   int32_t ldq;         // row stride of qkv
   int32_t n_heads, n_kv_heads;
-  void* out;           // [rows][A d]
+  void* out;           // [rows][A d]: fragment-packed (16-bit) or row-major (float32)
   int32_t ldo;
   const float2* rope;  // (cos, sin)[pos][d/2]; used by kernels that rotate on load
   float scale;         // 1/sqrt(d)
 };
 
 struct NormArgs {
-  const Seg* segs;
+  const NormSeg* segs;
   int32_t nsegs, nrows;
-  const float* x;      // residual [rows][D]
+  float* x;            // residual [rows][D] (written back when partials are added)
+  const float* partial;  // split-K slices to add: slice p at partial + p * pslice
+  int32_t nsplit;
+  int64_t pslice;
   const void* gain;    // [D], weight dtype
-  void* out;           // [rows][D], activation dtype
+  void* out;           // normed rows: fragment-packed (16-bit) or row-major (float32)
   int32_t D;
   float eps;
 };
@@ -67,8 +73,8 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
                          int32_t B, int32_t N, int32_t T, int32_t D, int32_t total_rows,
                          const void* vision, const void* text, int32_t dtype, float* resid,
                          hipStream_t st);
-// out_kind: 0 float32, 1 bf16, 2 fp16
-hipError_t launch_rmsnorm(const NormArgs& a, int32_t out_kind, hipStream_t st);
+// out_kind: 0 float32 row-major, 1 bf16 packed, 2 fp16 packed
+hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st);
 hipError_t launch_gemm_mfma(const GemmArgs& a, int32_t epi, int32_t bn, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
