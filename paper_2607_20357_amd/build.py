@@ -23,7 +23,7 @@ SOURCES = ["abi.cpp", "plan.cpp", "select_gather.hip", "norm_misc.hip", "gemm_mf
            "attn_mfma.hip", "fp32_path.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC",
           # no packed-fp32 instructions anywhere in the device code
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-result", f"-I{os.path.join(ROOT, 'include')}"]

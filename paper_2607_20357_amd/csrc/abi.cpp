@@ -127,7 +127,7 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
     off = align256(off + bytes);
     return o;
   };
-  L.plan = take(plan_bytes_bound(c, B, c.n_layers));
+  L.plan = take(plan_bytes_bound(c, B, R, c.n_layers));
   L.rope = take(std::max<int64_t>(R, 1) * (c.head_dim / 2) * 8);
   L.partial = take(partial_rows_bound(c, R) * c.d_model * 4);
   L.partial_slice = (int64_t)R * c.d_model;
@@ -168,10 +168,30 @@ struct Exec {
     a.rope_cols = (c.n_heads + c.n_kv_heads) * c.head_dim;
     a.partial = reinterpret_cast<float*>(ws + L.partial);
     a.pslice = L.partial_slice;
-    const bool bf16 = c.dtype == SVL_BF16;
+    return timed(cls, st, [&] { return launch_gemm_f32(a, epi, st); });
+  }
+
+  // 16-bit MFMA GEMM over the launch's tile table.  W holds up to three
+  // weight matrices with their row counts.
+  hipError_t mm(const GemmLaunch& g, const KChunk* chunks, const void* A, int lda,
+                const void* const (&W)[3], const int32_t (&w_rows)[3], int ldw, void* out, int ldo,
+                int epi, int cls) const {
+    if (g.ntiles == 0) return hipSuccess;
+    MmArgs a{};
+    a.groups = at<MmGroup>(g.groups_off);
+    a.tiles = at<MmTile>(g.tiles_off);
+    a.ntiles = g.ntiles;
+    a.chunks = chunks;
+    a.A = A; a.lda = lda;
+    for (int i = 0; i < 3; ++i) { a.W[i] = W[i]; a.w_rows[i] = w_rows[i]; }
+    a.ldw = ldw;
+    a.out = out; a.ldo = ldo;
+    a.rope = reinterpret_cast<const float2*>(ws + L.rope);
+    a.head_dim = c.head_dim;
+    a.partial = reinterpret_cast<float*>(ws + L.partial);
+    a.pslice = L.partial_slice;
     return timed(cls, st, [&] {
-      return bf16 ? launch_gemm_mfma(a, epi, g.bn, c.compute == SVL_COMPUTE_F16, st)
-                  : launch_gemm_f32(a, epi, st);
+      return launch_gemm_mfma(a, epi, g.nb, c.compute == SVL_COMPUTE_F16, st);
     });
   }
 
@@ -205,9 +225,15 @@ struct Exec {
     hipError_t e = hipSuccess;
     if ((e = norm(P.norm_attn, w.attn_norm)) != hipSuccess) return e;
     if (P.qkv.ntiles > 0) {
-      if ((e = gemm(P.qkv, chunks, ws + L.xn, D, w.wq, w.wk, w.wv, D, A * d, (A + KV) * d,
-                    ws + L.qkv, qkv_w, mfma ? EPI_QKV : EPI_STORE, K_QKV)) != hipSuccess)
-        return e;
+      if (mfma) {
+        const void* const W[3] = {w.wq, w.wk, w.wv};
+        const int32_t rows[3] = {A * d, KV * d, KV * d};
+        e = mm(P.qkv, chunks, ws + L.xn, D, W, rows, D, ws + L.qkv, qkv_w, EPI_QKV, K_QKV);
+      } else {
+        e = gemm(P.qkv, chunks, ws + L.xn, D, w.wq, w.wk, w.wv, D, A * d, (A + KV) * d,
+                 ws + L.qkv, qkv_w, EPI_STORE, K_QKV);
+      }
+      if (e != hipSuccess) return e;
       AttnArgs a{};
       a.groups = at<AttnGroup>(P.attn.groups_off);
       a.ngroups = P.attn.ngroups;
@@ -226,18 +252,35 @@ struct Exec {
                     : launch_attn_f32(a, d, st);
       });
       if (e != hipSuccess) return e;
-      if ((e = gemm(P.o, chunks, ws + L.attn_out, A * d, w.wo, nullptr, nullptr, A * d, 0, 0, resid,
-                    D, resid_epi(P.o), K_O)) != hipSuccess)
-        return e;
+      if (mfma) {
+        const void* const W[3] = {w.wo, nullptr, nullptr};
+        const int32_t rows[3] = {D, 0, 0};
+        e = mm(P.o, chunks, ws + L.attn_out, A * d, W, rows, A * d, resid, D, resid_epi(P.o), K_O);
+      } else {
+        e = gemm(P.o, chunks, ws + L.attn_out, A * d, w.wo, nullptr, nullptr, A * d, 0, 0, resid,
+                 D, resid_epi(P.o), K_O);
+      }
+      if (e != hipSuccess) return e;
     }
     if ((e = norm(P.norm_ffn, w.ffn_norm)) != hipSuccess) return e;
     if (P.gu.ntiles > 0) {
-      if ((e = gemm(P.gu, chunks, ws + L.xn, D, w.w_gate, w.w_up, nullptr, D, 0, 0, ws + L.h, F,
-                    EPI_SWIGLU, K_GU)) != hipSuccess)
-        return e;
-      if ((e = gemm(P.down, chunks, ws + L.h, F, w.w_down, nullptr, nullptr, F, 0, 0, resid, D,
-                    resid_epi(P.down), K_DOWN)) != hipSuccess)
-        return e;
+      if (mfma) {
+        const void* const Wg[3] = {w.w_gate, w.w_up, nullptr};
+        const int32_t rg[3] = {F, F, 0};
+        if ((e = mm(P.gu, chunks, ws + L.xn, D, Wg, rg, D, ws + L.h, F, EPI_SWIGLU, K_GU)) !=
+            hipSuccess)
+          return e;
+        const void* const Wd[3] = {w.w_down, nullptr, nullptr};
+        const int32_t rd[3] = {D, 0, 0};
+        e = mm(P.down, chunks, ws + L.h, F, Wd, rd, F, resid, D, resid_epi(P.down), K_DOWN);
+      } else {
+        if ((e = gemm(P.gu, chunks, ws + L.xn, D, w.w_gate, w.w_up, nullptr, D, 0, 0, ws + L.h, F,
+                      EPI_SWIGLU, K_GU)) != hipSuccess)
+          return e;
+        e = gemm(P.down, chunks, ws + L.h, F, w.w_down, nullptr, nullptr, F, 0, 0, resid, D,
+                 resid_epi(P.down), K_DOWN);
+      }
+      if (e != hipSuccess) return e;
     }
     return hipSuccess;
   }

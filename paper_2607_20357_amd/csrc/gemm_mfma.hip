@@ -1,49 +1,49 @@
 // Masked grouped GEMM on 16-bit MFMA (gfx950 v_mfma_f32_16x16x32_{f16,bf16}).
 //
-//   C[rows, cols] = sum over the group's K chunks of A[rows, k] * W[cols, k]
+//   C[rows, cols] = sum over the tile's K chunks of A[rows, k] * W[cols, k]
 //
-// A is an activation matrix in the fragment-packed layout (see plan_types.h:
+// A is an activation matrix in the fragment-packed layout (plan_types.h:
 // 16-row x 64-column blocks of 2 KB, fp16 or bf16); W a bf16 weight matrix
 // in [out][in] layout.  With fp16 activations each weight tile is widened
 // bf16 -> fp16 on its way into LDS (exact inside fp16's range), so both
 // operands of the fp16 MFMA carry 11-bit significands; with bf16 activations
 // the weights go through unchanged.  Accumulation is float32.
 //
-// A launch is a list of groups (one sample and one active column range each,
-// or one sample and its active K chunks), so weight rows of inactive heads /
-// FFN slices (QKV, gate/up) and weight columns of inactive heads / slices
-// (output and down projections) are never read.
+// The launch is a table of tiles built on the host.  A group is one sample
+// and one active column range (QKV: a run of active heads of one of Q, K, V;
+// gate/up: a run of active FFN slices; output / down projections: all
+// columns, with K restricted to the active heads' / slices' columns), so
+// weight rows and columns of inactive heads and FFN slices are never read.
+// A tile is up to 256 rows of a group times nblk <= NB 16-column blocks
+// times a range of K chunks; the planner balances the block counts so a
+// launch has about one tile per CU (every tile streams the whole activation
+// slice it multiplies, so a launch with fewer, wider tiles reads less).
 //
-// Tile: 256 rows x BN weight rows, 512 threads = 8 waves, wave w owning rows
-// 32w .. 32w+31 (two 16-row MFMA blocks) and all BN columns.  K advances in
+// Workgroup: 512 threads = 8 waves, wave w owning tile rows 32w .. 32w+31
+// (two 16-row MFMA blocks) and all blocks of the tile.  K advances in
 // chunks of 64.  Per chunk:
 //   * each wave loads its own A fragments straight from the packed layout
-//     into registers (two 1 KB contiguous loads per 16-row block: every
-//     cache line fully used, no LDS traffic for A);
-//   * the BN weight rows are loaded cooperatively (16 bytes per thread and
-//     row segment) and staged through LDS, where all eight waves read them;
-// and NS = 3 chunks are in flight (register stages, one LDS buffer per
-// stage); at most 128 VGPRs, so two workgroups share a CU.  A sample of up to 256 rows is one M tile, so each weight tile is
-// streamed from HBM once.  Buffer loads: one resource per operand spans the
-// tile's valid rows, so rows past the tile read as zero.
-//
-// Split-K (skinny output and down projections): a group may be cut into
-// nsplit K ranges; piece p stores its float32 tile into partial slice p.  The
-// next residual-finish kernel adds the slices in order, so no atomics or
-// cross-workgroup synchronisation are needed and the sum order is fixed.
+//     into registers (two 1 KB contiguous loads per 16-row block);
+//   * the tile's weight rows are loaded cooperatively (16 bytes per thread
+//     and row segment) and staged through LDS, where all eight waves read
+//     them.
+// The weights are staged KS = 4 chunks at a time (one barrier per stage,
+// so the waves drift freely inside a stage), double-buffered in LDS with one
+// or two further stages in flight in registers; A runs KS chunks ahead.
+// Loads are buffer loads whose range ends at the last valid row, so rows
+// past the tile read as zero.
 //
 // Epilogues:
-//   QKV: store row-major; query and key columns are first rotated by RoPE at
-//     the row's position inside its sample (the float32 accumulators are
-//     rotated, so Q and K are rounded once).  A tile holds BN/2 dims of the
-//     first half of a head and the same dims of the second half, so one lane
-//     holds both members (r, r + d/2) of each rotation pair;
-//   RESID: add into the float32 residual;
-//   PARTIAL: store the float32 split-K piece;
-//   SWIGLU: the tile's weight rows are BN/2 gate rows followed by the BN/2
-//     matching up rows, so one lane holds the gate and the up value of a
-//     channel; silu(gate) * up is stored fragment-packed for the down GEMM.
+//   QKV (paired): RoPE at the row's position inside its sample is applied to
+//     the float32 accumulators of query and key groups (partner value from
+//     lane ^ 8), then the 16-bit result is stored row-major;
+//   SWIGLU (paired): silu(gate) * up, stored fragment-packed for the down
+//     projection;
+//   RESID (plain): added into the float32 residual;
+//   PARTIAL (plain): split-K piece stored into its float32 partial slice; the
+//     next residual-finish kernel adds the slices in slice order.
 #include <type_traits>
+#include <utility>
 
 #include "svl_internal.h"
 #include "device_util.h"
@@ -52,17 +52,38 @@ namespace svl {
 namespace {
 
 constexpr int BM = MFMA_BM, NWAVE = 8, NT = NWAVE * 64;
-constexpr int LDS_STRIDE = MFMA_BK + 8;   // 16-bit elements per LDS row (144 B)
-constexpr int MAX_CHUNKS = 1024;          // K chunks per group (K <= 65536)
-constexpr int NS = 3;                     // chunks in flight
+constexpr int KS = 4;                          // K chunks per weight stage (one barrier each)
+constexpr int LDS_STRIDE = KS * MFMA_BK;       // 16-bit elements per LDS row (512 B, 32 units)
+constexpr int MAX_CHUNKS = 1024;               // K chunks per tile (K <= 65536)
+constexpr int NSA = KS;                        // A chunks in flight (stage = chunk % KS)
 
 // Raw buffer resource over [p, p + bytes): loads past the end return zero.
+// The inputs are wave-uniform; readfirstlane keeps the descriptor in scalar
+// registers even where the compiler cannot prove it (a descriptor it takes
+// for divergent costs a loop over lanes at every load).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint64_t ua = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(ua), (short)0,
+                                           __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000);
 }
 
 __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// LDS row swizzle.  gfx950's LDS serves a 16-byte-per-lane access half a
+// wave at a time, 512 bytes over 128 four-byte banks, so the 32 lanes must
+// hit 32 distinct 16-byte units modulo 32.  A weight row of a stage is 32
+// units (4 chunks x 8); unit v of tile row r is stored at v ^ swz(r).  The
+// fragment reads (16 rows x lane groups 0, 1 or 2, 3) and the stores (one
+// row's 32 units per half wave) are then conflict-free.
+__device__ __forceinline__ int swz(int r) { return (r & 1) | (((r >> 1) & 7) << 2); }
+
+// Weights are streamed once: non-temporal loads.
+__device__ __forceinline__ uint4 load16w(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2));
 }
 
 template <bool F16>
@@ -75,103 +96,99 @@ __device__ __forceinline__ uint4 weight_to_act(const uint4& v) {
   }
 }
 
-template <int EPI, int BN, bool F16>
-__global__ __launch_bounds__(NT, 2) void gemm_mfma_kernel(GemmArgs a) {
-  constexpr int NB = BN / 16;                             // 16-column blocks per wave
-  constexpr int BNO = (EPI == EPI_SWIGLU) ? BN / 2 : BN;  // output columns per tile
-  constexpr int WLD = (BN * 8 + NT - 1) / NT;             // 16-byte W loads per thread
-  constexpr int WROWS = NT / 8;                           // W rows one load round covers
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[NS][BN * LDS_STRIDE];
-  __shared__ int32_t s_k0[MAX_CHUNKS];   // the piece's chunk offsets (LDS, no vmcnt waits)
+template <int P>
+using Phase = std::integral_constant<int, P>;
+
+template <int EPI, int NB, bool F16>
+__global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
+  constexpr int BN = NB * 16;                   // weight rows per tile
+  constexpr int NWS = NB <= 5 ? 2 : 1;          // weight register stages
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
+  __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
 
   const int t = xcd_tile_index();
   if (t >= a.ntiles) return;
-  const GemmGroup g = a.groups[find_group(a.groups, a.ngroups, t)];
-  const int local = t - g.tile0;
-  const int split = local % g.nsplit, rest = local / g.nsplit;
-  const int nm = (g.nrows + BM - 1) / BM;
-  const int mt = rest % nm, nt = rest / nm;
-  const int mcnt = min(BM, g.nrows - mt * BM);
-  const int n0 = g.n0 + nt * BNO;
-  const int ncnt = min(BNO, g.n1 - n0);
-  const int kb = g.kc_off + (g.kc_cnt * split) / g.nsplit;
-  const int nk = g.kc_off + (g.kc_cnt * (split + 1)) / g.nsplit - kb;
-
+  const MmTile tl = a.tiles[t];
+  const MmGroup g = a.groups[tl.group];
+  const int mcnt = min(BM, g.nrows - tl.m0);
+  const int nblk = tl.nblk;
+  const int nk = tl.kcn;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int c = tid; c < nk; c += NT) s_k0[c] = a.chunks[kb + c].k0;
+  for (int c = tid; c < nk; c += NT) s_k0[c] = a.chunks[g.kc_off + tl.kc0 + c].k0;
 
-  // QKV: first dim (of the head's first half) this tile holds
-  int hbase = n0, c0 = 0;
-  if constexpr (EPI == EPI_QKV) {
-    hbase = n0 - (n0 % a.head_dim);
-    c0 = ((n0 - hbase) / BN) * (BN / 2);
-  }
+  const int d = a.head_dim, hb = d >> 4;        // QKV: blocks per head
 
-  // A: packed blocks of this tile's rows; wave w reads blocks 2w and 2w+1.
+  // A: packed blocks of this tile's rows; wave w reads 16-row blocks 2w, 2w+1.
   const uint32_t kblocks = (uint32_t)(a.lda / 64);
   const uint32_t blk_bytes = kblocks * 2048u;   // one 16-row block over all of K
-  const int rb0 = (g.arow0 + mt * BM) / 16;
+  const int rb0 = (g.arow0 + tl.m0) / 16;
   const __amdgpu_buffer_rsrc_t rsA =
       make_rsrc(static_cast<const uint16_t*>(a.A) + (size_t)rb0 * kblocks * 1024,
                 (uint32_t)((mcnt + 15) / 16) * blk_bytes);
   uint32_t voA[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) voA[i] = (uint32_t)(2 * wave + i) * blk_bytes + lane * 16u;
+  bool rowblk[2];   // this wave's 16-row blocks hold rows of the tile (wave-uniform)
+#pragma unroll
+  for (int i = 0; i < 2; ++i) rowblk[i] = 32 * wave + 16 * i < mcnt;
 
-  // W: tile rows lr + WROWS i, 16-byte segment lc of the chunk's 128 bytes.
-  const int lc = tid & 7, lr = tid >> 3;
+  // Weights, one stage = KS chunks: piece p = tid + NT*s (s < NB) is unit
+  // p % 32 (chunk u / 8 of the stage, 16-byte segment u % 8) of tile row
+  // p / 32 (block j = row/16, column i = row%16 of the block).  Half a wave
+  // loads 512 bytes of one weight row; a wave's two rows share one column
+  // half of a block (i < 8 or i >= 8), so the matrix choice is wave-uniform.
+  constexpr int WLD = NB;                       // BN * 32 pieces / NT threads
   __amdgpu_buffer_rsrc_t rsB[WLD];
   uint32_t voB[WLD];
+  const int wu = tid & 31, wqc = wu >> 3;       // this thread's unit and chunk of the stage
 #pragma unroll
-  for (int i = 0; i < WLD; ++i) {
-    const int r = lr + WROWS * i;     // tile row (weight row of the tile)
-    const uint16_t* base;
-    int nrows, row;
-    if constexpr (EPI == EPI_SWIGLU) {
-      // rows [0, BN/2) are gate channels n0.., rows [BN/2, BN) the same up
-      // channels; the choice is uniform across a wave
-      const int up = __builtin_amdgcn_readfirstlane(r >= BN / 2 ? 1 : 0);
-      base = static_cast<const uint16_t*>(up ? a.W1 : a.W0) + (size_t)n0 * a.ldw;
-      row = up ? r - BN / 2 : r;
-      nrows = ncnt;
-    } else if constexpr (EPI == EPI_QKV) {
-      const int half = a.head_dim / 2;
-      row = (r < BN / 2) ? c0 + r : half + c0 + (r - BN / 2);
-      nrows = a.head_dim;
-      if (hbase < a.nb1) base = static_cast<const uint16_t*>(a.W0) + (size_t)hbase * a.ldw;
-      else if (hbase < a.nb2) base = static_cast<const uint16_t*>(a.W1) + (size_t)(hbase - a.nb1) * a.ldw;
-      else base = static_cast<const uint16_t*>(a.W2) + (size_t)(hbase - a.nb2) * a.ldw;
+  for (int s = 0; s < WLD; ++s) {
+    const int tr = (tid + NT * s) >> 5;
+    const int j = tr >> 4, i = tr & 15;
+    const int gb = tl.b0 + j;
+    int m = 0, row = 0;
+    if constexpr (EPI == EPI_QKV) {
+      m = g.wsel;
+      row = g.wrow0 + (gb / hb) * d + (gb % hb) * 8 + (i & 7) + ((i >> 3) ? (d >> 1) : 0);
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      m = __builtin_amdgcn_readfirstlane((i >> 3) & 1);   // gate rows, then up rows
+      row = g.wrow0 + gb * 8 + (i & 7);
     } else {
-      base = static_cast<const uint16_t*>(a.W0) + (size_t)n0 * a.ldw;
-      row = r;
-      nrows = ncnt;
+      m = 0;
+      row = g.wrow0 + gb * 16 + i;
     }
-    rsB[i] = make_rsrc(base, (uint32_t)nrows * a.ldw * 2u);
-    // threads past the tile's rows read out of range (zero, no traffic)
-    voB[i] = (r < BN) ? (uint32_t)row * a.ldw * 2u + lc * 16u : 0xfffffff0u;
+    const void* base = m == 0 ? a.W[0] : (m == 1 ? a.W[1] : a.W[2]);
+    const int rows = m == 0 ? a.w_rows[0] : (m == 1 ? a.w_rows[1] : a.w_rows[2]);
+    rsB[s] = make_rsrc(base, (uint32_t)rows * (uint32_t)a.ldw * 2u);
+    // pieces past the tile's blocks read out of range (zero, no traffic)
+    voB[s] = j < nblk ? (uint32_t)row * a.ldw * 2u + (wu & 7) * 16u : 0xfffffff0u;
   }
   __syncthreads();   // s_k0 ready
 
-  // Register stages: stage s holds the A fragments and the W rows of chunk
-  // c = s (mod NS).
-  uint4 sa[NS][2][2], sb[NS][WLD];
-  auto gload = [&](int c, uint4 (&ra)[2][2], uint4 (&rb)[WLD]) {
-    const uint32_t k0 = (uint32_t)__builtin_amdgcn_readfirstlane(s_k0[c]);
-    const uint32_t soA = k0 * 32u, soB = k0 * 2u;
+  const int last = nk - 1;
+  uint4 sa[NSA][2][2], sw[NWS][WLD];
+  auto loadA = [&](int c, uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+    const uint32_t soA = (uint32_t)__builtin_amdgcn_readfirstlane(s_k0[c]) * 32u;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       ra[i][0] = load16(rsA, voA[i], soA);
       ra[i][1] = load16(rsA, voA[i] + 1024u, soA);
     }
-#pragma unroll
-    for (int i = 0; i < WLD; ++i) rb[i] = load16(rsB[i], voB[i], soB);
   };
-  auto wstore = [&](int buf, const uint4 (&rb)[WLD]) {
+  // weight stage S: chunks S*KS .. S*KS + KS-1 (past the last: the last again);
+  // the chunk offset varies across the half wave, so it goes in the lane offset
+  auto loadW = [&](int S, uint4 (&rb)[WLD]) __attribute__((always_inline)) {
+    const uint32_t ko = (uint32_t)s_k0[min(S * KS + wqc, last)] * 2u;
 #pragma unroll
-    for (int i = 0; i < WLD; ++i) {
-      const int r = lr + WROWS * i;
-      if (BN * 8 >= NT * (i + 1) || r < BN)
-        *reinterpret_cast<uint4*>(&Bs[buf][r * LDS_STRIDE + lc * 8]) = weight_to_act<F16>(rb[i]);
+    for (int s = 0; s < WLD; ++s) rb[s] = load16w(rsB[s], voB[s] + ko, 0);
+  };
+  auto wstore = [&](int buf, const uint4 (&rb)[WLD]) __attribute__((always_inline)) {
+    uint16_t* B = Bs + buf * (BN * LDS_STRIDE);
+#pragma unroll
+    for (int s = 0; s < WLD; ++s) {
+      const int tr = (tid + NT * s) >> 5;
+      *reinterpret_cast<uint4*>(&B[tr * LDS_STRIDE + (wu ^ swz(tr)) * 8]) =
+          weight_to_act<F16>(rb[s]);
     }
   };
 
@@ -183,157 +200,201 @@ __global__ __launch_bounds__(NT, 2) void gemm_mfma_kernel(GemmArgs a) {
 
   // Inside a chunk, lane group q = lane / 16 holds k 16q + [0, 8) in the
   // first MFMA k-step and 16q + [8, 16) in the second, for both operands.
-  auto compute = [&](int buf, const uint4 (&ra)[2][2]) {
+  // fragment unit of lane group g in chunk q, k-step ks: q*8 + 2g + ks; the
+  // swizzle of rows j*16 + lane%16 depends on lane%16 only
+  const int fl = (2 * (lane >> 4)) ^ swz(lane & 15);
+  const uint16_t* Bl = Bs + (lane & 15) * LDS_STRIDE;
+  auto compute = [&](int buf, int q, const uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+    const uint16_t* B = Bl + buf * (BN * LDS_STRIDE);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       uint4 bfr[NB];
+      const int u = ((q * 8 + ks) ^ fl) * 8;
 #pragma unroll
       for (int j = 0; j < NB; ++j)
-        bfr[j] = *reinterpret_cast<const uint4*>(
-            &Bs[buf][(j * 16 + (lane & 15)) * LDS_STRIDE + (lane >> 4) * 16 + ks * 8]);
+        if (j < nblk)
+          bfr[j] = *reinterpret_cast<const uint4*>(&B[j * 16 * LDS_STRIDE + u]);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
+        if (rowblk[i])
 #pragma unroll
-        for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
+          for (int j = 0; j < NB; ++j)
+            if (j < nblk) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
     }
   };
 
-  // Pipeline: chunk c is multiplied from registers (A) and LDS buffer c % NS
-  // (W) while chunks c+1 .. c+NS-1 are in flight; the W rows of chunk c+1 go
-  // to LDS right after, and the freed stage is refilled with chunk c+NS.
-  // Past the last chunk the loads repeat the last chunk (cache hits, unused).
+  // Pipeline.  Weight stage S (KS chunks) is multiplied from LDS buffer S % 2
+  // while stages S+1 .. S+NWS are in flight in registers; chunk c's A
+  // fragments sit in register stage c % KS, loaded KS chunks ahead.  After
+  // stage S: stage S+1 goes from registers into the other LDS buffer, one
+  // barrier, and the register stage is refilled with stage S+1+NWS.  Waves
+  // synchronise once per KS chunks.
   if (nk > 0) {
-    const int last = nk - 1;
+    const int nst = (nk + KS - 1) / KS;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) gload(min(s, last), sa[s], sb[s]);
-    wstore(0, sb[0]);
+    for (int s = 0; s < NWS; ++s) loadW(s, sw[s]);
+    [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
+      (loadA(min(Q, last), sa[Q]), ...);
+    }(std::make_integer_sequence<int, KS>{});
+    wstore(0, sw[0]);
+    loadW(NWS, sw[0]);
     __syncthreads();
-    auto step = [&](int cc, auto sc) {
-      constexpr int s = decltype(sc)::value;
-      compute(s, sa[s]);
-      wstore((s + 1) % NS, sb[(s + 1) % NS]);
-      __syncthreads();
-      gload(min(cc + NS, last), sa[s], sb[s]);
+    // FULL: the stage has KS chunks and a successor (no checks, so the
+    // compiler's waits count exactly the loads issued since).
+    auto stage = [&](int S, auto ph, auto full) __attribute__((always_inline)) {
+      constexpr int P = decltype(ph)::value;   // S % NWS
+      constexpr bool FULL = decltype(full)::value;
+      [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
+        ((FULL || S * KS + Q < nk
+              ? (compute(S & 1, Q, sa[Q]), loadA(min(S * KS + Q + KS, last), sa[Q]))
+              : void()),
+         ...);
+      }(std::make_integer_sequence<int, KS>{});
+      if (FULL || S + 1 < nst) {
+        wstore((S + 1) & 1, sw[(P + 1) % NWS]);
+        __syncthreads();
+        loadW(S + 1 + NWS, sw[(P + 1) % NWS]);
+      }
     };
-    // Whole groups of NS chunks: one exit, so the compiler waits on exactly
-    // the oldest stage; then the remaining chunks.
-    int c = 0;
-    static_assert(NS == 3, "the step sequence below is written for three stages");
-    for (; c + NS <= nk; c += NS) {
-      step(c + 0, std::integral_constant<int, 0>{});
-      step(c + 1, std::integral_constant<int, 1>{});
-      step(c + 2, std::integral_constant<int, 2>{});
-    }
-    if (c + 0 < nk) step(c + 0, std::integral_constant<int, 0>{});
-    if (c + 1 < nk) step(c + 1, std::integral_constant<int, 1>{});
+    const int nmain = min(nk / KS, nst - 1);   // full stages with a successor
+    int S = 0;
+    for (; S + NWS <= nmain; S += NWS)
+      [&]<int... P>(std::integer_sequence<int, P...>) __attribute__((always_inline)) {
+        (stage(S + P, Phase<P>{}, std::true_type{}), ...);
+      }(std::make_integer_sequence<int, NWS>{});
+    // at most NWS + 1 stages remain
+    [&]<int... P>(std::integer_sequence<int, P...>) __attribute__((always_inline)) {
+      ((S + P < nst ? stage(S + P, Phase<P % NWS>{}, std::false_type{}) : void()), ...);
+    }(std::make_integer_sequence<int, NWS + 1>{});
   }
 
-  // Epilogue.  acc[i][j][r] is C[wave*32 + i*16 + 4*(lane/16) + r][j*16 + lane%16]
-  // of the tile; tile row m is row mt*BM + m of the group.
+  // Epilogue.  acc[i][j][r] is C[32 wave + 16 i + 4 (lane/16) + r][16 j + lane%16]
+  // of the tile; tile row m is row m0 + m of the group.
   const int rbase = wave * 32 + (lane >> 4) * 4;
-  const int l16 = lane & 15;
+  const int ci = lane & 15;           // column inside the block
   if constexpr (EPI == EPI_QKV) {
     uint16_t* out = static_cast<uint16_t*>(a.out);
-    const bool rot = hbase < a.rope_cols;
-    const int half = a.head_dim >> 1;
+    const int half = d >> 1;
+    // All table loads first, then all stores (a wait on a load issued after
+    // stores would also wait for the stores).
+    float2 cs[2][4][NB];
+    if (g.rope) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rbase + i * 16 + r;
-        const int rowc = min(row, mcnt - 1);
-        const int pos = mt * BM + rowc;
-        uint16_t* orow = out + (size_t)(g.orow0 + pos) * a.ldo + hbase;
+        for (int r = 0; r < 4; ++r) {
+          const int pos = tl.m0 + min(rbase + 16 * i + r, mcnt - 1);
 #pragma unroll
-        for (int j = 0; j < NB / 2; ++j) {
-          // this lane's dims: dim (block j) and dim + d/2 (block j + NB/2)
-          const int dim = c0 + j * 16 + l16;
-          float v1 = acc[i][j][r], v2 = acc[i][j + NB / 2][r];
-          if (rot) {
-            const float2 cs = a.rope[(size_t)pos * half + dim];
-            const float o1 = v1 * cs.x - v2 * cs.y;
-            const float o2 = v2 * cs.x + v1 * cs.y;
-            v1 = o1;
-            v2 = o2;
-          }
-          if (row < mcnt) {   // QKV tiles are always full (ranges are whole heads)
-            orow[dim] = f32_to_act_bits<F16>(v1);
-            orow[dim + half] = f32_to_act_bits<F16>(v2);
+          for (int j = 0; j < NB; ++j) {
+            const int gb = tl.b0 + min(j, nblk - 1);
+            const int dim = (gb % hb) * 8 + (ci & 7);
+            cs[i][r][j] = a.rope[(size_t)pos * half + dim];
           }
         }
-      }
-  } else if constexpr (EPI == EPI_RESID || EPI == EPI_PARTIAL) {
-    float* out = static_cast<float*>(EPI == EPI_PARTIAL ? a.partial + split * a.pslice : a.out);
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = rbase + i * 16 + r;
-        float* orow = out + (size_t)(g.orow0 + mt * BM + min(row, mcnt - 1)) * a.ldo + n0;
+        const int row = rbase + 16 * i + r;
+        uint16_t* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.ldo + g.ocol0;
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          const int col = j * 16 + l16;
-          if (row < mcnt && col < ncnt) {
-            if constexpr (EPI == EPI_RESID) orow[col] += acc[i][j][r];
-            else orow[col] = acc[i][j][r];
+          float v = acc[i][j][r];
+          const float pv = __shfl_xor(v, 8, 64);
+          if (g.rope) {
+            // (x1, x2) -> (x1 cos - x2 sin, x2 cos + x1 sin); lanes ci < 8 hold x1
+            const float2 c2 = cs[i][r][j];
+            v = v * c2.x + ((ci < 8) ? -pv : pv) * c2.y;
           }
+          const int gb = tl.b0 + j;
+          const int col = (gb / hb) * d + (gb % hb) * 8 + (ci & 7) + ((ci >> 3) ? half : 0);
+          if (j < nblk && row < mcnt) orow[col] = f32_to_act_bits<F16>(v);
+        }
+      }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    uint16_t* out = static_cast<uint16_t*>(a.out);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rbase + 16 * i + r;
+        const int64_t prow = g.orow0 + tl.m0 + min(row, mcnt - 1);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const float gt = acc[i][j][r];
+          const float up = __shfl_xor(gt, 8, 64);   // lanes ci < 8: gate, ci >= 8: up
+          const int ch = g.ocol0 + (tl.b0 + j) * 8 + (ci & 7);
+          if (j < nblk && row < mcnt && ci < 8)
+            out[packed_index(prow, ch, a.ldo)] =
+                f32_to_act_bits<F16>(gt / (1.0f + __expf(-gt)) * up);
         }
       }
   } else {
-    uint16_t* out = static_cast<uint16_t*>(a.out);
+    float* out = EPI == EPI_PARTIAL ? a.partial + (size_t)tl.slice * a.pslice
+                                    : static_cast<float*>(a.out);
+    float old[2][4][NB];
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float* orow =
+              out + (size_t)(g.orow0 + tl.m0 + min(rbase + 16 * i + r, mcnt - 1)) * a.ldo + g.ocol0;
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            old[i][r][j] = orow[(tl.b0 + min(j, nblk - 1)) * 16 + ci];
+        }
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = rbase + i * 16 + r;
-        const int64_t prow = g.orow0 + mt * BM + min(row, mcnt - 1);
+        const int row = rbase + 16 * i + r;
+        float* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.ldo + g.ocol0;
 #pragma unroll
-        for (int j = 0; j < NB / 2; ++j) {
-          const int ch = j * 16 + l16;
-          const float gt = acc[i][j][r], up = acc[i][j + NB / 2][r];
-          if (row < mcnt && ch < ncnt)
-            out[packed_index(prow, n0 + ch, a.ldo)] = f32_to_act_bits<F16>(gt / (1.0f + __expf(-gt)) * up);
+        for (int j = 0; j < NB; ++j) {
+          float v = acc[i][j][r];
+          if constexpr (EPI == EPI_RESID) v += old[i][r][j];
+          if (j < nblk && row < mcnt) orow[(tl.b0 + j) * 16 + ci] = v;
         }
       }
   }
 }
 
-template <int EPI, int BN, bool F16>
-hipError_t launch(const GemmArgs& a, hipStream_t st) {
+template <int EPI, int NB, bool F16>
+hipError_t launch(const MmArgs& a, hipStream_t st) {
   const unsigned grid = (unsigned)((a.ntiles + 7) / 8 * 8);
-  gemm_mfma_kernel<EPI, BN, F16><<<grid, NT, 0, st>>>(a);
+  gemm_mfma_kernel<EPI, NB, F16><<<grid, NT, 0, st>>>(a);
   return hipGetLastError();
 }
 
-template <bool F16>
-hipError_t dispatch(const GemmArgs& a, int32_t epi, int32_t bn, hipStream_t st) {
-  switch (epi) {
-    case EPI_QKV:
-      if (bn == 32) return launch<EPI_QKV, 32, F16>(a, st);
-      if (bn == 64) return launch<EPI_QKV, 64, F16>(a, st);
-      if (bn == 128) return launch<EPI_QKV, 128, F16>(a, st);
-      break;
-    case EPI_RESID:
-      if (bn == 64) return launch<EPI_RESID, 64, F16>(a, st);
-      break;
-    case EPI_PARTIAL:
-      if (bn == 64) return launch<EPI_PARTIAL, 64, F16>(a, st);
-      break;
-    case EPI_SWIGLU:
-      if (bn == 64) return launch<EPI_SWIGLU, 64, F16>(a, st);
-      if (bn == 128) return launch<EPI_SWIGLU, 128, F16>(a, st);
-      break;
-    default:
-      break;
+template <int EPI, bool F16>
+hipError_t by_nb(const MmArgs& a, int32_t nb, hipStream_t st) {
+  switch (nb) {
+    case 4: return launch<EPI, 4, F16>(a, st);
+    case 5: return launch<EPI, 5, F16>(a, st);
+    case 8: return launch<EPI, 8, F16>(a, st);
+    default: return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
+}
+
+template <bool F16>
+hipError_t dispatch(const MmArgs& a, int32_t epi, int32_t nb, hipStream_t st) {
+  switch (epi) {
+    case EPI_QKV: return by_nb<EPI_QKV, F16>(a, nb, st);
+    case EPI_SWIGLU: return by_nb<EPI_SWIGLU, F16>(a, nb, st);
+    case EPI_RESID: return by_nb<EPI_RESID, F16>(a, nb, st);
+    case EPI_PARTIAL: return by_nb<EPI_PARTIAL, F16>(a, nb, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
 
-hipError_t launch_gemm_mfma(const GemmArgs& a, int32_t epi, int32_t bn, bool f16, hipStream_t st) {
+hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st) {
   if (a.ntiles <= 0) return hipSuccess;
-  return f16 ? dispatch<true>(a, epi, bn, st) : dispatch<false>(a, epi, bn, st);
+  return f16 ? dispatch<true>(a, epi, nb, st) : dispatch<false>(a, epi, nb, st);
 }
 
 }  // namespace svl

@@ -6,9 +6,10 @@
 //   * the active K chunks of the output and down projections (only active
 //     heads' / slices' weight columns are ever read);
 //   * the active heads of the attention launch.
-// It also picks each 16-bit MFMA GEMM launch's tile width and, for skinny
-// samples, the split-K factor of the output and down projections, so that a
-// launch has about one workgroup per CU.
+// On the 16-bit MFMA path it also cuts every GEMM launch into a tile table:
+// the QKV and gate/up launches spread their column blocks evenly over about
+// one tile per CU; the output and down projections use 4-block tiles and,
+// for skinny samples, split K so the launch still covers the CUs.
 #include "plan.h"
 
 #include <algorithm>
@@ -81,10 +82,103 @@ struct GemmBuild {
     L.groups_off = w.append(groups);
     L.ngroups = (int32_t)groups.size();
     L.ntiles = tile;
-    L.bn = bn;
+    L.nb = bn;
     L.nsplit = nsplit;
     return L;
   }
+};
+
+// 16-bit MFMA GEMM launch: groups, then the tile table.
+struct MmBuild {
+  std::vector<MmGroup> groups;
+  int32_t max_rows = 0, min_chunks = 1 << 30;
+  void add(int32_t arow0, int32_t orow0, int32_t nrows, int32_t wsel, int32_t wrow0,
+           int32_t ocol0, int32_t nblocks, int32_t kc_off, int32_t kc_cnt, int32_t rope) {
+    if (nrows <= 0 || nblocks <= 0 || kc_cnt <= 0) return;
+    MmGroup g{};
+    g.arow0 = arow0; g.orow0 = orow0; g.nrows = nrows; g.wsel = wsel; g.wrow0 = wrow0;
+    g.ocol0 = ocol0; g.kc_off = kc_off; g.kc_cnt = kc_cnt; g.rope = rope; g.nblocks = nblocks;
+    groups.push_back(g);
+    max_rows = std::max(max_rows, nrows);
+    min_chunks = std::min(min_chunks, kc_cnt);
+  }
+  // (group, M tile) pairs' total block count
+  int64_t total_blocks() const {
+    int64_t tb = 0;
+    for (const auto& g : groups) tb += (int64_t)cdiv(g.nrows, MFMA_BM) * g.nblocks;
+    return tb;
+  }
+  // Tiles of `bpt` blocks at most, the blocks of a (group, M tile) split
+  // evenly; tiles that share weight blocks (M tiles) and split-K pieces are
+  // consecutive, so they land on one XCD.
+  GemmLaunch finish(ImageWriter& w, int32_t bpt, int32_t nb, int32_t nsplit) {
+    std::vector<MmTile> tiles;
+    for (int32_t gi = 0; gi < (int32_t)groups.size(); ++gi) {
+      const MmGroup& g = groups[gi];
+      const int32_t nt = cdiv(g.nblocks, bpt), nm = cdiv(g.nrows, MFMA_BM);
+      for (int32_t q = 0; q < nt; ++q) {
+        const int32_t b0 = (int32_t)((int64_t)q * g.nblocks / nt);
+        const int32_t b1 = (int32_t)((int64_t)(q + 1) * g.nblocks / nt);
+        for (int32_t mt = 0; mt < nm; ++mt)
+          for (int32_t p = 0; p < nsplit; ++p) {
+            MmTile t{};
+            t.group = gi; t.m0 = mt * MFMA_BM; t.b0 = b0; t.nblk = b1 - b0;
+            t.kc0 = (int32_t)((int64_t)g.kc_cnt * p / nsplit);
+            t.kcn = (int32_t)((int64_t)g.kc_cnt * (p + 1) / nsplit) - t.kc0;
+            t.slice = p;
+            tiles.push_back(t);
+          }
+      }
+    }
+    GemmLaunch L;
+    L.groups_off = w.append(groups);
+    L.tiles_off = w.append(tiles);
+    L.ngroups = (int32_t)groups.size();
+    L.ntiles = (int32_t)tiles.size();
+    L.nb = nb;
+    L.nsplit = nsplit;
+    return L;
+  }
+  int64_t tiles_for(int32_t bpt) const {
+    int64_t n = 0;
+    for (const auto& g : groups) n += (int64_t)cdiv(g.nrows, MFMA_BM) * cdiv(g.nblocks, bpt);
+    return n;
+  }
+  // QKV and gate/up: blocks per tile by a cost model of the launch time,
+  // (rounds of one tile per CU) x (cost of the widest tile), the tile cost
+  // being its activation rows plus its weight rows (16 per block), the bytes
+  // it streams per K chunk.  A CU that runs two tiles doubles the time; a
+  // wider tile costs little more while its activation rows dominate.
+  GemmLaunch finish_paired(ImageWriter& w) {
+    const int64_t rows = std::min<int64_t>(MFMA_BM, max_rows);
+    int32_t best = 1;
+    int64_t best_cost = -1;
+    for (int32_t bpt = 1; bpt <= MFMA_MAX_NB; ++bpt) {
+      const int64_t rounds = (tiles_for(bpt) + kTargetTiles - 1) / kTargetTiles;
+      const int64_t cost = rounds * (rows + 16 * bpt);
+      if (best_cost < 0 || cost < best_cost) { best = bpt; best_cost = cost; }
+    }
+    // the smallest block count with the same number of rounds
+    const int64_t rounds = (tiles_for(best) + kTargetTiles - 1) / kTargetTiles;
+    while (best > 1 && (tiles_for(best - 1) + kTargetTiles - 1) / kTargetTiles == rounds) --best;
+    return finish(w, best, kernel_nb(best), 1);
+  }
+  // Output and down projections: 4-block tiles; a skinny launch splits K
+  // into float32 partial slices (at least 2 chunks per piece, the slices
+  // within the partial buffer).
+  GemmLaunch finish_plain(ImageWriter& w, int32_t R) {
+    int32_t s = 1;
+    if (!groups.empty() && max_rows <= kSkinnyRows) {
+      int64_t base = 0;
+      for (const auto& g : groups) base += (int64_t)cdiv(g.nrows, MFMA_BM) * cdiv(g.nblocks, 4);
+      s = (int32_t)std::max<int64_t>(1, kTargetTiles / std::max<int64_t>(1, base));
+      s = std::min(s, MFMA_MAX_SPLIT);
+      s = std::min(s, std::max(1, min_chunks / 2));
+      s = std::min(s, std::max(1, MFMA_PARTIAL_ROWS / std::max(1, R)));
+    }
+    return finish(w, 4, 4, s);
+  }
+  static int32_t kernel_nb(int32_t bpt) { return bpt <= 4 ? 4 : (bpt <= 5 ? 5 : 8); }
 };
 
 // K chunks covering [a, b) in pieces of at most `bk` columns.
@@ -94,17 +188,33 @@ void push_chunks(std::vector<KChunk>& ch, int32_t a, int32_t b, int32_t bk) {
 
 }  // namespace
 
-int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t nlayers) {
+int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t R, int32_t nlayers) {
   const int64_t A = c.n_heads, KV = c.n_kv_heads, G = c.n_groups, d = c.head_dim;
   const int64_t F = c.d_ffn, D = c.d_model;
   const int64_t bk = 64;
+  // M tiles over all samples: sum of ceil(S_b / BM) <= B + R / BM
+  const int64_t mts = B + (int64_t)R / MFMA_BM + 1;
+  auto tile_bound = [&](int64_t groups, int64_t blocks) {
+    // (group, M tile) pairs + max(one launch's CU target, blocks / MFMA_MAX_NB);
+    // a split launch keeps its tile count at the CU target
+    const int64_t pairs = groups * mts;
+    const int64_t tb = mts * blocks;
+    return (pairs + std::max<int64_t>(kTargetTiles, tb / MFMA_MAX_NB + 1) +
+            std::max<int64_t>(kTargetTiles, mts * ((blocks + 3) / 4))) *
+               (int64_t)sizeof(MmTile) + 32;
+  };
   int64_t per_layer = 0;
   per_layer += 2 * (B * (int64_t)sizeof(NormSeg) + 16);
   // QKV: at most one range per head (q) and per kv head (k and v)
-  per_layer += B * (A + 2 * KV) * (int64_t)sizeof(GemmGroup) + 16;
-  per_layer += B * (int64_t)sizeof(GemmGroup) + 16;                 // o
-  per_layer += B * G * (int64_t)sizeof(GemmGroup) + 16;             // gate/up
-  per_layer += B * (int64_t)sizeof(GemmGroup) + 16;                 // down
+  const int64_t gsz = std::max<int64_t>(sizeof(GemmGroup), sizeof(MmGroup));
+  per_layer += B * (A + 2 * KV) * gsz + 16;
+  per_layer += B * gsz + 16;                 // o
+  per_layer += B * G * gsz + 16;             // gate/up
+  per_layer += B * gsz + 16;                 // down
+  per_layer += tile_bound(B * (A + 2 * KV), (A + 2 * KV) * d / 16);
+  per_layer += tile_bound(B, D / 16);
+  per_layer += tile_bound(B * G, F / 8);
+  per_layer += tile_bound(B, D / 16);
   per_layer += B * (int64_t)sizeof(AttnGroup) + 16;
   per_layer += B * A * 4 + 16;
   // chunks: dense D, per sample active head columns and FFN slices
@@ -174,17 +284,6 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     return L;
   };
 
-  // split-K factor for a skinny output / down projection launch
-  auto split_for = [&](const GemmBuild& g, int32_t bn) {
-    if (!mfma || g.groups.empty() || g.max_rows > kSkinnyRows) return 1;
-    const int32_t base = g.out_tiles(BM, bn);
-    int32_t s = std::max(1, kTargetTiles / std::max(1, base));
-    s = std::min(s, MFMA_MAX_SPLIT);
-    s = std::min(s, std::max(1, g.min_chunks / 2));          // >= 2 chunks per piece
-    s = std::min(s, std::max(1, MFMA_PARTIAL_ROWS / std::max(1, R)));
-    return s;
-  };
-
   std::vector<uint8_t> kv_on(KV), run_attn(B), run_ffn(B);
   for (int32_t l = 0; l < nlayers; ++l) {
     const LayerMasks& m = masks[l];
@@ -193,7 +292,8 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     push_chunks(chunks, 0, D, bk);   // dense K of the QKV and gate/up GEMMs
     const int32_t dense_cnt = (int32_t)chunks.size();
 
-    GemmBuild qkv, o, gu, down;
+    GemmBuild qkv, o, gu, down;       // float32 path
+    MmBuild mqkv, mo, mgu, mdown;     // 16-bit MFMA path
     std::vector<AttnGroup> ag;
     std::vector<int32_t> heads;
     int32_t attn_tiles = 0;
@@ -209,19 +309,29 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
       if (fm) { for (int32_t j = 0; j < G; ++j) nf += fm[j] ? 1 : 0; } else { nf = G; }
       if (nh > 0) {
         run_attn[b] = 1;
-        for (auto r : runs(hm, A, d, 0)) qkv.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
         for (int32_t g = 0; g < KV; ++g) {
           kv_on[g] = 0;
           for (int32_t h = g * rep; h < (g + 1) * rep; ++h) kv_on[g] |= hm[h];
         }
-        for (auto r : runs(kv_on.data(), KV, d, A * d))
-          qkv.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
-        for (auto r : runs(kv_on.data(), KV, d, (A + KV) * d))
-          qkv.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
+        // (section, weight matrix, active-head mask, heads, first output column)
+        struct Sec { int32_t wsel; const uint8_t* on; int32_t n, col0; };
+        const Sec secs[3] = {{0, hm, A, 0}, {1, kv_on.data(), KV, A * d},
+                             {2, kv_on.data(), KV, (A + KV) * d}};
+        for (const Sec& sc : secs)
+          for (auto r : runs(sc.on, sc.n, d, 0)) {
+            if (mfma)
+              mqkv.add(pcu[b], pcu[b], S, sc.wsel, r.a, sc.col0 + r.a, (r.b - r.a) / 16, 0,
+                       dense_cnt, sc.wsel < 2 ? 1 : 0);
+            else
+              qkv.add(pcu[b], pcu[b], S, sc.col0 + r.a, sc.col0 + r.b, 0, dense_cnt);
+          }
         // output projection: K runs over the active heads' columns of W_o
         int32_t off = (int32_t)chunks.size();
         for (auto r : runs(hm, A, d, 0)) push_chunks(chunks, r.a, r.b, bk);
-        o.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
+        if (mfma)
+          mo.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0);
+        else
+          o.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
         // attention: one group per sample
         AttnGroup g{};
         g.row0 = pcu[b]; g.S = S; g.h_off = (int32_t)heads.size(); g.h_cnt = nh;
@@ -234,22 +344,27 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
         run_ffn[b] = 1;
         std::vector<uint8_t> all(G, 1);
         const uint8_t* fmm = fm ? fm : all.data();
-        for (auto r : runs(fmm, G, slice, 0)) gu.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
+        for (auto r : runs(fmm, G, slice, 0)) {
+          if (mfma)
+            mgu.add(pcu[b], pcu[b], S, 0, r.a, r.a, (r.b - r.a) / 8, 0, dense_cnt, 0);
+          else
+            gu.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
+        }
         int32_t off = (int32_t)chunks.size();
         for (auto r : runs(fmm, G, slice, 0)) push_chunks(chunks, r.a, r.b, bk);
-        down.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
+        if (mfma)
+          mdown.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0);
+        else
+          down.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
       }
     }
 
     // attention sub-block
     LP.norm_attn = norm_launch(run_attn);
     if (mfma) {
-      const bool skinny_a = qkv.max_rows <= kSkinnyRows;
-      const int32_t bn_qkv = skinny_a ? 32 : std::min(128, d);
-      LP.qkv = qkv.finish(w, BM, bn_qkv, bn_qkv, 1);
-      const int32_t bn_o = 64;
-      const int32_t so = split_for(o, bn_o);
-      LP.o = o.finish(w, BM, bn_o, bn_o, so);
+      LP.qkv = mqkv.finish_paired(w);
+      LP.o = mo.finish_plain(w, R);
+      const int32_t so = LP.o.nsplit;
       if (so > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_attn[b];
         pending_split = so;
@@ -266,12 +381,9 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     // FFN sub-block
     LP.norm_ffn = norm_launch(run_ffn);
     if (mfma) {
-      const bool skinny_f = gu.max_rows <= kSkinnyRows;
-      const int32_t bn_gu = skinny_f ? 64 : 128;
-      LP.gu = gu.finish(w, BM, bn_gu / 2, bn_gu, 1);
-      const int32_t bn_d = 64;
-      const int32_t sd = split_for(down, bn_d);
-      LP.down = down.finish(w, BM, bn_d, bn_d, sd);
+      LP.gu = mgu.finish_paired(w);
+      LP.down = mdown.finish_plain(w, R);
+      const int32_t sd = LP.down.nsplit;
       if (sd > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_ffn[b];
         pending_split = sd;

@@ -13,10 +13,13 @@
 namespace svl {
 
 struct GemmLaunch {
-  int64_t groups_off = 0;   // byte offset of the GemmGroup array in the plan image
+  int64_t groups_off = 0;   // byte offset of the group array in the plan image
+                            // (MmGroup on the 16-bit MFMA path, GemmGroup on the
+                            // float32 path)
+  int64_t tiles_off = 0;    // 16-bit MFMA path: byte offset of the MmTile table
   int32_t ngroups = 0;
   int32_t ntiles = 0;
-  int32_t bn = 0;           // weight rows per tile (16-bit MFMA kernels: 64 or 128)
+  int32_t nb = 0;           // 16-bit MFMA path: kernel block count (tiles hold <= nb)
   int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
 };
 
@@ -74,8 +77,8 @@ constexpr int32_t kTargetTiles = 256;
 bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int32_t* seqlens,
                 int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err);
 
-// Upper bound of the plan image for any masks.
-int64_t plan_bytes_bound(const svl_config& cfg, int32_t B, int32_t nlayers);
+// Upper bound of the plan image for any masks (B samples, R packed rows).
+int64_t plan_bytes_bound(const svl_config& cfg, int32_t B, int32_t R, int32_t nlayers);
 
 // Upper bound of the padded activation rows for B samples and R packed rows.
 inline int64_t padded_rows_bound(const svl_config& cfg, int32_t B, int32_t R) {

@@ -48,6 +48,36 @@ struct GemmGroup {
   int32_t pad0, pad1, pad2;
 };
 
+// 16-bit MFMA GEMM.  The output columns of a group are cut into 16-column
+// blocks.  A block of a PLAIN launch (output / down projection) holds 16
+// consecutive columns.  A block of a PAIRED launch holds 8 columns and their
+// 8 partners, so a lane (column i of the block) and lane ^ 8 hold both
+// members of a pair: for QKV the rotary pair (dim, dim + d/2) of a head, 8
+// blocks (d = 128) or 4 blocks (d = 64) per head; for gate/up the gate and
+// the up row of the same FFN channel, 8 channels per block.
+struct MmGroup {
+  int32_t arow0;        // first packed row of A (multiple of 16)
+  int32_t orow0;        // first output row (residual rows for RESID / PARTIAL)
+  int32_t nrows;
+  int32_t wsel;         // weight matrix (QKV: 0 query, 1 key, 2 value; else 0)
+  int32_t wrow0;        // weight row of the group's first column (QKV: first
+                        // head * d; gate/up: first channel; PLAIN: 0)
+  int32_t ocol0;        // output column of the group's first column
+  int32_t kc_off;       // first entry of the group's K chunks in the chunk table
+  int32_t kc_cnt;
+  int32_t rope;         // QKV: rotate (query and key groups)
+  int32_t nblocks;      // 16-column blocks
+  int32_t pad0, pad1;
+};
+
+// One workgroup of a 16-bit MFMA GEMM launch: rows [m0, m0 + 256) of the
+// group, blocks [b0, b0 + nblk), K chunks [kc0, kc0 + kcn) of the group's
+// list; a split-K piece stores its float32 result in partial slice `slice`.
+struct MmTile {
+  int32_t group, m0, b0, nblk;
+  int32_t kc0, kcn, slice, pad0;
+};
+
 // One sample of an attention launch: one workgroup per (active head, q tile).
 struct AttnGroup {
   int32_t row0, S;      // first activation row of the sample, sequence length
@@ -64,11 +94,12 @@ struct KChunk {
 
 // ---------------------------------------------------------------------------
 // Tile sizes (the planner and the kernels must agree).
-// 16-bit MFMA path: 256-row tiles (8 waves x 32 rows); the tile width BN
-// (weight rows per tile) is chosen per launch from {64, 128} (gate/up tiles
-// hold BN/2 channels); K walks in chunks of 64.
+// 16-bit MFMA path: 256-row tiles (8 waves x 32 rows) of up to
+// MFMA_MAX_NB 16-column blocks (the kernel is instantiated for a few block
+// counts, the planner picks one per launch); K walks in chunks of 64.
 constexpr int MFMA_BM = 256, MFMA_BK = 64;
 constexpr int MFMA_MAX_SPLIT = 8;
+constexpr int MFMA_MAX_NB = 8;
 constexpr int MFMA_PARTIAL_ROWS = 4096;   // split pieces x rows the partial buffer holds
 constexpr int F32_BM = 64, F32_BN = 64, F32_BK = 16;
 constexpr int F32_SWIGLU_CH = 32;

@@ -39,6 +39,26 @@ struct GemmArgs {
   int64_t pslice;
 };
 
+// 16-bit MFMA GEMM (tile table built by the planner).
+struct MmArgs {
+  const MmGroup* groups;
+  const MmTile* tiles;
+  int32_t ntiles;
+  const KChunk* chunks;
+  const void* A;         // fragment-packed activations, K = lda
+  int32_t lda;
+  const void* W[3];      // bf16 weight matrices [rows][ldw] (gate/up: W[0] gate, W[1] up)
+  int32_t w_rows[3];     // their row counts (load range)
+  int32_t ldw;
+  void* out;             // QKV: row-major 16-bit [rows][ldo]; SWIGLU: packed 16-bit,
+                         // K = ldo; RESID: float32 residual [rows][ldo]
+  int32_t ldo;
+  const float2* rope;    // QKV: (cos, sin)[pos][head_dim/2]
+  int32_t head_dim;
+  float* partial;        // PARTIAL: slice p at partial + p * pslice, row stride ldo
+  int64_t pslice;
+};
+
 struct AttnArgs {
   const AttnGroup* groups;
   int32_t ngroups, ntiles;
@@ -75,7 +95,7 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
                          hipStream_t st);
 // out_kind: 0 float32 row-major, 1 bf16 packed, 2 fp16 packed
 hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st);
-hipError_t launch_gemm_mfma(const GemmArgs& a, int32_t epi, int32_t bn, bool f16, hipStream_t st);
+hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);
