@@ -44,7 +44,81 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=3,
                    help="executed layers the CPU-baseline sample runs")
+    p.add_argument("--traffic-from", default=None,
+                   help="directory holding fetch/ and write/ rocprofv3 --pmc FETCH_SIZE / "
+                        "WRITE_SIZE runs of `bench.py --copy-calibration`: write the gate/up "
+                        "traffic summary and exit")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run one plain device copy of COPY_BYTES (the known-size kernel "
+                        "that scales the FETCH_SIZE / WRITE_SIZE counters of a --pmc run)")
     return p.parse_args()
+
+
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_20357_amd", "csrc", "gemm_mfma.hip")
+
+
+def source_hash(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def write_traffic(run_dir):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the gate/up GEMM, each
+    scaled by counter / true bytes of the COPY_BYTES calibration copy (the
+    dispatch whose WRITE_SIZE is largest), into TRAFFIC_FILE."""
+    import collections
+    import csv
+
+    def per_dispatch(path):
+        vals, names = collections.defaultdict(float), {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                d = int(r["Dispatch_Id"])
+                vals[d] += float(r["Counter_Value"])
+                names[d] = r["Kernel_Name"]
+        return vals, names
+
+    out = {"gemm_source_sha256": source_hash(GEMM_SOURCE), "copy_bytes": COPY_BYTES}
+    for kind, sub in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
+        path = os.path.join(run_dir, kind, "t_counter_collection.csv")
+        vals, names = per_dispatch(path)
+        copies = [d for d, n in names.items() if "elementwise" in n or "copy" in n.lower()]
+        if kind == "write":
+            cal = max(copies, key=lambda d: vals[d])
+            cal_kib_write = vals[cal]
+        else:
+            # the copy dispatch is the one right before the first prefill kernel
+            first = min(d for d, n in names.items() if "svl::" in n)
+            cal = max(d for d in copies if d < first)
+        factor = COPY_BYTES / (vals[cal] * 1024.0)
+        gu = [vals[d] for d, n in names.items() if "gemm_mfma_kernel<2," in n]
+        out[f"{kind}_kib_per_dispatch_raw"] = sum(gu) / len(gu)
+        out[f"{kind}_calibration_factor"] = factor
+        out[f"{kind}_bytes_per_launch"] = sum(gu) / len(gu) * 1024.0 * factor
+        out[f"{kind}_dispatches"] = len(gu)
+        out[f"{kind}_counter"] = sub
+    out["command"] = ("rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE -d <dir>/fetch|write -o t "
+                      "--output-format csv -- python3 -u bench.py --steps 3 --warmup 1 "
+                      "--no-cpu-baseline --copy-calibration")
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed counter runs, or None
+    when there are none or the GEMM source changed since they were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256") != source_hash(GEMM_SOURCE):
+        return None
+    return t
 
 
 def gemm_bytes(shape, seqlens, layer_mask, head_mask, ffn_mask):
@@ -121,6 +195,9 @@ def cpu_baseline(w, inp, layers, n_exec_layers):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        write_traffic(args.traffic_from)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; multi-GPU runs are not part of "
                                    "it (samples would shard data-parallel, see DESIGN.md)"}))
@@ -154,6 +231,12 @@ def main():
                         inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
                         want_flops=False)
 
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -185,6 +268,7 @@ def main():
     value = tokens / (ms * 1e-3)
 
     bytes_, launches = gemm_bytes(shape, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    traffic = measured_traffic() if w.name == W.HEADLINE else None
     gu_ms, gu_n = ktime["gemm_gate_up"]
     gu_avg_ms = gu_ms / max(1, gu_n)
     gu_bytes_per_launch = bytes_["gu"] / max(1, launches["gu"])
@@ -223,9 +307,12 @@ def main():
         "roofline": {
             "kernel": "gemm_mfma_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": (traffic["fetch_bytes_per_launch"] + traffic["write_bytes_per_launch"])
+            if traffic else None,
             "avg_launch_ms": round(gu_avg_ms, 5),
             "algorithmic_bytes_per_launch": int(gu_bytes_per_launch),
+            "traffic_source": os.path.relpath(TRAFFIC_FILE, ROOT) if traffic else None,
         },
     }
     if not args.no_cpu_baseline:
