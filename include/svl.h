@@ -82,7 +82,9 @@ typedef enum { SVL_COMPUTE_F16 = 0, SVL_COMPUTE_BF16 = 1 } svl_compute;
  * channel range [j*d_ffn/G, (j+1)*d_ffn/G).
  * Requirements: all sizes > 0; n_heads % n_kv_heads == 0; head_dim even;
  * d_ffn % n_groups == 0; for SVL_BF16 also d_model % 64 == 0,
- * head_dim in {64, 128}, d_ffn/n_groups % 64 == 0. */
+ * head_dim in {64, 128}, d_ffn/n_groups % 64 == 0, d_model, d_ffn and
+ * n_heads*head_dim at most 65536, and every weight matrix under 2 GiB
+ * (SVL_E_SHAPE otherwise). */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, n_groups;
   float rms_eps;     /* RMSNorm epsilon */

@@ -95,6 +95,10 @@ svl_status check_config(const svl_config* c, bool for_kernels = true) {
     if ((c->d_ffn / c->n_groups) % 64) return fail(SVL_E_SHAPE, "bf16 path: d_ffn/n_groups %% 64 != 0");
     if (c->d_model > 65536 || c->d_ffn > 65536 || c->n_heads * c->head_dim > 65536)
       return fail(SVL_E_SHAPE, "bf16 path: reduction dimensions above 65536");
+    // the GEMM kernels address a weight matrix with 32-bit byte offsets below 2^31
+    const int64_t D = c->d_model, F = c->d_ffn, Ad = (int64_t)c->n_heads * c->head_dim;
+    if (F * D * 2 >= (int64_t(1) << 31) || Ad * D * 2 >= (int64_t(1) << 31))
+      return fail(SVL_E_SHAPE, "bf16 path: a weight matrix of 2 GiB or more");
   } else {
     if (c->d_model % 4) return fail(SVL_E_SHAPE, "f32 path: d_model %% 4 != 0");
     if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)

@@ -102,7 +102,9 @@ using Phase = std::integral_constant<int, P>;
 template <int EPI, int NB, bool F16>
 __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   constexpr int BN = NB * 16;                   // weight rows per tile
-  constexpr int NWS = NB <= 5 ? 2 : 1;          // weight register stages
+  // weight register stages: about 48 registers' worth, so a narrow tile keeps
+  // more of its (HBM-latency) weight stream in flight
+  constexpr int NWS = NB <= 3 ? 4 : (NB == 4 ? 3 : (NB <= 6 ? 2 : 1));
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
   __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
 
@@ -160,8 +162,10 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     const void* base = m == 0 ? a.W[0] : (m == 1 ? a.W[1] : a.W[2]);
     const int rows = m == 0 ? a.w_rows[0] : (m == 1 ? a.w_rows[1] : a.w_rows[2]);
     rsB[s] = make_rsrc(base, (uint32_t)rows * (uint32_t)a.ldw * 2u);
-    // pieces past the tile's blocks read out of range (zero, no traffic)
-    voB[s] = j < nblk ? (uint32_t)row * a.ldw * 2u + (wu & 7) * 16u : 0xfffffff0u;
+    // pieces past the tile's blocks read out of range (zero, no traffic); the
+    // chunk offset added later (< 2^17) keeps 2^31 out of range without
+    // wrapping (a weight matrix spans less than 2^31 bytes)
+    voB[s] = j < nblk ? (uint32_t)row * a.ldw * 2u + (wu & 7) * 16u : 0x80000000u;
   }
   __syncthreads();   // s_k0 ready
 
@@ -210,16 +214,17 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     for (int ks = 0; ks < 2; ++ks) {
       uint4 bfr[NB];
       const int u = ((q * 8 + ks) ^ fl) * 8;
+      // Blocks past the tile's nblk hold zero weights (their loads read out
+      // of range), so they are multiplied unconditionally: straight-line code
+      // lets the compiler overlap the LDS reads with the MFMAs.
 #pragma unroll
       for (int j = 0; j < NB; ++j)
-        if (j < nblk)
-          bfr[j] = *reinterpret_cast<const uint4*>(&B[j * 16 * LDS_STRIDE + u]);
+        bfr[j] = *reinterpret_cast<const uint4*>(&B[j * 16 * LDS_STRIDE + u]);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
         if (rowblk[i])
 #pragma unroll
-          for (int j = 0; j < NB; ++j)
-            if (j < nblk) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
+          for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
     }
   };
 
@@ -372,8 +377,11 @@ hipError_t launch(const MmArgs& a, hipStream_t st) {
 template <int EPI, bool F16>
 hipError_t by_nb(const MmArgs& a, int32_t nb, hipStream_t st) {
   switch (nb) {
+    case 2: return launch<EPI, 2, F16>(a, st);
+    case 3: return launch<EPI, 3, F16>(a, st);
     case 4: return launch<EPI, 4, F16>(a, st);
     case 5: return launch<EPI, 5, F16>(a, st);
+    case 6: return launch<EPI, 6, F16>(a, st);
     case 8: return launch<EPI, 8, F16>(a, st);
     default: return hipErrorInvalidValue;
   }

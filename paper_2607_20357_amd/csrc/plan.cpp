@@ -178,7 +178,9 @@ struct MmBuild {
     }
     return finish(w, 4, 4, s);
   }
-  static int32_t kernel_nb(int32_t bpt) { return bpt <= 4 ? 4 : (bpt <= 5 ? 5 : 8); }
+  // kernel instantiations: 2, 3, 4, 5, 6, 8 blocks (a tile's unused blocks
+  // still cost their MFMAs, so the kernel is the smallest that fits)
+  static int32_t kernel_nb(int32_t bpt) { return bpt <= 2 ? 2 : (bpt <= 6 ? bpt : 8); }
 };
 
 // K chunks covering [a, b) in pieces of at most `bk` columns.
