@@ -192,7 +192,8 @@ int32_t svl_abi_version(void);
  * then forgets them.  Timing adds event records between launches, so time
  * whole calls with timing off.
  * Kernel classes: 0 select, 1 gather, 2 rmsnorm, 3 qkv gemm, 4 attention,
- * 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope table, 9 other. */
+ * 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope table, 9 split-K finish
+ * (QKV and gate/up launches whose K was split). */
 #define SVL_KCLASS_COUNT 10
 svl_status svl_timing_enable(int32_t on);
 svl_status svl_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libsvl.so")
 SVL_F32, SVL_BF16 = 0, 1
 SVL_COMPUTE_F16, SVL_COMPUTE_BF16 = 0, 1
 KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
-          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "other": 9}
+          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9}
 STATUS = {0: "SVL_OK", 1: "SVL_E_NULL", 2: "SVL_E_SHAPE", 3: "SVL_E_VALUE", 4: "SVL_E_WORKSPACE",
           5: "SVL_E_DTYPE", 6: "SVL_E_HIP", 7: "SVL_E_ALIGN"}
 WEIGHT_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")

@@ -71,7 +71,7 @@ hipError_t timed(int cls, hipStream_t st, F&& f) {
   return r;
 }
 
-enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_OTHER };
+enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_FINISH };
 
 // ------------------------------------------------------------------ validation
 svl_status check_config(const svl_config* c, bool for_kernels = true) {
@@ -116,7 +116,8 @@ svl_status check_mask(const uint8_t* m, int64_t n, const char* what) {
 // ------------------------------------------------------------------ workspace
 struct WsLayout {
   int64_t plan, rope, partial, xn, qkv, attn_out, h, total;
-  int64_t partial_slice;   // floats per split-K slice (R x d_model)
+  int64_t partial_slice;   // floats per split-K slice of the output / down projections (R x d_model)
+  int64_t prows;           // padded activation rows
 };
 
 // Activation buffers use the padded row space (16-row blocks per sample on
@@ -133,8 +134,9 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
   };
   L.plan = take(plan_bytes_bound(c, B, R, c.n_layers));
   L.rope = take(std::max<int64_t>(R, 1) * (c.head_dim / 2) * 8);
-  L.partial = take(partial_rows_bound(c, R) * c.d_model * 4);
+  L.partial = take(partial_floats_bound(c, B, R) * 4);
   L.partial_slice = (int64_t)R * c.d_model;
+  L.prows = prow;
   L.xn = take(prow * c.d_model * es);
   L.qkv = take(prow * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
   L.attn_out = take(prow * (int64_t)c.n_heads * c.head_dim * es);
@@ -193,10 +195,33 @@ struct Exec {
     a.rope = reinterpret_cast<const float2*>(ws + L.rope);
     a.head_dim = c.head_dim;
     a.partial = reinterpret_cast<float*>(ws + L.partial);
-    a.pslice = L.partial_slice;
-    return timed(cls, st, [&] {
-      return launch_gemm_mfma(a, epi, g.nb, c.compute == SVL_COMPUTE_F16, st);
-    });
+    const bool f16 = c.compute == SVL_COMPUTE_F16;
+    const bool paired = epi == EPI_QKV || epi == EPI_SWIGLU;
+    if (paired && g.nsplit > 1) {
+      // split pieces: float32 slices [nsplit][padded rows][pld], then the finish
+      a.split = g.nsplit;
+      a.pld = epi == EPI_QKV ? ldo : 2 * c.d_ffn;
+      a.pslice = plan.padded_rows * (int64_t)a.pld;
+    } else {
+      a.split = 1;
+      a.pld = ldo;
+      a.pslice = L.partial_slice;
+    }
+    hipError_t e = timed(cls, st, [&] { return launch_gemm_mfma(a, epi, g.nb, f16, st); });
+    if (e != hipSuccess || !(paired && g.nsplit > 1)) return e;
+    FinishArgs f{};
+    f.groups = a.groups;
+    f.ngroups = g.ngroups;
+    f.nitems = g.nitems;
+    f.partial = a.partial;
+    f.pslice = a.pslice;
+    f.pld = a.pld;
+    f.nsplit = g.nsplit;
+    f.out = out;
+    f.ldo = ldo;
+    f.rope = a.rope;
+    f.head_dim = c.head_dim;
+    return timed(K_FINISH, st, [&] { return launch_finish(f, epi, f16, st); });
   }
 
   hipError_t norm(const NormLaunch& n, const void* gain) const {

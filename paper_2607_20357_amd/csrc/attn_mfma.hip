@@ -5,7 +5,10 @@
 //
 // One workgroup = one (sample, active query head, 64-row query tile); the
 // launch lists only active heads, so inactive heads are never read or
-// written.  Each of the 4 waves owns 16 query rows.  Scores are formed
+// written.  8 waves: wave w owns 16 query rows (w % 4) and the key tiles of
+// parity w / 4; each half runs its own online softmax and the halves are
+// combined at the end, so a query tile's key range is walked two tiles at a
+// time.  Scores are formed
 // transposed, S^T = K Q^T (kv rows x q columns), so that a lane's
 // accumulator entries all belong to one query (q = lane % 16): the softmax
 // row statistics stay per lane, and the probabilities already sit in the
@@ -24,7 +27,8 @@
 namespace svl {
 namespace {
 
-constexpr int BQ = ATTN_BQ, BKV = 64, NT = 256;
+constexpr int BQ = ATTN_BQ, BKV = 64, NT = 512;
+constexpr int GT = 4;   // key tiles loaded together (one LDS buffer each)
 constexpr float NEG_BIG = -1.0e30f;
 
 template <int D, bool F16>
@@ -33,8 +37,8 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   constexpr int VS = BKV + 8;    // transposed V tile row stride (elements)
   constexpr int NS = D / 32;     // MFMA k-steps over the head dimension
   constexpr int NB = D / 16;     // 16-wide head-dimension blocks of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BKV * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[GT][BKV * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[GT][D * VS];
 
   const int t = blockIdx.x;
   if (t >= a.ntiles) return;
@@ -46,6 +50,8 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   const int kvh = h / (a.n_heads / a.n_kv_heads);
   const int S = g.S, q0 = qt * BQ;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qw = wave & 3;       // 16-row query group
+  const int half = wave >> 2;    // key tiles of parity `half`
   const int gq = lane >> 4, lq = lane & 15;
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
   const size_t ldq = (size_t)a.ldq;
@@ -53,7 +59,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   const int qcol = h * D, kcol = (a.n_heads + kvh) * D, vcol = (a.n_heads + a.n_kv_heads + kvh) * D;
 
   // Query fragments: lane holds Q[qi][32 s + 8 gq + j].
-  const int qi = q0 + wave * 16 + lq;
+  const int qi = q0 + qw * 16 + lq;
   const bool qvalid = qi < S;
   uint4 qf[NS];
   {
@@ -73,34 +79,77 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;   // scores in log2 units
   const int kv_end = min(S, q0 + BQ);
 
-  for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
-    __syncthreads();
-    // K tile: task = (row, 16-byte chunk).
-    for (int task = tid; task < BKV * (D / 8); task += NT) {
-      const int row = task / (D / 8), c = task % (D / 8);
-      const int kv = kv0 + row;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kv < S) v = *reinterpret_cast<const uint4*>(base + (size_t)kv * ldq + kcol + 8 * c);
-      *reinterpret_cast<uint4*>(&Ks[row * KS + 8 * c]) = v;
-    }
-    // V tile, transposed: task = (row pair, 8-column chunk).
-    for (int task = tid; task < (BKV / 2) * (D / 8); task += NT) {
-      const int pr = task / (D / 8), c = task % (D / 8);
-      const int kva = kv0 + 2 * pr, kvb = kva + 1;
-      uint4 va = make_uint4(0, 0, 0, 0), vb = va;
-      if (kva < S) va = *reinterpret_cast<const uint4*>(base + (size_t)kva * ldq + vcol + 8 * c);
-      if (kvb < S) vb = *reinterpret_cast<const uint4*>(base + (size_t)kvb * ldq + vcol + 8 * c);
-      const uint32_t aw[4] = {va.x, va.y, va.z, va.w}, bw[4] = {vb.x, vb.y, vb.z, vb.w};
+  // Keys are handled in groups of GT tiles of 64: the group's K and V are
+  // loaded into registers all at once (one memory round trip per group;
+  // a sequence of up to 256 tokens is a single group), stored into GT LDS
+  // buffers, and the next group's loads are issued before the tiles are
+  // multiplied.  Buffer loads over the sample's rows (range S rows) read
+  // rows past the sample as zero, without branches.
+  constexpr int KTASKS = BKV * (D / 8), VTASKS = (BKV / 2) * (D / 8);
+  constexpr int KT = (KTASKS + NT - 1) / NT;     // K tile: 16-byte pieces per thread
+  constexpr int VT = (VTASKS + NT - 1) / NT;     // V tile: row pairs per thread
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(base), (short)0, (int)((uint32_t)S * (uint32_t)ldq * 2u), 0x00020000);
+  uint4 kr[GT][KT], va[GT][VT], vb[GT][VT];
+  auto load_group = [&](int g0) __attribute__((always_inline)) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = (aw[j] & 0xffffu) | (bw[j] << 16);
-        const uint32_t hi = (aw[j] >> 16) | (bw[j] & 0xffff0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(8 * c + 2 * j) * VS + 2 * pr]) = lo;
-        *reinterpret_cast<uint32_t*>(&Vt[(8 * c + 2 * j + 1) * VS + 2 * pr]) = hi;
+    for (int j = 0; j < GT; ++j) {
+      const int kv0 = g0 + j * BKV;
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        const int task = min(tid + i * NT, KTASKS - 1), row = task / (D / 8), c = task % (D / 8);
+        kr[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+            rs, (uint32_t)((kv0 + row) * ldq + kcol + 8 * c) * 2u, 0, 0));
+      }
+#pragma unroll
+      for (int i = 0; i < VT; ++i) {
+        const int task = min(tid + i * NT, VTASKS - 1), pr = task / (D / 8), c = task % (D / 8);
+        const uint32_t off = (uint32_t)((kv0 + 2 * pr) * ldq + vcol + 8 * c) * 2u;
+        va[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+        vb[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+            rs, off + (uint32_t)ldq * 2u, 0, 0));
       }
     }
+  };
+  auto store_group = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < GT; ++j) {
+#pragma unroll
+      for (int i = 0; i < KT; ++i) {
+        const int task = tid + i * NT, row = task / (D / 8), c = task % (D / 8);
+        if (KTASKS % NT == 0 || task < KTASKS)
+          *reinterpret_cast<uint4*>(&Ks[j][row * KS + 8 * c]) = kr[j][i];
+      }
+      // V transposed: rows 2pr, 2pr+1 interleaved into 32-bit pairs
+#pragma unroll
+      for (int i = 0; i < VT; ++i) {
+        const int task = tid + i * NT, pr = task / (D / 8), c = task % (D / 8);
+        if (VTASKS % NT != 0 && task >= VTASKS) continue;
+        const uint32_t aw[4] = {va[j][i].x, va[j][i].y, va[j][i].z, va[j][i].w};
+        const uint32_t bw[4] = {vb[j][i].x, vb[j][i].y, vb[j][i].z, vb[j][i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = (aw[e] & 0xffffu) | (bw[e] << 16);
+          const uint32_t hi = (aw[e] >> 16) | (bw[e] & 0xffff0000u);
+          *reinterpret_cast<uint32_t*>(&Vt[j][(8 * c + 2 * e) * VS + 2 * pr]) = lo;
+          *reinterpret_cast<uint32_t*>(&Vt[j][(8 * c + 2 * e + 1) * VS + 2 * pr]) = hi;
+        }
+      }
+    }
+  };
+  load_group(0);
+  for (int g0 = 0; g0 < kv_end; g0 += GT * BKV) {
+    __syncthreads();   // the previous group's readers are done
+    store_group();
     __syncthreads();
-
+    if (g0 + GT * BKV < kv_end) load_group(g0 + GT * BKV);
+#pragma unroll
+    for (int j = 0; j < GT; ++j) {
+    const int kv0 = g0 + j * BKV;
+    if (kv0 >= kv_end) break;
+    if (((kv0 / BKV) & 1) != half) continue;   // the other half's tile
+    const uint16_t* Kt = Ks[j];
+    const uint16_t* Vtt = Vt[j];
     // S^T = K Q^T for the four 16-row kv blocks.
     floatx4 st[4];
 #pragma unroll
@@ -108,7 +157,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
       st[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const uint4 kf = *reinterpret_cast<const uint4*>(&Ks[(16 * i + lq) * KS + 32 * s + 8 * gq]);
+        const uint4 kf = *reinterpret_cast<const uint4*>(&Kt[(16 * i + lq) * KS + 32 * s + 8 * gq]);
         st[i] = mfma16x16x32<F16>(kf, qf[s], st[i]);
       }
     }
@@ -132,7 +181,8 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(st[i][r] - m_new);
+        // masked keys contribute exactly 0 (a half may see only masked keys)
+        const float p = st[i][r] > 0.5f * NEG_BIG ? exp2f(st[i][r] - m_new) : 0.f;
         st[i][r] = p;
         lsum += p;
       }
@@ -150,14 +200,41 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
                                   pack_act2<F16>(st[2 * t2 + 1][2], st[2 * t2 + 1][3]));
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const uint16_t* vr = &Vt[(16 * b + lq) * VS + 32 * t2 + 4 * gq];
+        const uint16_t* vr = &Vtt[(16 * b + lq) * VS + 32 * t2 + 4 * gq];
         const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
         const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 16);
         o[b] = mfma16x16x32<F16>(make_uint4(v0.x, v0.y, v1.x, v1.y), pb, o[b]);
       }
     }
+    }
   }
 
+  // Combine the two halves: the odd-tile waves hand (m, l, o) to the even
+  // ones through LDS (the K buffers, free after the barrier).
+  constexpr int CW = 2 + 4 * NB;   // floats per lane
+  static_assert(4 * 64 * CW * 4 <= (int)sizeof(Ks), "combine buffer");
+  float* comb = reinterpret_cast<float*>(&Ks[0][0]) + (qw * 64 + lane) * CW;
+  __syncthreads();
+  if (half == 1) {
+    comb[0] = m_i;
+    comb[1] = l_i;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) comb[2 + 4 * b + r] = o[b][r];
+  }
+  __syncthreads();
+  if (half == 1) return;
+  {
+    const float m1 = comb[0], l1 = comb[1];
+    const float m = fmaxf(m_i, m1);
+    const float a0 = exp2f(m_i - m), a1 = exp2f(m1 - m);
+    l_i = l_i * a0 + l1 * a1;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[b][r] = o[b][r] * a0 + comb[2 + 4 * b + r] * a1;
+  }
   l_i += __shfl_xor(l_i, 16, 64);
   l_i += __shfl_xor(l_i, 32, 64);
   if (qvalid) {

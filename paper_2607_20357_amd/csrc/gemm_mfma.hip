@@ -102,9 +102,7 @@ using Phase = std::integral_constant<int, P>;
 template <int EPI, int NB, bool F16>
 __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   constexpr int BN = NB * 16;                   // weight rows per tile
-  // weight register stages: about 48 registers' worth, so a narrow tile keeps
-  // more of its (HBM-latency) weight stream in flight
-  constexpr int NWS = NB <= 3 ? 4 : (NB == 4 ? 3 : (NB <= 6 ? 2 : 1));
+  constexpr int NWS = NB <= 6 ? 2 : 1;          // weight register stages
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
   __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
 
@@ -277,6 +275,31 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   // of the tile; tile row m is row m0 + m of the group.
   const int rbase = wave * 32 + (lane >> 4) * 4;
   const int ci = lane & 15;           // column inside the block
+  if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {
+    if (a.split > 1) {
+      // split-K piece: raw float32 accumulators at the output column (QKV) or
+      // at the gate / up column (SWIGLU); the finish kernel does the rest
+      float* out = a.partial + (size_t)tl.slice * a.pslice;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = rbase + 16 * i + r;
+          float* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.pld;
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const int gb = tl.b0 + j;
+            int col;
+            if constexpr (EPI == EPI_QKV)
+              col = g.ocol0 + (gb / hb) * d + (gb % hb) * 8 + (ci & 7) + ((ci >> 3) ? (d >> 1) : 0);
+            else
+              col = ((ci >> 3) ? (a.pld >> 1) : 0) + g.ocol0 + gb * 8 + (ci & 7);
+            if (j < nblk && row < mcnt) orow[col] = acc[i][j][r];
+          }
+        }
+      return;
+    }
+  }
   if constexpr (EPI == EPI_QKV) {
     uint16_t* out = static_cast<uint16_t*>(a.out);
     const int half = d >> 1;

@@ -95,15 +95,109 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
   if (i < n) p[i] = v;
 }
 
+// Register-resident variant for D <= 4 * NT * VPT: the row, its pending
+// partial slices (four slices per batch of loads) and the gain are loaded
+// with every load of a batch in flight at once, the row stays in registers
+// for the normed output, and the residual is written back once.  Slices are
+// added in slice order, as in the general kernel.
+template <int OUT, int VPT>
+__global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
+  __shared__ float s_part[NT / 64];
+  const int r = blockIdx.x;
+  int lo = 0, hi = a.nsegs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.segs[mid].prefix <= r) lo = mid; else hi = mid - 1;
+  }
+  const NormSeg sg = a.segs[lo];
+  const size_t row = (size_t)sg.row0 + (r - sg.prefix);
+  const size_t prow = (size_t)sg.prow0 + (r - sg.prefix);
+  const int D4 = a.D >> 2, tid = threadIdx.x;
+  float4* x = reinterpret_cast<float4*>(a.x + row * a.D);
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 v[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int c = tid + i * NT;
+    v[i] = c < D4 ? x[c] : zero;
+  }
+  const bool add = (sg.flags & NORM_ADD_PARTIALS) != 0;
+  if (add) {
+    for (int p0 = 0; p0 < a.nsplit; p0 += 4) {
+      float4 q[4][VPT];
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+          const int c = tid + i * NT;
+          q[p][i] = (p0 + p < a.nsplit && c < D4)
+                        ? reinterpret_cast<const float4*>(a.partial + (p0 + p) * a.pslice + row * a.D)[c]
+                        : zero;
+        }
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+          v[i].x += q[p][i].x; v[i].y += q[p][i].y; v[i].z += q[p][i].z; v[i].w += q[p][i].w;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < D4) x[c] = v[i];
+    }
+  }
+  if (!(sg.flags & NORM_WRITE_OUT)) return;   // uniform across the workgroup
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+  ss = warp_sum(ss);
+  if ((tid & 63) == 0) s_part[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) tot += s_part[i];
+  const float inv = rsqrtf(tot / (float)a.D + a.eps);
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int c = tid + i * NT;
+    if (c >= D4) continue;
+    if constexpr (OUT != 0) {
+      const uint2 gw = reinterpret_cast<const uint2*>(a.gain)[c];
+      const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
+      const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
+      const uint2 o = make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
+                                 pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + packed_index((int64_t)prow, 4 * c, a.D)) = o;
+    } else {
+      const float4 g = reinterpret_cast<const float4*>(a.gain)[c];
+      reinterpret_cast<float4*>(static_cast<float*>(a.out) + prow * a.D)[c] =
+          make_float4(v[i].x * inv * g.x, v[i].y * inv * g.y, v[i].z * inv * g.z, v[i].w * inv * g.w);
+    }
+  }
+}
+
+template <int OUT>
+hipError_t launch_norm(const NormArgs& a, hipStream_t st) {
+  const int d4 = a.D / 4;
+  if (d4 <= NT) resid_norm_reg_kernel<OUT, 1><<<a.nrows, NT, 0, st>>>(a);
+  else if (d4 <= 2 * NT) resid_norm_reg_kernel<OUT, 2><<<a.nrows, NT, 0, st>>>(a);
+  else if (d4 <= 4 * NT) resid_norm_reg_kernel<OUT, 4><<<a.nrows, NT, 0, st>>>(a);
+  else if (d4 <= 8 * NT) resid_norm_reg_kernel<OUT, 8><<<a.nrows, NT, 0, st>>>(a);
+  else resid_norm_kernel<OUT><<<a.nrows, NT, 0, st>>>(a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st) {
   if (a.nrows <= 0) return hipSuccess;
-  if (out_kind == 2) resid_norm_kernel<2><<<a.nrows, NT, 0, st>>>(a);
-  else if (out_kind == 1) resid_norm_kernel<1><<<a.nrows, NT, 0, st>>>(a);
-  else resid_norm_kernel<0><<<a.nrows, NT, 0, st>>>(a);
-  return hipGetLastError();
+  if (out_kind == 2) return launch_norm<2>(a, st);
+  if (out_kind == 1) return launch_norm<1>(a, st);
+  return launch_norm<0>(a, st);
 }
+
+
 
 hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, float theta,
                              hipStream_t st) {

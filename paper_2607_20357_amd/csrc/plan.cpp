@@ -13,6 +13,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 
 namespace svl {
@@ -101,7 +102,9 @@ struct MmBuild {
     groups.push_back(g);
     max_rows = std::max(max_rows, nrows);
     min_chunks = std::min(min_chunks, kc_cnt);
+    max_chunks = std::max(max_chunks, kc_cnt);
   }
+  int32_t max_chunks = 0;
   // (group, M tile) pairs' total block count
   int64_t total_blocks() const {
     int64_t tb = 0;
@@ -144,29 +147,68 @@ struct MmBuild {
     for (const auto& g : groups) n += (int64_t)cdiv(g.nrows, MFMA_BM) * cdiv(g.nblocks, bpt);
     return n;
   }
-  // QKV and gate/up: blocks per tile by a cost model of the launch time,
-  // (rounds of one tile per CU) x (cost of the widest tile), the tile cost
-  // being its activation rows plus its weight rows (16 per block), the bytes
-  // it streams per K chunk.  A CU that runs two tiles doubles the time; a
-  // wider tile costs little more while its activation rows dominate.
-  GemmLaunch finish_paired(ImageWriter& w) {
-    const int64_t rows = std::min<int64_t>(MFMA_BM, max_rows);
-    int32_t best = 1;
-    int64_t best_cost = -1;
-    for (int32_t bpt = 1; bpt <= MFMA_MAX_NB; ++bpt) {
-      const int64_t rounds = (tiles_for(bpt) + kTargetTiles - 1) / kTargetTiles;
-      const int64_t cost = rounds * (rows + 16 * bpt);
-      if (best_cost < 0 || cost < best_cost) { best = bpt; best_cost = cost; }
+  // QKV and gate/up: blocks per tile (and split-K pieces) by a cost model of
+  // the launch time.  A CU's vector memory path keeps a bounded number of
+  // cache lines in flight, so a tile costs (lines it loads) x (their
+  // latency): per K chunk, one 128-byte line per activation row (L2 hits,
+  // ~280 cycles) and one per weight row (HBM, ~1400 cycles).  The launch
+  // costs (rounds of one tile per CU) x (the widest tile), plus, when split,
+  // the finish kernel that reads the float32 slices back (~3 us fixed).
+  // Splitting cuts each tile's activation lines; wider tiles cut the number
+  // of tiles that all stream the same activations.
+  //
+  // Measured on the headline shapes, splitting does not pay: wider tiles
+  // stop hiding their MFMA work behind the loads and the finish costs a
+  // launch, so splitting is off unless forced (`force_split` > 1, from the
+  // SVL_PAIRED_SPLIT environment variable: tuning and tests).
+  GemmLaunch finish_paired(ImageWriter& w, int32_t pld, int64_t cap_floats, int32_t prows,
+                           int32_t items_per_block, int32_t force_split) {
+    const double rows = (double)std::min<int64_t>(MFMA_BM, max_rows);
+    int32_t best_b = 1, best_s = 1;
+    double best_t = -1.0;
+    // a forced split applies to skinny launches and only while it needs no
+    // more tiles than one per CU (the plan image is sized for that)
+    const int32_t s_lo = (force_split > 1 && max_rows <= kSkinnyRows) ? force_split : 1;
+    const int32_t s_hi = s_lo;
+    for (int32_t s = s_lo; s <= s_hi; ++s) {
+      if (s > 1 && (min_chunks < 4 * s || (int64_t)s * prows * pld > cap_floats)) break;
+      for (int32_t bpt = 1; bpt <= MFMA_MAX_NB; ++bpt) {
+        const int64_t rounds = (tiles_for(bpt) * s + kTargetTiles - 1) / kTargetTiles;
+        const double kcn = (double)max_chunks / s;
+        const double tile_us = kcn * (rows * 280.0 + 16.0 * bpt * 1400.0) / 90.0 / 2400.0;
+        const double t = (double)rounds * tile_us;
+        if (best_t < 0 || t < best_t - 1e-9) { best_b = bpt; best_s = s; best_t = t; }
+      }
+    }
+    if (best_s > 1 && tiles_for(best_b) * best_s > kTargetTiles) {
+      best_s = 1;
+      best_t = -1.0;
+      for (int32_t bpt = 1; bpt <= MFMA_MAX_NB; ++bpt) {
+        const int64_t rounds = (tiles_for(bpt) + kTargetTiles - 1) / kTargetTiles;
+        const double t = (double)rounds * max_chunks * (rows * 280.0 + 16.0 * bpt * 1400.0) / 216000.0;
+        if (best_t < 0 || t < best_t - 1e-9) { best_b = bpt; best_t = t; }
+      }
+    }
+    if (best_s > 1) {
+      int32_t item = 0;
+      for (auto& g : groups) {
+        g.fitem0 = item;
+        item += g.nrows * g.nblocks * items_per_block;
+      }
+      GemmLaunch L = finish(w, best_b, kernel_nb(best_b), best_s);
+      L.nitems = item;
+      return L;
     }
     // the smallest block count with the same number of rounds
-    const int64_t rounds = (tiles_for(best) + kTargetTiles - 1) / kTargetTiles;
-    while (best > 1 && (tiles_for(best - 1) + kTargetTiles - 1) / kTargetTiles == rounds) --best;
-    return finish(w, best, kernel_nb(best), 1);
+    const int64_t rounds = (tiles_for(best_b) + kTargetTiles - 1) / kTargetTiles;
+    while (best_b > 1 && (tiles_for(best_b - 1) + kTargetTiles - 1) / kTargetTiles == rounds)
+      --best_b;
+    return finish(w, best_b, kernel_nb(best_b), 1);
   }
   // Output and down projections: 4-block tiles; a skinny launch splits K
   // into float32 partial slices (at least 2 chunks per piece, the slices
   // within the partial buffer).
-  GemmLaunch finish_plain(ImageWriter& w, int32_t R) {
+  GemmLaunch finish_plain(ImageWriter& w, int32_t R, int32_t D, int64_t cap_floats) {
     int32_t s = 1;
     if (!groups.empty() && max_rows <= kSkinnyRows) {
       int64_t base = 0;
@@ -174,7 +216,7 @@ struct MmBuild {
       s = (int32_t)std::max<int64_t>(1, kTargetTiles / std::max<int64_t>(1, base));
       s = std::min(s, MFMA_MAX_SPLIT);
       s = std::min(s, std::max(1, min_chunks / 2));
-      s = std::min(s, std::max(1, MFMA_PARTIAL_ROWS / std::max(1, R)));
+      s = std::min<int64_t>(s, std::max<int64_t>(1, cap_floats / ((int64_t)std::max(1, R) * D)));
     }
     return finish(w, 4, 4, s);
   }
@@ -250,6 +292,14 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
   }
   const int32_t R = cu[B];
   plan->padded_rows = pcu[B];
+  if (mfma && (int64_t)plan->max_seq * (A + 2 * KV) * d * 2 >= (int64_t(1) << 31)) {
+    *err = "a sample's Q/K/V rows span 2 GiB or more (attention addresses them with 32-bit offsets)";
+    return false;
+  }
+  const int64_t cap = partial_floats_bound(cfg, B, R);
+  int32_t force_split = 1;
+  if (const char* e = std::getenv("SVL_PAIRED_SPLIT")) force_split = std::max(1, std::min(4, std::atoi(e)));
+  const int32_t qkv_width = (A + 2 * KV) * d;
   std::vector<int32_t> kp(B, 0);
   if (keep) for (int32_t b = 0; b < B; ++b) kp[b] = keep[b];
   plan->keep_off = w.append(kp);
@@ -364,8 +414,8 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     // attention sub-block
     LP.norm_attn = norm_launch(run_attn);
     if (mfma) {
-      LP.qkv = mqkv.finish_paired(w);
-      LP.o = mo.finish_plain(w, R);
+      LP.qkv = mqkv.finish_paired(w, qkv_width, cap, plan->padded_rows, 2, force_split);
+      LP.o = mo.finish_plain(w, R, D, cap);
       const int32_t so = LP.o.nsplit;
       if (so > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_attn[b];
@@ -383,8 +433,8 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     // FFN sub-block
     LP.norm_ffn = norm_launch(run_ffn);
     if (mfma) {
-      LP.gu = mgu.finish_paired(w);
-      LP.down = mdown.finish_plain(w, R);
+      LP.gu = mgu.finish_paired(w, 2 * F, cap, plan->padded_rows, 1, force_split);
+      LP.down = mdown.finish_plain(w, R, D, cap);
       const int32_t sd = LP.down.nsplit;
       if (sd > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_ffn[b];

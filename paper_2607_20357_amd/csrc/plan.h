@@ -21,6 +21,7 @@ struct GemmLaunch {
   int32_t ntiles = 0;
   int32_t nb = 0;           // 16-bit MFMA path: kernel block count (tiles hold <= nb)
   int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
+  int32_t nitems = 0;       // split QKV / gate-up launches: finish kernel work items
 };
 
 struct AttnLaunch {
@@ -85,11 +86,20 @@ inline int64_t padded_rows_bound(const svl_config& cfg, int32_t B, int32_t R) {
   return cfg.dtype == SVL_BF16 ? (int64_t)R + 15 * (int64_t)B : (int64_t)R;
 }
 
-// Rows of float32 partial slices the workspace holds (split pieces x rows).
-inline int64_t partial_rows_bound(const svl_config& cfg, int32_t R) {
+// Floats of split-K partial slices the workspace holds: (split pieces x
+// rows) up to min(8 x padded rows, MFMA_PARTIAL_ROWS), each as wide as the
+// widest split output (d_model for the output / down projections, the Q/K/V
+// width, or gate + up = 2 d_ffn).  The planner splits a launch only while its
+// slices fit.
+inline int64_t partial_floats_bound(const svl_config& cfg, int32_t B, int32_t R) {
   if (cfg.dtype != SVL_BF16) return 0;
-  const int64_t r = (int64_t)R * MFMA_MAX_SPLIT;
-  return r < MFMA_PARTIAL_ROWS ? r : MFMA_PARTIAL_ROWS;
+  int64_t r = padded_rows_bound(cfg, B, R) * MFMA_MAX_SPLIT;
+  if (r > MFMA_PARTIAL_ROWS) r = MFMA_PARTIAL_ROWS;
+  int64_t w = cfg.d_model;
+  const int64_t qkv = (int64_t)(cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
+  if (qkv > w) w = qkv;
+  if (2 * (int64_t)cfg.d_ffn > w) w = 2 * (int64_t)cfg.d_ffn;
+  return r * w;
 }
 
 }  // namespace svl

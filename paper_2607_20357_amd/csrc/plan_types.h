@@ -67,7 +67,8 @@ struct MmGroup {
   int32_t kc_cnt;
   int32_t rope;         // QKV: rotate (query and key groups)
   int32_t nblocks;      // 16-column blocks
-  int32_t pad0, pad1;
+  int32_t fitem0;       // split paired launches: first finish work item of the group
+  int32_t pad1;
 };
 
 // One workgroup of a 16-bit MFMA GEMM launch: rows [m0, m0 + 256) of the

@@ -55,8 +55,26 @@ struct MmArgs {
   int32_t ldo;
   const float2* rope;    // QKV: (cos, sin)[pos][head_dim/2]
   int32_t head_dim;
-  float* partial;        // PARTIAL: slice p at partial + p * pslice, row stride ldo
+  float* partial;        // split-K slices: slice p at partial + p * pslice
   int64_t pslice;
+  int32_t split;         // QKV / SWIGLU: > 1 stores raw float32 pieces (row stride
+                         // pld; SWIGLU: gate columns, then up columns at pld / 2)
+                         // for the finish kernel; PARTIAL: row stride ldo
+  int32_t pld;
+};
+
+// Finish of a split QKV / gate-up launch: sums the split slices in order,
+// then RoPE (QKV) or silu(gate) * up (SWIGLU), rounded once to 16 bits.
+struct FinishArgs {
+  const MmGroup* groups;     // the GEMM launch's groups; pad0 = first work item
+  int32_t ngroups, nitems;
+  const float* partial;
+  int64_t pslice;
+  int32_t pld, nsplit;
+  void* out;                 // QKV: row-major [rows][ldo]; SWIGLU: packed, K = ldo
+  int32_t ldo;
+  const float2* rope;
+  int32_t head_dim;
 };
 
 struct AttnArgs {
@@ -96,6 +114,7 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
 // out_kind: 0 float32 row-major, 1 bf16 packed, 2 fp16 packed
 hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st);
 hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st);
+hipError_t launch_finish(const FinishArgs& a, int32_t epi, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);

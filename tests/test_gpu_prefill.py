@@ -141,6 +141,32 @@ def test_layer_full_size(name, compute):
     assert max(errs) <= tol_for(w.shape), errs
 
 
+@pytest.mark.parametrize("split", [2, 3])
+def test_layer_forced_paired_split(split, monkeypatch):
+    """The split-K QKV and gate/up path (float32 slices, then the finish
+    kernels: RoPE or SwiGLU after the ordered sum), which the planner uses
+    only when forced: the per-head-mask edge case and the headline layer."""
+    monkeypatch.setenv("SVL_PAIRED_SPLIT", str(split))
+    shape = W.ModelShape(n_layers=1, d_model=512, n_heads=8, n_kv_heads=4, head_dim=64,
+                         d_ffn=1024, n_groups=4, dtype="bf16")
+    seqlens = np.array([70, 0, 1, 129, 200], np.int32)
+    rng = np.random.default_rng(1)
+    head_mask = (rng.random((5, 8)) > 0.4).astype(np.uint8)
+    ffn_mask = (rng.random((5, 4)) > 0.4).astype(np.uint8)
+    layer_on = np.array([1, 1, 1, 1, 1], np.uint8)
+    print(f"forced split {split}: edge case", flush=True)
+    errs = _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask)
+    print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(shape), errs
+    w = W.get_workload("llava7b_b1_keep25")
+    keep, lm, hm, fm = W.draw_masks(w, 0)
+    l = w.shape.prefix
+    print(f"forced split {split}: headline layer", flush=True)
+    errs = _layer_case(w.shape, (keep + w.n_text).astype(np.int32), lm[:, l], hm[:, l], fm[:, l])
+    print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+
+
 def test_prefill_deterministic_and_flops():
     w = W.get_workload("llava7b_b8_ragged")
     w = W.scaled(w, n_layers=3, d_model=512, n_heads=4, n_kv_heads=4, d_ffn=1024, name="det")
