@@ -34,7 +34,9 @@ constexpr float NEG_BIG = -1.0e30f;
 template <int D, bool F16>
 __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D + 8;      // K tile row stride (elements)
-  constexpr int VS = BKV + 8;    // transposed V tile row stride (elements)
+  // transposed V tile row stride (elements): 160 bytes, so the 8-byte fragment
+  // reads of 16 rows x 4 lane groups hit distinct banks
+  constexpr int VS = BKV + 16;
   constexpr int NS = D / 32;     // MFMA k-steps over the head dimension
   constexpr int NB = D / 16;     // 16-wide head-dimension blocks of O^T
   __shared__ __attribute__((aligned(16))) uint16_t Ks[GT][BKV * KS];
@@ -103,7 +105,9 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int i = 0; i < VT; ++i) {
-        const int task = min(tid + i * NT, VTASKS - 1), pr = task / (D / 8), c = task % (D / 8);
+        // row pair fastest across lanes: the transposed stores of half a wave
+        // are 32 consecutive words
+        const int task = min(tid + i * NT, VTASKS - 1), pr = task % (BKV / 2), c = task / (BKV / 2);
         const uint32_t off = (uint32_t)((kv0 + 2 * pr) * ldq + vcol + 8 * c) * 2u;
         va[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
         vb[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -123,7 +127,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
       // V transposed: rows 2pr, 2pr+1 interleaved into 32-bit pairs
 #pragma unroll
       for (int i = 0; i < VT; ++i) {
-        const int task = tid + i * NT, pr = task / (D / 8), c = task % (D / 8);
+        const int task = tid + i * NT, pr = task % (BKV / 2), c = task / (BKV / 2);
         if (VTASKS % NT != 0 && task >= VTASKS) continue;
         const uint32_t aw[4] = {va[j][i].x, va[j][i].y, va[j][i].z, va[j][i].w};
         const uint32_t bw[4] = {vb[j][i].x, vb[j][i].y, vb[j][i].z, vb[j][i].w};

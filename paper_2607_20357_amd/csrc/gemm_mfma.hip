@@ -52,7 +52,10 @@ namespace svl {
 namespace {
 
 constexpr int BM = MFMA_BM, NWAVE = 8, NT = NWAVE * 64;
-constexpr int KS = 4;                          // K chunks per weight stage (one barrier each)
+#ifndef SVL_GEMM_KS
+#define SVL_GEMM_KS 4
+#endif
+constexpr int KS = SVL_GEMM_KS;                // K chunks per weight stage (one barrier each)
 constexpr int LDS_STRIDE = KS * MFMA_BK;       // 16-bit elements per LDS row (512 B, 32 units)
 constexpr int MAX_CHUNKS = 1024;               // K chunks per tile (K <= 65536)
 constexpr int NSA = KS;                        // A chunks in flight (stage = chunk % KS)
@@ -102,7 +105,11 @@ using Phase = std::integral_constant<int, P>;
 template <int EPI, int NB, bool F16>
 __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   constexpr int BN = NB * 16;                   // weight rows per tile
+#ifdef SVL_GEMM_NWS
+  constexpr int NWS = SVL_GEMM_NWS;
+#else
   constexpr int NWS = NB <= 6 ? 2 : 1;          // weight register stages
+#endif
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
   __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
 
@@ -137,13 +144,15 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   // p / 32 (block j = row/16, column i = row%16 of the block).  Half a wave
   // loads 512 bytes of one weight row; a wave's two rows share one column
   // half of a block (i < 8 or i >= 8), so the matrix choice is wave-uniform.
-  constexpr int WLD = NB;                       // BN * 32 pieces / NT threads
+  static_assert(KS == 4 || KS == 8, "stage rows are 512 or 1024 bytes");
+  constexpr int RU = KS * 8;                    // 16-byte units per stage row
+  constexpr int WLD = NB * KS / 4;              // BN * RU pieces / NT threads
   __amdgpu_buffer_rsrc_t rsB[WLD];
   uint32_t voB[WLD];
-  const int wu = tid & 31, wqc = wu >> 3;       // this thread's unit and chunk of the stage
+  const int wu = tid & (RU - 1), wqc = wu >> 3;   // this thread's unit and chunk of the stage
 #pragma unroll
   for (int s = 0; s < WLD; ++s) {
-    const int tr = (tid + NT * s) >> 5;
+    const int tr = (tid + NT * s) / RU;
     const int j = tr >> 4, i = tr & 15;
     const int gb = tl.b0 + j;
     int m = 0, row = 0;
@@ -169,10 +178,16 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 
   const int last = nk - 1;
   uint4 sa[NSA][2][2], sw[NWS][WLD];
-  auto loadA = [&](int c, uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+  // A loads and MFMAs of the wave's NRB row blocks that hold rows of the
+  // tile (the pipeline is instantiated per NRB, so a wave past the tile's
+  // rows issues no loads for them and the waits stay exact).  NRB < 0: both
+  // blocks are loaded (out-of-range rows read zero) and the MFMAs branch on
+  // rowblk, which keeps the widest tiles within the registers.
+  auto loadA = [&](auto nrb, int c, uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+    constexpr int NRB = decltype(nrb)::value < 0 ? 2 : decltype(nrb)::value;
     const uint32_t soA = (uint32_t)__builtin_amdgcn_readfirstlane(s_k0[c]) * 32u;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NRB; ++i) {
       ra[i][0] = load16(rsA, voA[i], soA);
       ra[i][1] = load16(rsA, voA[i] + 1024u, soA);
     }
@@ -188,7 +203,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     uint16_t* B = Bs + buf * (BN * LDS_STRIDE);
 #pragma unroll
     for (int s = 0; s < WLD; ++s) {
-      const int tr = (tid + NT * s) >> 5;
+      const int tr = (tid + NT * s) / RU;
       *reinterpret_cast<uint4*>(&B[tr * LDS_STRIDE + (wu ^ swz(tr)) * 8]) =
           weight_to_act<F16>(rb[s]);
     }
@@ -206,7 +221,9 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   // swizzle of rows j*16 + lane%16 depends on lane%16 only
   const int fl = (2 * (lane >> 4)) ^ swz(lane & 15);
   const uint16_t* Bl = Bs + (lane & 15) * LDS_STRIDE;
-  auto compute = [&](int buf, int q, const uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+  auto compute = [&](auto nrb, int buf, int q, const uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+    constexpr bool DYN = decltype(nrb)::value < 0;
+    constexpr int NRB = DYN ? 2 : decltype(nrb)::value;
     const uint16_t* B = Bl + buf * (BN * LDS_STRIDE);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -219,8 +236,8 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       for (int j = 0; j < NB; ++j)
         bfr[j] = *reinterpret_cast<const uint4*>(&B[j * 16 * LDS_STRIDE + u]);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        if (rowblk[i])
+      for (int i = 0; i < NRB; ++i)
+        if (!DYN || rowblk[i])
 #pragma unroll
           for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
     }
@@ -232,12 +249,12 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   // stage S: stage S+1 goes from registers into the other LDS buffer, one
   // barrier, and the register stage is refilled with stage S+1+NWS.  Waves
   // synchronise once per KS chunks.
-  if (nk > 0) {
+  auto pipeline = [&](auto nrb) __attribute__((always_inline)) {
     const int nst = (nk + KS - 1) / KS;
 #pragma unroll
     for (int s = 0; s < NWS; ++s) loadW(s, sw[s]);
     [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
-      (loadA(min(Q, last), sa[Q]), ...);
+      (loadA(nrb, min(Q, last), sa[Q]), ...);
     }(std::make_integer_sequence<int, KS>{});
     wstore(0, sw[0]);
     loadW(NWS, sw[0]);
@@ -249,7 +266,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       constexpr bool FULL = decltype(full)::value;
       [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
         ((FULL || S * KS + Q < nk
-              ? (compute(S & 1, Q, sa[Q]), loadA(min(S * KS + Q + KS, last), sa[Q]))
+              ? (compute(nrb, S & 1, Q, sa[Q]), loadA(nrb, min(S * KS + Q + KS, last), sa[Q]))
               : void()),
          ...);
       }(std::make_integer_sequence<int, KS>{});
@@ -269,6 +286,16 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     [&]<int... P>(std::integer_sequence<int, P...>) __attribute__((always_inline)) {
       ((S + P < nst ? stage(S + P, Phase<P % NWS>{}, std::false_type{}) : void()), ...);
     }(std::make_integer_sequence<int, NWS + 1>{});
+  };
+  // every instantiation runs the same barrier sequence
+  if (nk > 0) {
+    if constexpr (NB >= 8) {
+      pipeline(std::integral_constant<int, -1>{});
+    } else {
+      if (rowblk[1]) pipeline(std::integral_constant<int, 2>{});
+      else if (rowblk[0]) pipeline(std::integral_constant<int, 1>{});
+      else pipeline(std::integral_constant<int, 0>{});
+    }
   }
 
   // Epilogue.  acc[i][j][r] is C[32 wave + 16 i + 4 (lane/16) + r][16 j + lane%16]
