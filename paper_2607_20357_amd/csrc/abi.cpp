@@ -229,6 +229,10 @@ struct Exec {
     NormArgs a{};
     a.segs = at<NormSeg>(n.segs_off);
     a.nsegs = n.nsegs;
+    const NormSeg* hs = reinterpret_cast<const NormSeg*>(plan.image.data() + n.segs_off);
+    for (int32_t i = 0; i < n.nsegs; ++i)   // normed rows need the gain
+      if ((hs[i].flags & NORM_WRITE_OUT) && gain == nullptr) return hipErrorInvalidValue;
+    if (n.nsegs <= NORM_INLINE_SEGS) std::memcpy(a.inl, hs, (size_t)n.nsegs * sizeof(NormSeg));
     a.nrows = n.nrows;
     a.x = resid;
     a.partial = reinterpret_cast<const float*>(ws + L.partial);

@@ -116,19 +116,22 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   const int t = xcd_tile_index();
   if (t >= a.ntiles) return;
   const MmTile tl = a.tiles[t];
-  const MmGroup g = a.groups[tl.group];
-  const int mcnt = min(BM, g.nrows - tl.m0);
+  const int mcnt = tl.mcnt;
   const int nblk = tl.nblk;
   const int nk = tl.kcn;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int c = tid; c < nk; c += NT) s_k0[c] = a.chunks[g.kc_off + tl.kc0 + c].k0;
+  if (tl.kdense >= 0) {
+    for (int c = tid; c < nk; c += NT) s_k0[c] = tl.kdense + MFMA_BK * c;
+  } else {
+    for (int c = tid; c < nk; c += NT) s_k0[c] = a.chunks[tl.chunk0 + c].k0;
+  }
 
   const int d = a.head_dim, hb = d >> 4;        // QKV: blocks per head
 
   // A: packed blocks of this tile's rows; wave w reads 16-row blocks 2w, 2w+1.
   const uint32_t kblocks = (uint32_t)(a.lda / 64);
   const uint32_t blk_bytes = kblocks * 2048u;   // one 16-row block over all of K
-  const int rb0 = (g.arow0 + tl.m0) / 16;
+  const int rb0 = (tl.arow) / 16;
   const __amdgpu_buffer_rsrc_t rsA =
       make_rsrc(static_cast<const uint16_t*>(a.A) + (size_t)rb0 * kblocks * 1024,
                 (uint32_t)((mcnt + 15) / 16) * blk_bytes);
@@ -157,14 +160,14 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     const int gb = tl.b0 + j;
     int m = 0, row = 0;
     if constexpr (EPI == EPI_QKV) {
-      m = g.wsel;
-      row = g.wrow0 + (gb / hb) * d + (gb % hb) * 8 + (i & 7) + ((i >> 3) ? (d >> 1) : 0);
+      m = tl.wsel;
+      row = tl.wrow0 + (gb / hb) * d + (gb % hb) * 8 + (i & 7) + ((i >> 3) ? (d >> 1) : 0);
     } else if constexpr (EPI == EPI_SWIGLU) {
       m = __builtin_amdgcn_readfirstlane((i >> 3) & 1);   // gate rows, then up rows
-      row = g.wrow0 + gb * 8 + (i & 7);
+      row = tl.wrow0 + gb * 8 + (i & 7);
     } else {
       m = 0;
-      row = g.wrow0 + gb * 16 + i;
+      row = tl.wrow0 + gb * 16 + i;
     }
     const void* base = m == 0 ? a.W[0] : (m == 1 ? a.W[1] : a.W[2]);
     const int rows = m == 0 ? a.w_rows[0] : (m == 1 ? a.w_rows[1] : a.w_rows[2]);
@@ -312,15 +315,15 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rbase + 16 * i + r;
-          float* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.pld;
+          float* orow = out + (size_t)(tl.orow + min(row, mcnt - 1)) * a.pld;
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
             const int gb = tl.b0 + j;
             int col;
             if constexpr (EPI == EPI_QKV)
-              col = g.ocol0 + (gb / hb) * d + (gb % hb) * 8 + (ci & 7) + ((ci >> 3) ? (d >> 1) : 0);
+              col = tl.ocol0 + (gb / hb) * d + (gb % hb) * 8 + (ci & 7) + ((ci >> 3) ? (d >> 1) : 0);
             else
-              col = ((ci >> 3) ? (a.pld >> 1) : 0) + g.ocol0 + gb * 8 + (ci & 7);
+              col = ((ci >> 3) ? (a.pld >> 1) : 0) + tl.ocol0 + gb * 8 + (ci & 7);
             if (j < nblk && row < mcnt) orow[col] = acc[i][j][r];
           }
         }
@@ -333,12 +336,12 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     // All table loads first, then all stores (a wait on a load issued after
     // stores would also wait for the stores).
     float2 cs[2][4][NB];
-    if (g.rope) {
+    if (tl.rope) {
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int pos = tl.m0 + min(rbase + 16 * i + r, mcnt - 1);
+          const int pos = tl.pos0 + min(rbase + 16 * i + r, mcnt - 1);
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
             const int gb = tl.b0 + min(j, nblk - 1);
@@ -352,12 +355,12 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rbase + 16 * i + r;
-        uint16_t* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.ldo + g.ocol0;
+        uint16_t* orow = out + (size_t)(tl.orow + min(row, mcnt - 1)) * a.ldo + tl.ocol0;
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           float v = acc[i][j][r];
           const float pv = __shfl_xor(v, 8, 64);
-          if (g.rope) {
+          if (tl.rope) {
             // (x1, x2) -> (x1 cos - x2 sin, x2 cos + x1 sin); lanes ci < 8 hold x1
             const float2 c2 = cs[i][r][j];
             v = v * c2.x + ((ci < 8) ? -pv : pv) * c2.y;
@@ -374,12 +377,12 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rbase + 16 * i + r;
-        const int64_t prow = g.orow0 + tl.m0 + min(row, mcnt - 1);
+        const int64_t prow = tl.orow + min(row, mcnt - 1);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           const float gt = acc[i][j][r];
           const float up = __shfl_xor(gt, 8, 64);   // lanes ci < 8: gate, ci >= 8: up
-          const int ch = g.ocol0 + (tl.b0 + j) * 8 + (ci & 7);
+          const int ch = tl.ocol0 + (tl.b0 + j) * 8 + (ci & 7);
           if (j < nblk && row < mcnt && ci < 8)
             out[packed_index(prow, ch, a.ldo)] =
                 f32_to_act_bits<F16>(gt / (1.0f + __expf(-gt)) * up);
@@ -395,7 +398,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float* orow =
-              out + (size_t)(g.orow0 + tl.m0 + min(rbase + 16 * i + r, mcnt - 1)) * a.ldo + g.ocol0;
+              out + (size_t)(tl.orow + min(rbase + 16 * i + r, mcnt - 1)) * a.ldo + tl.ocol0;
 #pragma unroll
           for (int j = 0; j < NB; ++j)
             old[i][r][j] = orow[(tl.b0 + min(j, nblk - 1)) * 16 + ci];
@@ -406,7 +409,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rbase + 16 * i + r;
-        float* orow = out + (size_t)(g.orow0 + tl.m0 + min(row, mcnt - 1)) * a.ldo + g.ocol0;
+        float* orow = out + (size_t)(tl.orow + min(row, mcnt - 1)) * a.ldo + tl.ocol0;
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           float v = acc[i][j][r];

@@ -9,6 +9,8 @@
 // fragment-packed fp16 / bf16 for the 16-bit MFMA GEMMs (16-byte stores of
 // 8-column groups), row-major float32 on the float32 path.  Rows of samples
 // that do not run the sub-block are not listed.
+#include <type_traits>
+
 #include "svl_internal.h"
 #include "device_util.h"
 
@@ -17,17 +19,30 @@ namespace {
 
 constexpr int NT = 256;
 
-// OUT: 0 float32 row-major (float32 gain), 1 bf16 packed, 2 fp16 packed (bf16 gain)
-template <int OUT>
-__global__ __launch_bounds__(NT) void resid_norm_kernel(NormArgs a) {
-  __shared__ float s_part[NT / 64];
-  const int r = blockIdx.x;
+// The segment holding listed row r (segments sorted by prefix): a scan of
+// the inline copy with static indices, else a binary search of the table.
+__device__ __forceinline__ NormSeg find_seg(const NormArgs& a, int r) {
+  if (a.nsegs <= NORM_INLINE_SEGS) {
+    NormSeg sg = a.inl[0];
+#pragma unroll
+    for (int i = 1; i < NORM_INLINE_SEGS; ++i)
+      if (i < a.nsegs && a.inl[i].prefix <= r) sg = a.inl[i];
+    return sg;
+  }
   int lo = 0, hi = a.nsegs - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (a.segs[mid].prefix <= r) lo = mid; else hi = mid - 1;
   }
-  const NormSeg sg = a.segs[lo];
+  return a.segs[lo];
+}
+
+// OUT: 0 float32 row-major (float32 gain), 1 bf16 packed, 2 fp16 packed (bf16 gain)
+template <int OUT>
+__global__ __launch_bounds__(NT) void resid_norm_kernel(NormArgs a) {
+  __shared__ float s_part[NT / 64];
+  const int r = blockIdx.x;
+  const NormSeg sg = find_seg(a, r);
   const size_t row = (size_t)sg.row0 + (r - sg.prefix);
   const size_t prow = (size_t)sg.prow0 + (r - sg.prefix);
   const int D = a.D, tid = threadIdx.x;
@@ -104,12 +119,7 @@ template <int OUT, int VPT>
 __global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
   __shared__ float s_part[NT / 64];
   const int r = blockIdx.x;
-  int lo = 0, hi = a.nsegs - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.segs[mid].prefix <= r) lo = mid; else hi = mid - 1;
-  }
-  const NormSeg sg = a.segs[lo];
+  const NormSeg sg = find_seg(a, r);
   const size_t row = (size_t)sg.row0 + (r - sg.prefix);
   const size_t prow = (size_t)sg.prow0 + (r - sg.prefix);
   const int D4 = a.D >> 2, tid = threadIdx.x;
@@ -120,6 +130,16 @@ __global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
   for (int i = 0; i < VPT; ++i) {
     const int c = tid + i * NT;
     v[i] = c < D4 ? x[c] : zero;
+  }
+  // rows that are normed load the gain with the row (it does not depend on
+  // the statistics); add-only launches carry no gain
+  const bool write_out = (sg.flags & NORM_WRITE_OUT) != 0;   // uniform across the workgroup
+  using GainT = std::conditional_t<OUT != 0, uint2, float4>;
+  GainT gv[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int c = tid + i * NT;
+    gv[i] = write_out && c < D4 ? reinterpret_cast<const GainT*>(a.gain)[c] : GainT{};
   }
   const bool add = (sg.flags & NORM_ADD_PARTIALS) != 0;
   if (add) {
@@ -147,7 +167,7 @@ __global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
       if (c < D4) x[c] = v[i];
     }
   }
-  if (!(sg.flags & NORM_WRITE_OUT)) return;   // uniform across the workgroup
+  if (!write_out) return;
   float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < VPT; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
@@ -163,14 +183,14 @@ __global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
     const int c = tid + i * NT;
     if (c >= D4) continue;
     if constexpr (OUT != 0) {
-      const uint2 gw = reinterpret_cast<const uint2*>(a.gain)[c];
+      const uint2 gw = gv[i];
       const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
       const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
       const uint2 o = make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
                                  pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
       *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + packed_index((int64_t)prow, 4 * c, a.D)) = o;
     } else {
-      const float4 g = reinterpret_cast<const float4*>(a.gain)[c];
+      const float4 g = gv[i];
       reinterpret_cast<float4*>(static_cast<float*>(a.out) + prow * a.D)[c] =
           make_float4(v[i].x * inv * g.x, v[i].y * inv * g.y, v[i].z * inv * g.z, v[i].w * inv * g.w);
     }

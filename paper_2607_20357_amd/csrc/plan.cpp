@@ -94,11 +94,19 @@ struct MmBuild {
   std::vector<MmGroup> groups;
   int32_t max_rows = 0, min_chunks = 1 << 30;
   void add(int32_t arow0, int32_t orow0, int32_t nrows, int32_t wsel, int32_t wrow0,
-           int32_t ocol0, int32_t nblocks, int32_t kc_off, int32_t kc_cnt, int32_t rope) {
+           int32_t ocol0, int32_t nblocks, int32_t kc_off, int32_t kc_cnt, int32_t rope,
+           const std::vector<KChunk>& chunks) {
     if (nrows <= 0 || nblocks <= 0 || kc_cnt <= 0) return;
     MmGroup g{};
     g.arow0 = arow0; g.orow0 = orow0; g.nrows = nrows; g.wsel = wsel; g.wrow0 = wrow0;
     g.ocol0 = ocol0; g.kc_off = kc_off; g.kc_cnt = kc_cnt; g.rope = rope; g.nblocks = nblocks;
+    // contiguous full chunks: the kernel computes the offsets
+    g.kdense = chunks[kc_off].k0;
+    for (int32_t c = 0; c < kc_cnt; ++c)
+      if (chunks[kc_off + c].k0 != g.kdense + MFMA_BK * c || chunks[kc_off + c].len != MFMA_BK) {
+        g.kdense = -1;
+        break;
+      }
     groups.push_back(g);
     max_rows = std::max(max_rows, nrows);
     min_chunks = std::min(min_chunks, kc_cnt);
@@ -125,10 +133,17 @@ struct MmBuild {
         for (int32_t mt = 0; mt < nm; ++mt)
           for (int32_t p = 0; p < nsplit; ++p) {
             MmTile t{};
-            t.group = gi; t.m0 = mt * MFMA_BM; t.b0 = b0; t.nblk = b1 - b0;
-            t.kc0 = (int32_t)((int64_t)g.kc_cnt * p / nsplit);
-            t.kcn = (int32_t)((int64_t)g.kc_cnt * (p + 1) / nsplit) - t.kc0;
+            const int32_t m0 = mt * MFMA_BM;
+            const int32_t kc0 = (int32_t)((int64_t)g.kc_cnt * p / nsplit);
+            t.arow = g.arow0 + m0; t.orow = g.orow0 + m0;
+            t.mcnt = std::min(MFMA_BM, g.nrows - m0); t.pos0 = m0;
+            t.wsel = g.wsel; t.wrow0 = g.wrow0; t.ocol0 = g.ocol0; t.rope = g.rope;
+            t.chunk0 = g.kc_off + kc0;
+            t.kcn = (int32_t)((int64_t)g.kc_cnt * (p + 1) / nsplit) - kc0;
+            t.kdense = g.kdense >= 0 ? g.kdense + MFMA_BK * kc0 : -1;
+            t.b0 = b0; t.nblk = b1 - b0;
             t.slice = p;
+            t.group = gi;
             tiles.push_back(t);
           }
       }
@@ -373,7 +388,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
           for (auto r : runs(sc.on, sc.n, d, 0)) {
             if (mfma)
               mqkv.add(pcu[b], pcu[b], S, sc.wsel, r.a, sc.col0 + r.a, (r.b - r.a) / 16, 0,
-                       dense_cnt, sc.wsel < 2 ? 1 : 0);
+                       dense_cnt, sc.wsel < 2 ? 1 : 0, chunks);
             else
               qkv.add(pcu[b], pcu[b], S, sc.col0 + r.a, sc.col0 + r.b, 0, dense_cnt);
           }
@@ -381,7 +396,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
         int32_t off = (int32_t)chunks.size();
         for (auto r : runs(hm, A, d, 0)) push_chunks(chunks, r.a, r.b, bk);
         if (mfma)
-          mo.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0);
+          mo.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0, chunks);
         else
           o.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
         // attention: one group per sample
@@ -398,14 +413,14 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
         const uint8_t* fmm = fm ? fm : all.data();
         for (auto r : runs(fmm, G, slice, 0)) {
           if (mfma)
-            mgu.add(pcu[b], pcu[b], S, 0, r.a, r.a, (r.b - r.a) / 8, 0, dense_cnt, 0);
+            mgu.add(pcu[b], pcu[b], S, 0, r.a, r.a, (r.b - r.a) / 8, 0, dense_cnt, 0, chunks);
           else
             gu.add(pcu[b], pcu[b], S, r.a, r.b, 0, dense_cnt);
         }
         int32_t off = (int32_t)chunks.size();
         for (auto r : runs(fmm, G, slice, 0)) push_chunks(chunks, r.a, r.b, bk);
         if (mfma)
-          mdown.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0);
+          mdown.add(pcu[b], cu[b], S, 0, 0, 0, D / 16, off, (int32_t)chunks.size() - off, 0, chunks);
         else
           down.add(pcu[b], cu[b], S, 0, D, off, (int32_t)chunks.size() - off);
       }

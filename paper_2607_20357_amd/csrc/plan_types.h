@@ -68,16 +68,30 @@ struct MmGroup {
   int32_t rope;         // QKV: rotate (query and key groups)
   int32_t nblocks;      // 16-column blocks
   int32_t fitem0;       // split paired launches: first finish work item of the group
-  int32_t pad1;
+  int32_t kdense;       // >= 0: the group's chunk c starts at column kdense + 64 c
 };
 
-// One workgroup of a 16-bit MFMA GEMM launch: rows [m0, m0 + 256) of the
+// One workgroup of a 16-bit MFMA GEMM launch: rows [m0, m0 + 256) of its
 // group, blocks [b0, b0 + nblk), K chunks [kc0, kc0 + kcn) of the group's
 // list; a split-K piece stores its float32 result in partial slice `slice`.
+// The record carries the group fields the GEMM reads, resolved for the tile,
+// so a workgroup starts from this one 64-byte load.
 struct MmTile {
-  int32_t group, m0, b0, nblk;
-  int32_t kc0, kcn, slice, pad0;
+  int32_t arow;     // first packed row of A: group arow0 + m0 (multiple of 16)
+  int32_t orow;     // first output row: group orow0 + m0
+  int32_t mcnt;     // rows of the tile (1 .. 256)
+  int32_t pos0;     // position in the sample of the first row: m0 (RoPE)
+  int32_t wsel, wrow0, ocol0, rope;   // as in the group
+  int32_t chunk0;   // first entry of the tile's K chunks in the chunk table
+  int32_t kcn;      // K chunks
+  int32_t kdense;   // >= 0: chunk c starts at column kdense + 64 c (the chunk
+                    // table is not read); -1: read it
+  int32_t b0, nblk; // 16-column blocks [b0, b0 + nblk) of the group
+  int32_t slice;    // split-K piece
+  int32_t group;    // group index (planner checks)
+  int32_t pad0;
 };
+static_assert(sizeof(MmTile) == 64, "one 64-byte record per workgroup");
 
 // One sample of an attention launch: one workgroup per (active head, q tile).
 struct AttnGroup {

@@ -90,9 +90,13 @@ struct AttnArgs {
   float scale;         // 1/sqrt(d)
 };
 
+constexpr int NORM_INLINE_SEGS = 8;
 struct NormArgs {
   const NormSeg* segs;
   int32_t nsegs, nrows;
+  // launches of up to NORM_INLINE_SEGS segments carry them here (read from
+  // the kernel arguments, no dependent global load); longer ones read segs
+  NormSeg inl[NORM_INLINE_SEGS];
   float* x;            // residual [rows][D] (written back when partials are added)
   const float* partial;  // split-K slices to add: slice p at partial + p * pslice
   int32_t nsplit;
