@@ -330,64 +330,97 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       return;
     }
   }
-  if constexpr (EPI == EPI_QKV) {
+  if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {
+    // 16-bit outputs go through a per-wave staging tile in the (now idle)
+    // weight buffers, 32 rows x RW values: QKV, both halves of every block
+    // (16 NB columns); SWIGLU, the 8 NB channels.  Each lane then stores
+    // whole 16-byte pieces (8 consecutive columns of one row), instead of
+    // one 2-byte value per row and block.
+    // (SWIGLU rows are padded to an odd number of 16-byte pieces, so the
+    // row-strided piece reads below hit distinct banks)
+    constexpr int RW = EPI == EPI_QKV ? NB * 16 : (NB | 1) * 8;
+    static_assert(NWAVE * 32 * RW <= 2 * BN * LDS_STRIDE, "staging tiles fit the weight buffers");
+    uint16_t* E = Bs + wave * (32 * RW);
+    const int lr0 = (lane >> 4) * 4;    // wave-local row of acc[i][j][0] is lr0 + 16 i
     uint16_t* out = static_cast<uint16_t*>(a.out);
-    const int half = d >> 1;
-    // All table loads first, then all stores (a wait on a load issued after
-    // stores would also wait for the stores).
-    float2 cs[2][4][NB];
-    if (tl.rope) {
+    if constexpr (EPI == EPI_QKV) {
+      const int half = d >> 1;
+      // all table loads before the barrier and the stores
+      float2 cs[2][4][NB];
+      if (tl.rope) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int pos = tl.pos0 + min(rbase + 16 * i + r, mcnt - 1);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+              const int gb = tl.b0 + min(j, nblk - 1);
+              const int dim = (gb % hb) * 8 + (ci & 7);
+              cs[i][r][j] = a.rope[(size_t)pos * half + dim];
+            }
+          }
+      }
+      __syncthreads();   // every wave is done with the weight buffers
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int pos = tl.pos0 + min(rbase + 16 * i + r, mcnt - 1);
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
-            const int gb = tl.b0 + min(j, nblk - 1);
-            const int dim = (gb % hb) * 8 + (ci & 7);
-            cs[i][r][j] = a.rope[(size_t)pos * half + dim];
+            float v = acc[i][j][r];
+            const float pv = __shfl_xor(v, 8, 64);
+            if (tl.rope) {
+              // (x1, x2) -> (x1 cos - x2 sin, x2 cos + x1 sin); lanes ci < 8 hold x1
+              const float2 c2 = cs[i][r][j];
+              v = v * c2.x + ((ci < 8) ? -pv : pv) * c2.y;
+            }
+            E[(lr0 + 16 * i + r) * RW + j * 16 + ci] = f32_to_act_bits<F16>(v);
           }
+      __syncthreads();
+      // piece q: wave-local row q / (2 NB), block (q / 2) % NB, half q % 2
+#pragma unroll
+      for (int it = 0; it < NB; ++it) {
+        const int q = it * 64 + lane;
+        const int lr = q / (2 * NB), j = (q >> 1) % NB, h = q & 1;
+        const int row = wave * 32 + lr;
+        const uint4 v = *reinterpret_cast<const uint4*>(&E[q * 8]);
+        const int gb = tl.b0 + j;
+        const int col = tl.ocol0 + (gb / hb) * d + (gb % hb) * 8 + h * half;
+        if (j < nblk && row < mcnt)
+          *reinterpret_cast<uint4*>(out + (size_t)(tl.orow + row) * a.ldo + col) = v;
+      }
+    } else {
+      __syncthreads();   // every wave is done with the weight buffers
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const float gt = acc[i][j][r];
+            const float up = __shfl_xor(gt, 8, 64);   // lanes ci < 8: gate, ci >= 8: up
+            // silu(g) * u = g / (1 + exp(-g)) * u, reciprocal in hardware
+            if (ci < 8)
+              E[(lr0 + 16 * i + r) * RW + j * 8 + ci] = f32_to_act_bits<F16>(
+                  gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up);
+          }
+      __syncthreads();
+      // piece q < 32 NB: wave-local row q % 32, block q / 32 (16 lanes store
+      // the 256 contiguous bytes of one 8-channel group of 16 packed rows)
+#pragma unroll
+      for (int it = 0; it < (NB + 1) / 2; ++it) {
+        const int q = it * 64 + lane;
+        const int lr = q & 31, j = q >> 5;
+        const int row = wave * 32 + lr;
+        if (j < NB) {
+          const uint4 v = *reinterpret_cast<const uint4*>(&E[lr * RW + j * 8]);
+          if (j < nblk && row < mcnt)
+            *reinterpret_cast<uint4*>(out + packed_index((int64_t)tl.orow + row,
+                                                         tl.ocol0 + (tl.b0 + j) * 8, a.ldo)) = v;
         }
+      }
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rbase + 16 * i + r;
-        uint16_t* orow = out + (size_t)(tl.orow + min(row, mcnt - 1)) * a.ldo + tl.ocol0;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          float v = acc[i][j][r];
-          const float pv = __shfl_xor(v, 8, 64);
-          if (tl.rope) {
-            // (x1, x2) -> (x1 cos - x2 sin, x2 cos + x1 sin); lanes ci < 8 hold x1
-            const float2 c2 = cs[i][r][j];
-            v = v * c2.x + ((ci < 8) ? -pv : pv) * c2.y;
-          }
-          const int gb = tl.b0 + j;
-          const int col = (gb / hb) * d + (gb % hb) * 8 + (ci & 7) + ((ci >> 3) ? half : 0);
-          if (j < nblk && row < mcnt) orow[col] = f32_to_act_bits<F16>(v);
-        }
-      }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    uint16_t* out = static_cast<uint16_t*>(a.out);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rbase + 16 * i + r;
-        const int64_t prow = tl.orow + min(row, mcnt - 1);
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const float gt = acc[i][j][r];
-          const float up = __shfl_xor(gt, 8, 64);   // lanes ci < 8: gate, ci >= 8: up
-          const int ch = tl.ocol0 + (tl.b0 + j) * 8 + (ci & 7);
-          if (j < nblk && row < mcnt && ci < 8)
-            out[packed_index(prow, ch, a.ldo)] =
-                f32_to_act_bits<F16>(gt / (1.0f + __expf(-gt)) * up);
-        }
-      }
   } else {
     float* out = EPI == EPI_PARTIAL ? a.partial + (size_t)tl.slice * a.pslice
                                     : static_cast<float*>(a.out);
