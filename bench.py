@@ -51,6 +51,11 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run one plain device copy of COPY_BYTES (the known-size kernel "
                         "that scales the FETCH_SIZE / WRITE_SIZE counters of a --pmc run)")
+    p.add_argument("--memory-sweep", action="store_true",
+                   help="instead of the step benchmark: HBM rate of the memory-bound kernels "
+                        "(select, gather, residual norm) on the headline per-row structure "
+                        "with the batch raised to 64 and 256, next to a device copy; one JSON "
+                        "line per batch")
     return p.parse_args()
 
 
@@ -193,10 +198,91 @@ def cpu_baseline(w, inp, layers, n_exec_layers):
                       f"{len(executed)}/{len(sample)}"}
 
 
+def memory_sweep(args):
+    """Select, gather and residual-norm launches of the headline per-row
+    structure (576 vision + 64 text tokens, keep 144, d_model 4096) with the
+    batch raised until the gather and norm working sets pass 1 GB (4x the
+    last-level cache).  Rates are algorithmic bytes / launch time (HIP events
+    the library records on the launch stream), next to a 1 GiB device-to-device
+    copy on the same GPU.  At these row counts the output and down projections
+    need no split-K, so each norm launch moves exactly rows*D*(4 in + 2 out)
+    bytes plus the gain."""
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    reps = max(5, args.steps // 5)
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * COPY_BYTES / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    head = W.get_workload(W.HEADLINE)
+    for B in (64, 256):
+        w = W.scaled(head, batch=B, name=f"{head.name}_b{B}")
+        shape = w.shape
+        inp = W.draw_inputs(w, args.seed, device=dev)
+        cfg = svl.make_config(shape)
+        k = int(inp.keep[0])
+        R = int((inp.keep + w.n_text).sum())
+        scores = torch.from_numpy(inp.scores).to(dev)
+        kept = torch.empty((B, w.n_vision), dtype=torch.int32, device=dev)
+        resid = torch.empty((R, shape.d_model), dtype=torch.float32, device=dev)
+        ws = svl.alloc_workspace(cfg, B, R, dev)
+        weights = W.draw_layer_weights(w, 0, args.seed, device=dev)
+        stream = torch.cuda.current_stream()
+        cu = svl.svl_select_tokens(cfg, inp.keep, scores, inp.vision, inp.text, kept, resid, ws,
+                                   stream=stream)
+        lon = np.ones(B, np.uint8)
+        fm = None if inp.ffn_mask is None else inp.ffn_mask[:, 0]
+        svl.svl_layer_forward(cfg, 0, weights, cu, lon, inp.head_mask[:, 0], fm, resid, ws,
+                              stream=stream)
+        torch.cuda.synchronize()
+        svl.svl_timing_enable(True)
+        for _ in range(reps):
+            svl.svl_select_tokens(cfg, inp.keep, scores, inp.vision, inp.text, kept, resid, ws,
+                                  stream=stream)
+            svl.svl_layer_forward(cfg, 0, weights, cu, lon, inp.head_mask[:, 0], fm, resid, ws,
+                                  stream=stream)
+        torch.cuda.synchronize()
+        svl.svl_timing_enable(False)
+        t = {c: svl.svl_timing_read(c) for c in ("select", "gather", "rmsnorm")}
+        D, N, T = shape.d_model, w.n_vision, w.n_text
+        algo = {"select": B * N * 4 + B * k * 4,
+                "gather": B * (k + T) * D * (2 + 4),
+                "rmsnorm": R * D * (4 + 2) + D * 2}
+        line = {"memory_sweep": True, "batch": B, "rows": R, "d_model": D,
+                "copy_gbs": round(copy_gbs, 1), "hbm_peak_gbs": HBM_PEAK_GBS}
+        for c, (ms, n) in t.items():
+            avg_ms = ms / max(1, n)
+            gbs = algo[c] / (avg_ms * 1e-3) / 1e9
+            line[c] = {"bytes_per_launch": algo[c], "avg_launch_ms": round(avg_ms, 5),
+                       "launches": n, "gbs": round(gbs, 1),
+                       "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+                       "frac_of_copy": round(gbs / copy_gbs, 4)}
+        print(json.dumps(line), flush=True)
+        del inp, scores, kept, resid, ws, weights
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.traffic_from:
         write_traffic(args.traffic_from)
+        return
+    if args.memory_sweep:
+        memory_sweep(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; multi-GPU runs are not part of "
@@ -240,15 +326,17 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event after each step (recording an event adds no GPU work)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
-    e1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     print(f"# timed {args.steps} steps: {ms:.4f} ms/step (wall {1e3 * t_wall / args.steps:.4f})",
           file=sys.stderr, flush=True)
 
@@ -284,6 +372,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_p10_p50_p90": [round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

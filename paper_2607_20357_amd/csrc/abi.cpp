@@ -234,6 +234,8 @@ struct Exec {
       if ((hs[i].flags & NORM_WRITE_OUT) && gain == nullptr) return hipErrorInvalidValue;
     if (n.nsegs <= NORM_INLINE_SEGS) std::memcpy(a.inl, hs, (size_t)n.nsegs * sizeof(NormSeg));
     a.nrows = n.nrows;
+    a.ngroups8 = n.ngroups8;
+    a.rows8 = n.rows8 ? 1 : 0;
     a.x = resid;
     a.partial = reinterpret_cast<const float*>(ws + L.partial);
     a.nsplit = n.nsplit;

@@ -58,7 +58,11 @@ constexpr int BM = MFMA_BM, NWAVE = 8, NT = NWAVE * 64;
 constexpr int KS = SVL_GEMM_KS;                // K chunks per weight stage (one barrier each)
 constexpr int LDS_STRIDE = KS * MFMA_BK;       // 16-bit elements per LDS row (512 B, 32 units)
 constexpr int MAX_CHUNKS = 1024;               // K chunks per tile (K <= 65536)
-constexpr int NSA = KS;                        // A chunks in flight (stage = chunk % KS)
+#ifndef SVL_GEMM_NSA
+#define SVL_GEMM_NSA KS
+#endif
+constexpr int NSA = SVL_GEMM_NSA;              // A chunks in flight (register slot = chunk % NSA)
+static_assert(KS % NSA == 0, "a stage holds whole rounds of A slots");
 
 // Raw buffer resource over [p, p + bytes): loads past the end return zero.
 // The inputs are wave-uniform; readfirstlane keeps the descriptor in scalar
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 
   // Pipeline.  Weight stage S (KS chunks) is multiplied from LDS buffer S % 2
   // while stages S+1 .. S+NWS are in flight in registers; chunk c's A
-  // fragments sit in register stage c % KS, loaded KS chunks ahead.  After
+  // fragments sit in register slot c % NSA, loaded NSA chunks ahead.  After
   // stage S: stage S+1 goes from registers into the other LDS buffer, one
   // barrier, and the register stage is refilled with stage S+1+NWS.  Waves
   // synchronise once per KS chunks.
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     for (int s = 0; s < NWS; ++s) loadW(s, sw[s]);
     [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
       (loadA(nrb, min(Q, last), sa[Q]), ...);
-    }(std::make_integer_sequence<int, KS>{});
+    }(std::make_integer_sequence<int, NSA>{});
     wstore(0, sw[0]);
     loadW(NWS, sw[0]);
     __syncthreads();
@@ -269,7 +273,8 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       constexpr bool FULL = decltype(full)::value;
       [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
         ((FULL || S * KS + Q < nk
-              ? (compute(nrb, S & 1, Q, sa[Q]), loadA(nrb, min(S * KS + Q + KS, last), sa[Q]))
+              ? (compute(nrb, S & 1, Q, sa[Q % NSA]),
+                 loadA(nrb, min(S * KS + Q + NSA, last), sa[Q % NSA]))
               : void()),
          ...);
       }(std::make_integer_sequence<int, KS>{});

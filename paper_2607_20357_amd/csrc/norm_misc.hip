@@ -197,9 +197,113 @@ __global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
   }
 }
 
+// Row-group variant for large 16-bit launches: a workgroup takes 8
+// consecutive rows of one segment, one wave per row, so the 16-row packed
+// layout receives whole 128-byte lines (8 rows x 8 columns) instead of
+// 8-byte pieces of one row.  Each wave keeps its row in registers (vpt
+// float4 per lane, D = 256 vpt), adds the pending slices in slice order,
+// takes the row statistics with a wave reduction, and writes its normed
+// values into an LDS staging area whose entry (8-column group kg, row w) sits
+// at kg * 144 + w * 16 bytes: the 144-byte stride keeps both the row-wise
+// 8-byte writes and the 8-lane line reads on distinct banks.
+constexpr int NT8 = 512;
+__device__ __forceinline__ NormSeg find_seg8(const NormArgs& a, int g) {
+  if (a.nsegs <= NORM_INLINE_SEGS) {
+    NormSeg sg = a.inl[0];
+#pragma unroll
+    for (int i = 1; i < NORM_INLINE_SEGS; ++i)
+      if (i < a.nsegs && a.inl[i].gprefix <= g) sg = a.inl[i];
+    return sg;
+  }
+  int lo = 0, hi = a.nsegs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.segs[mid].gprefix <= g) lo = mid; else hi = mid - 1;
+  }
+  return a.segs[lo];
+}
+
+template <int OUT, int VMAX>
+__global__ __launch_bounds__(NT8) void resid_norm8_kernel(NormArgs a) {
+  static_assert(OUT != 0, "16-bit packed output");
+  __shared__ __attribute__((aligned(16))) uint8_t stage[32 * VMAX * 144];
+  const int g = blockIdx.x;
+  const NormSeg sg = find_seg8(a, g);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int base = (g - sg.gprefix) * 8;          // first local row of the group
+  const int local = base + wave;
+  const bool valid = local < sg.nrows;            // wave-uniform
+  const int vpt = a.D >> 8;
+  const size_t row = (size_t)sg.row0 + local;
+  float4* x = reinterpret_cast<float4*>(a.x + row * a.D);
+  const bool write_out = (sg.flags & NORM_WRITE_OUT) != 0;   // uniform across the workgroup
+  float4 v[VMAX];
+  uint2 gv[VMAX];
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i) {
+    const int c = lane + 64 * i;
+    const bool in = valid && i < vpt;
+    v[i] = in ? x[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    gv[i] = in && write_out ? reinterpret_cast<const uint2*>(a.gain)[c] : make_uint2(0u, 0u);
+  }
+  if (valid && (sg.flags & NORM_ADD_PARTIALS)) {
+    for (int p = 0; p < a.nsplit; ++p) {
+      const float4* q = reinterpret_cast<const float4*>(a.partial + p * a.pslice + row * a.D);
+#pragma unroll
+      for (int i = 0; i < VMAX; ++i) {
+        if (i >= vpt) continue;
+        const float4 t = q[lane + 64 * i];
+        v[i].x += t.x; v[i].y += t.y; v[i].z += t.z; v[i].w += t.w;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VMAX; ++i)
+      if (i < vpt) x[lane + 64 * i] = v[i];
+  }
+  if (!write_out) return;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+  ss = warp_sum(ss);
+  const float inv = rsqrtf(ss / (float)a.D + a.eps);
+  if (valid) {
+#pragma unroll
+    for (int i = 0; i < VMAX; ++i) {
+      if (i >= vpt) continue;
+      const int c = lane + 64 * i;                 // columns 4c .. 4c+3
+      const uint2 gw = gv[i];
+      const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
+      const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
+      *reinterpret_cast<uint2*>(stage + (c >> 1) * 144 + wave * 16 + (c & 1) * 8) =
+          make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
+                     pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
+    }
+  }
+  __syncthreads();
+  // piece p: row w = p % 8 of the group, columns 8 (p / 8) .. + 7
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  for (int p = threadIdx.x; p < a.D; p += NT8) {
+    const int w = p & 7, kg = p >> 3;
+    if (base + w < sg.nrows)
+      *reinterpret_cast<uint4*>(out + packed_index((int64_t)sg.prow0 + base + w, 8 * kg, a.D)) =
+          *reinterpret_cast<const uint4*>(stage + kg * 144 + w * 16);
+  }
+}
+
 template <int OUT>
 hipError_t launch_norm(const NormArgs& a, hipStream_t st) {
   const int d4 = a.D / 4;
+  if constexpr (OUT != 0) {
+    if (a.rows8) {
+      if (a.D % 256 != 0 || a.D > 8192 || a.ngroups8 <= 0) return hipErrorInvalidValue;
+      const int vpt = a.D / 256;
+      const unsigned grid = (unsigned)a.ngroups8;
+      if (vpt <= 8) resid_norm8_kernel<OUT, 8><<<grid, NT8, 0, st>>>(a);
+      else if (vpt <= 16) resid_norm8_kernel<OUT, 16><<<grid, NT8, 0, st>>>(a);
+      else resid_norm8_kernel<OUT, 32><<<grid, NT8, 0, st>>>(a);
+      return hipGetLastError();
+    }
+  }
   if (d4 <= NT) resid_norm_reg_kernel<OUT, 1><<<a.nrows, NT, 0, st>>>(a);
   else if (d4 <= 2 * NT) resid_norm_reg_kernel<OUT, 2><<<a.nrows, NT, 0, st>>>(a);
   else if (d4 <= 4 * NT) resid_norm_reg_kernel<OUT, 4><<<a.nrows, NT, 0, st>>>(a);

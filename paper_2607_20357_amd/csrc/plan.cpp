@@ -314,6 +314,12 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
   const int64_t cap = partial_floats_bound(cfg, B, R);
   int32_t force_split = 1;
   if (const char* e = std::getenv("SVL_PAIRED_SPLIT")) force_split = std::max(1, std::min(4, std::atoi(e)));
+  // 8-row-group norm kernel: 16-bit output, d_model % 256 == 0 and <= 8192
+  // (a row in one wave's registers); SVL_NORM8_MIN_ROWS overrides the row
+  // threshold (tuning and tests)
+  int32_t rows8_min = kNormRows8;
+  if (const char* e = std::getenv("SVL_NORM8_MIN_ROWS")) rows8_min = std::max(0, std::atoi(e));
+  const bool rows8_ok = mfma && D % 256 == 0 && D <= 8192;
   const int32_t qkv_width = (A + 2 * KV) * d;
   std::vector<int32_t> kp(B, 0);
   if (keep) for (int32_t b = 0; b < B; ++b) kp[b] = keep[b];
@@ -329,7 +335,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
   auto norm_launch = [&](const std::vector<uint8_t>& run) {
     NormLaunch L;
     std::vector<NormSeg> segs;
-    int32_t prefix = 0;
+    int32_t prefix = 0, gprefix = 0;
     for (int32_t b = 0; b < B; ++b) {
       const int32_t S = seqlens[b];
       int32_t flags = 0;
@@ -338,13 +344,17 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
       if (!flags || S == 0) continue;
       NormSeg s{};
       s.row0 = cu[b]; s.prow0 = pcu[b]; s.nrows = S; s.prefix = prefix; s.flags = flags;
+      s.gprefix = gprefix;
       segs.push_back(s);
       prefix += S;
+      gprefix += (S + 7) / 8;
       L.write_out = L.write_out || run[b];
     }
     L.segs_off = w.append(segs);
     L.nsegs = (int32_t)segs.size();
     L.nrows = prefix;
+    L.ngroups8 = gprefix;
+    L.rows8 = rows8_ok && prefix > 0 && prefix >= rows8_min;
     L.nsplit = pending_split > 1 ? pending_split : 0;
     std::fill(pending.begin(), pending.end(), 0);
     pending_split = 0;

@@ -35,6 +35,8 @@ struct AttnLaunch {
 struct NormLaunch {
   int64_t segs_off = 0;
   int32_t nsegs = 0, nrows = 0;
+  int32_t ngroups8 = 0;     // sum over segments of ceil(nrows / 8)
+  bool rows8 = false;       // 16-bit output through the 8-row-group kernel
   int32_t nsplit = 0;       // partial slices to add (0: none pending)
   bool write_out = false;   // some segment writes normed rows
 };
@@ -72,6 +74,10 @@ struct LayerMasks {
 constexpr int32_t kSkinnyRows = MFMA_BM;
 // Workgroups a launch aims for (one per CU).
 constexpr int32_t kTargetTiles = 256;
+// Norm launches of at least this many rows (16-bit output) use the 8-row
+// group kernel (whole packed lines per store) instead of one row per
+// workgroup (more workgroups for short launches).
+constexpr int32_t kNormRows8 = 2048;
 
 // Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks[l]
 // gives layer l's masks.  Returns false with a message on inconsistency.

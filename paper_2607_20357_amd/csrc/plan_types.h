@@ -28,7 +28,8 @@ struct NormSeg {
   int32_t nrows;
   int32_t prefix;  // sum of nrows of the earlier segments of the launch
   int32_t flags;   // NormFlags
-  int32_t pad0, pad1, pad2;
+  int32_t gprefix; // sum of ceil(nrows / 8) of the earlier segments (8-row groups)
+  int32_t pad1, pad2;
 };
 
 // One (sample, output-column range) pair of a GEMM launch.  Its tiles are

@@ -97,6 +97,8 @@ struct NormArgs {
   // launches of up to NORM_INLINE_SEGS segments carry them here (read from
   // the kernel arguments, no dependent global load); longer ones read segs
   NormSeg inl[NORM_INLINE_SEGS];
+  int32_t ngroups8;    // 8-row groups (row-group kernel grid)
+  int32_t rows8;       // 1: the 8-row-group kernel (16-bit output)
   float* x;            // residual [rows][D] (written back when partials are added)
   const float* partial;  // split-K slices to add: slice p at partial + p * pslice
   int32_t nsplit;

@@ -167,6 +167,34 @@ def test_layer_forced_paired_split(split, monkeypatch):
     assert max(errs) <= tol_for(w.shape), errs
 
 
+def test_norm_row_groups(monkeypatch):
+    """The 8-row-group residual norm (taken by launches of 2048+ rows), forced
+    onto small launches: ragged segments whose lengths are not multiples of 8,
+    split-K partial slices to add (the output and down projections split at
+    these row counts), a final add-only launch, and row widths in registers of
+    2, 16 and 20 float4 per lane (d_model 512, 4096, 5120)."""
+    monkeypatch.setenv("SVL_NORM8_MIN_ROWS", "0")
+    rng = np.random.default_rng(3)
+    for D, A, seqlens in ((512, 8, [70, 0, 1, 129, 200]), (5120, 8, [37, 250])):
+        shape = W.ModelShape(n_layers=1, d_model=D, n_heads=A, n_kv_heads=A // 2, head_dim=64,
+                             d_ffn=1024, n_groups=4, dtype="bf16")
+        B = len(seqlens)
+        head_mask = (rng.random((B, A)) > 0.3).astype(np.uint8)
+        ffn_mask = (rng.random((B, 4)) > 0.3).astype(np.uint8)
+        print(f"row-group norm: d_model {D}, rows {seqlens}", flush=True)
+        errs = _layer_case(shape, np.array(seqlens, np.int32), np.ones(B, np.uint8), head_mask,
+                           ffn_mask)
+        print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+        assert max(errs) <= tol_for(shape), errs
+    w = W.get_workload("llava7b_b1_keep25")
+    keep, lm, hm, fm = W.draw_masks(w, 0)
+    l = w.shape.prefix
+    print("row-group norm: headline layer", flush=True)
+    errs = _layer_case(w.shape, (keep + w.n_text).astype(np.int32), lm[:, l], hm[:, l], fm[:, l])
+    print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+
+
 def test_prefill_deterministic_and_flops():
     w = W.get_workload("llava7b_b8_ragged")
     w = W.scaled(w, n_layers=3, d_model=512, n_heads=4, n_kv_heads=4, d_ffn=1024, name="det")
