@@ -5,8 +5,10 @@
 //   1. every score is mapped to an unsigned key whose order is the required
 //      order: larger score -> larger key, -0 and +0 -> one key, NaN -> 0
 //      (below -inf, whose key is 0x007fffff);
-//   2. a 4-pass radix select (8 bits per pass, 256-bin LDS histogram) finds
-//      the k-th largest key T and how many keys equal to T are kept;
+//   2. a 4-pass radix select (8 bits per pass, 256-bin LDS histogram whose
+//      suffix counts come from a parallel scan; keys kept in LDS for samples
+//      of up to 16384 scores) finds the k-th largest key T and how many keys
+//      equal to T are kept;
 //   3. one ordered pass over the indices keeps key > T, and key == T while
 //      fewer than the needed number of equal keys have been seen (ties go to
 //      the lower index); wave ballots give the prefix counts, so the kept
@@ -47,35 +49,58 @@ __device__ __forceinline__ int block_excl_count(bool p, int* s_wave, int* total)
   return off + below;
 }
 
+// Keys of samples with at most this many scores stay in LDS across the passes.
+constexpr int SEL_LDS_KEYS = 16384;
+
 __global__ __launch_bounds__(NT) void select_kernel(const float* scores, int N, const int32_t* keep,
                                                     int32_t* kept_idx) {
+  static_assert(NT == 256, "one thread per histogram bin");
+  __shared__ uint32_t s_keys[SEL_LDS_KEYS];
   __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_wsum[NT / 64];
   __shared__ uint32_t s_digit, s_remaining;
   __shared__ int s_wave[NT / 64];
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const float* s = scores + (size_t)b * N;
   int32_t* out = kept_idx + (size_t)b * N;
   const int k = keep[b];
+  const bool cached = N <= SEL_LDS_KEYS;
+  auto key_at = [&](int i) { return cached ? s_keys[i] : score_key(s[i]); };
 
   if (k > 0 && k < N) {
+    if (cached) {
+      for (int i = tid; i < N; i += NT) s_keys[i] = score_key(s[i]);
+      __syncthreads();
+    }
     uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
     for (int shift = 24; shift >= 0; shift -= 8) {
       hist[tid] = 0;
       __syncthreads();
       for (int i = tid; i < N; i += NT) {
-        const uint32_t key = score_key(s[i]);
+        const uint32_t key = key_at(i);
         if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
       }
       __syncthreads();
-      if (tid == 0) {
-        uint32_t cum = 0;
-        int d = 255;
-        for (; d > 0; --d) {
-          if (cum + hist[d] >= remaining) break;
-          cum += hist[d];
-        }
-        s_digit = (uint32_t)d;
-        s_remaining = remaining - cum;
+      // Suffix counts S(t) = number of candidate keys whose digit is >= t
+      // (thread t holds bin t).  S(0) >= remaining > S(256) = 0, and S never
+      // increases, so exactly one bin has S(t) >= remaining > S(t + 1): the
+      // digit of the k-th largest key.
+      const uint32_t h = hist[tid];
+      uint32_t v = h;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t n = __shfl_down(v, o, 64);
+        if (lane + o < 64) v += n;
+      }
+      if (lane == 0) s_wsum[w] = v;
+      __syncthreads();
+      uint32_t above = 0;
+#pragma unroll
+      for (int j = 0; j < NT / 64; ++j) above += j > w ? s_wsum[j] : 0u;
+      const uint32_t S = v + above, S_next = S - h;
+      if (S >= remaining && S_next < remaining) {
+        s_digit = (uint32_t)tid;
+        s_remaining = remaining - S_next;
       }
       __syncthreads();
       prefix |= s_digit << shift;
@@ -88,7 +113,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* scores, int N, 
     int eq_seen = 0, written = 0;
     for (int c0 = 0; c0 < N; c0 += NT) {
       const int i = c0 + tid;
-      const uint32_t key = i < N ? score_key(s[i]) : 0u;
+      const uint32_t key = i < N ? key_at(i) : 0u;
       const bool gt = i < N && key > T;
       const bool eq = i < N && key == T;
       int eq_tot, keep_tot;
