@@ -23,7 +23,8 @@
  *   "host" pointers are ordinary host memory.
  * Streams.  `stream` is a hipStream_t passed as void* (NULL: the null
  *   stream).  All device work is enqueued on it; device outputs are valid once
- *   the stream reaches that point.  No call synchronises the stream.
+ *   the stream reaches that point.  No call synchronises the stream, except
+ *   svl_count_positive (its counts are host outputs).
  * Dtypes.  `svl_config.dtype` selects the storage type of weights and of the
  *   vision / text hidden states: SVL_F32 (float) or SVL_BF16 (bfloat16).  The
  *   residual stream `resid` is always float32.  SVL_BF16 runs 16-bit MFMA
@@ -178,6 +179,57 @@ size_t svl_workspace_bytes(const svl_config *cfg, int32_t batch, int32_t total_r
 svl_status svl_count_flops(const svl_config *cfg, int32_t batch, const int32_t *seqlens,
                            const uint8_t *layer_mask, const uint8_t *head_mask,
                            const uint8_t *ffn_mask, svl_flops *out);
+
+/* ---- threshold selection and budget projection -------------------------
+ * At inference the token controller keeps visual token i iff
+ * sigma(z_i) > 0.5, i.e. iff its logit z_i > 0 (Sec. 3.1), and for a budget
+ * b < 1 a deterministic projection brings the estimated prefill cost of
+ * Eq. (8) within b * C_full, discarding the lowest-confidence visual tokens
+ * first and reducing layers / heads only when that is not enough (Sec. 3.3
+ * "Inference").  The two calls below give the keep counts and the masks that
+ * svl_prefill then runs with, the logits serving as its scores (the kept
+ * tokens are the keep[b] largest logits, which are all positive). */
+
+/* Threshold counts: counts[b] = number of i with logits[b][i] > 0 (zero, -0
+ * and NaN do not count).
+ *   logits  dev float [batch][n_vision]
+ *   counts  host int32 [batch] (out)
+ *   ws/ws_bytes: device workspace of at least 4 * batch bytes.
+ * Unlike the other calls, this one synchronises `stream`: the counts come
+ * back to the host, which plans the prefill from them. */
+svl_status svl_count_positive(int32_t batch, int32_t n_vision, const float *logits,
+                              int32_t *counts, void *ws, size_t ws_bytes, void *stream);
+
+/* Budget projection, host only (no device work).  Per sample, with S =
+ * n_text + s, alpha_l = (active query heads of layer l) / A (0 for a skipped
+ * layer) and
+ *   C(s) = sum_l alpha_l [(8 D^2 + 6 D F) S + 4 D S^2] + 2 D V S    (Eq. (8)),
+ * C_full = C with every alpha_l = 1 and s = n_vision:
+ *   budget >= 1: keep[b] = counts[b], masks unchanged;
+ *   otherwise keep[b] = the largest s <= counts[b] with C(s) <= budget * C_full;
+ *   if even s = 0 does not fit, whole head groups (heads [j A/G, (j+1) A/G)
+ *   and FFN slice j) of layers l >= prefix are switched off one at a time,
+ *   lowest gate logit first (ties: the later layer, then the higher group;
+ *   without gate logits: the later layer first, then the higher group), a
+ *   layer left with no active head is skipped, until s = 0 fits, and keep[b]
+ *   is then the largest s that fits with the reduced masks; if every
+ *   eligible group is off and s = 0 still does not fit, keep[b] = 0.
+ * C(s) <= budget * C_full is decided exactly (budget at its exact float
+ * value, costs in integer arithmetic).
+ *   counts      host int32 [batch]: threshold counts, each in [0, n_vision]
+ *   budget      target fraction of C_full; finite and > 0 (else SVL_E_VALUE)
+ *   vocab       V of the LM-head term, >= 0 (0 leaves the term out)
+ *   prefix      P: layers 0..P-1 are never reduced, 0 <= P <= n_layers
+ *   layer_mask  host uint8 [batch][L] (in/out); head_mask host uint8
+ *               [batch][L][A] (in/out); ffn_mask host uint8 [batch][L][G]
+ *               (in/out) or NULL (FFN ungated)
+ *   gate_logits host float [batch][L][G] or NULL: the compute controller's
+ *               group logits (finite)
+ *   keep        host int32 [batch] (out) */
+svl_status svl_budget_project(const svl_config *cfg, int32_t batch, int32_t n_vision,
+                              int32_t n_text, const int32_t *counts, float budget, int64_t vocab,
+                              int32_t prefix, uint8_t *layer_mask, uint8_t *head_mask,
+                              uint8_t *ffn_mask, const float *gate_logits, int32_t *keep);
 
 /* Message for the last non-OK status returned on this thread. */
 const char *svl_last_error(void);

@@ -6,6 +6,7 @@ numpy arrays into its calls.
 """
 from .binding import (  # noqa: F401
     KCLASS, SVL_BF16, SVL_COMPUTE_BF16, SVL_COMPUTE_F16, SVL_F32, LayerTable, SvlError, alloc_workspace, layer_weights,
-    load_library, make_config, svl_abi_version, svl_count_flops, svl_layer_forward, svl_prefill,
-    svl_select_tokens, svl_timing_enable, svl_timing_read, svl_workspace_bytes,
+    load_library, make_config, svl_abi_version, svl_budget_project, svl_count_flops,
+    svl_count_positive, svl_layer_forward, svl_prefill, svl_select_tokens, svl_timing_enable,
+    svl_timing_read, svl_workspace_bytes,
 )

@@ -80,6 +80,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.svl_prefill.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), ctypes.POINTER(svl_batch),
                                 P, P, P, P, P, P, P, P, ctypes.POINTER(i32),
                                 ctypes.POINTER(svl_flops), P, sz, P]
+    lib.svl_count_positive.argtypes = [i32, i32, P, P, P, sz, P]
+    lib.svl_budget_project.argtypes = [cfgp, i32, i32, i32, P, ctypes.c_float, ctypes.c_int64,
+                                       i32, P, P, P, P, P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_workspace_bytes.restype = sz
     lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
@@ -90,7 +93,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.svl_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_int64)]
     for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
-              "svl_timing_enable", "svl_timing_read"):
+              "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -182,6 +185,36 @@ def svl_count_flops(cfg: svl_config, seqlens, layer_mask, head_mask, ffn_mask=No
     _check(load_library().svl_count_flops(ctypes.byref(cfg), int(sq.shape[0]), sqp, lmp, hmp, fmp,
                                           ctypes.byref(out)))
     return out.as_dict()
+
+
+def svl_count_positive(logits: torch.Tensor, ws: torch.Tensor, stream=None) -> np.ndarray:
+    """Threshold counts (logits > 0 per sample), host int32 [B]; synchronises the stream."""
+    B, N = logits.shape
+    counts = np.zeros(B, dtype=np.int32)
+    _check(load_library().svl_count_positive(int(B), int(N), _dev(logits, "logits"),
+                                             counts.ctypes.data_as(ctypes.c_void_p),
+                                             _dev(ws, "ws"), ws.numel(), _stream(stream)))
+    return counts
+
+
+def svl_budget_project(cfg: svl_config, counts, n_vision: int, n_text: int, budget: float,
+                       vocab: int, prefix: int, layer_mask, head_mask, ffn_mask=None,
+                       gate_logits=None):
+    """Budget projection (host only): returns (keep [B], layer_mask, head_mask, ffn_mask)
+    after the projection; the inputs are not modified."""
+    cnt, cntp = _host_i32(counts)
+    B = int(cnt.shape[0])
+    lm = np.array(layer_mask, dtype=np.uint8, copy=True, order="C")
+    hm = np.array(head_mask, dtype=np.uint8, copy=True, order="C")
+    fm = None if ffn_mask is None else np.array(ffn_mask, dtype=np.uint8, copy=True, order="C")
+    gl = None if gate_logits is None else np.ascontiguousarray(np.asarray(gate_logits, dtype=np.float32))
+    keep = np.zeros(B, dtype=np.int32)
+    vp = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    _check(load_library().svl_budget_project(
+        ctypes.byref(cfg), B, int(n_vision), int(n_text), cntp, ctypes.c_float(budget),
+        ctypes.c_int64(int(vocab)), int(prefix), vp(lm), vp(hm), vp(fm), vp(gl),
+        keep.ctypes.data_as(ctypes.c_void_p)))
+    return keep, lm, hm, fm
 
 
 def svl_select_tokens(cfg: svl_config, keep, scores: torch.Tensor, vision: torch.Tensor,

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "../../include/svl.h"
+#include "budget.h"
 #include "plan.h"
 #include "svl_internal.h"
 
@@ -576,6 +577,55 @@ svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, c
   }
   hipError_t e = ex.norm(t_plan.final_norm, nullptr);
   if (e != hipSuccess) return hip_fail(e, "final residual launch");
+  return SVL_OK;
+}
+
+svl_status svl_count_positive(int32_t batch, int32_t n_vision, const float* logits,
+                              int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+  if (batch <= 0 || n_vision < 0) return fail(SVL_E_SHAPE, "batch must be positive, n_vision >= 0");
+  if (!logits || !counts || !ws) return fail(SVL_E_NULL, "NULL argument");
+  if (reinterpret_cast<uintptr_t>(logits) % 16 || reinterpret_cast<uintptr_t>(ws) % 16)
+    return fail(SVL_E_VALUE, "device pointers must be 16-byte aligned");
+  if (ws_bytes < (size_t)batch * 4) return fail(SVL_E_WORKSPACE, "workspace below 4 * batch bytes");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* dev = static_cast<int32_t*>(ws);
+  hipError_t e = launch_count_positive(logits, batch, n_vision, dev, st);
+  if (e != hipSuccess) return hip_fail(e, "threshold count");
+  e = hipMemcpyAsync(counts, dev, (size_t)batch * 4, hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return hip_fail(e, "threshold count copy");
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "threshold count sync");
+  return SVL_OK;
+}
+
+svl_status svl_budget_project(const svl_config* cfg, int32_t batch, int32_t n_vision,
+                              int32_t n_text, const int32_t* counts, float budget, int64_t vocab,
+                              int32_t prefix, uint8_t* layer_mask, uint8_t* head_mask,
+                              uint8_t* ffn_mask, const float* gate_logits, int32_t* keep) {
+  svl_status s = check_config(cfg, false);
+  if (s != SVL_OK) return s;
+  if (batch <= 0 || n_vision < 0 || n_text < 0)
+    return fail(SVL_E_SHAPE, "batch must be positive, token counts >= 0");
+  if (!counts || !layer_mask || !head_mask || !keep) return fail(SVL_E_NULL, "NULL argument");
+  if (!std::isfinite(budget) || !(budget > 0.f)) return fail(SVL_E_VALUE, "budget must be finite and > 0");
+  if (vocab < 0) return fail(SVL_E_VALUE, "vocab must be >= 0");
+  const int64_t L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
+  if (A % G) return fail(SVL_E_SHAPE, "n_heads %% n_groups != 0 (head groups)");
+  if (prefix < 0 || prefix > L) return fail(SVL_E_VALUE, "prefix outside [0, n_layers]");
+  if ((s = check_mask(layer_mask, batch * L, "layer_mask")) != SVL_OK) return s;
+  if ((s = check_mask(head_mask, batch * L * A, "head_mask")) != SVL_OK) return s;
+  if (ffn_mask && (s = check_mask(ffn_mask, batch * L * G, "ffn_mask")) != SVL_OK) return s;
+  for (int32_t b = 0; b < batch; ++b)
+    if (counts[b] < 0 || counts[b] > n_vision)
+      return fail(SVL_E_VALUE, "counts[%d] = %d outside [0, %d]", b, counts[b], n_vision);
+  if (gate_logits)
+    for (int64_t i = 0; i < batch * L * G; ++i)
+      if (!std::isfinite(gate_logits[i])) return fail(SVL_E_VALUE, "gate_logits[%lld] is not finite", (long long)i);
+  for (int32_t b = 0; b < batch; ++b)
+    keep[b] = project_budget_sample(*cfg, n_vision, n_text, counts[b], budget, vocab, prefix,
+                                    layer_mask + b * L, head_mask + b * L * A,
+                                    ffn_mask ? ffn_mask + b * L * G : nullptr,
+                                    gate_logits ? gate_logits + b * L * G : nullptr);
   return SVL_OK;
 }
 

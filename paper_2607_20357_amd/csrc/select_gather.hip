@@ -130,6 +130,27 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* scores, int N, 
   for (int i = k + tid; i < N; i += NT) out[i] = -1;
 }
 
+// Threshold count, one workgroup per sample: visual tokens with
+// sigma(z) > 0.5, i.e. z > 0 (zero, -0 and NaN are not counted).
+__global__ __launch_bounds__(NT) void count_positive_kernel(const float* logits, int N,
+                                                            int32_t* counts) {
+  __shared__ int s_wave[NT / 64];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const float* z = logits + (size_t)b * N;
+  int n = 0;
+  for (int i = tid; i < N; i += NT) n += z[i] > 0.0f ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o, 64);
+  if ((tid & 63) == 0) s_wave[tid >> 6] = n;
+  __syncthreads();
+  if (tid == 0) {
+    int tot = 0;
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) tot += s_wave[i];
+    counts[b] = tot;
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(NT) void gather_kernel(const int32_t* kept_idx, const int32_t* keep,
                                                     const int32_t* cu, int B, int N, int T, int D,
@@ -173,6 +194,13 @@ hipError_t launch_select(const float* scores, int32_t B, int32_t N, const int32_
                          int32_t* kept_idx, hipStream_t st) {
   if (B <= 0 || N <= 0) return hipSuccess;
   select_kernel<<<B, NT, 0, st>>>(scores, N, keep_dev, kept_idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_positive(const float* logits, int32_t B, int32_t N, int32_t* counts,
+                                 hipStream_t st) {
+  if (B <= 0) return hipSuccess;
+  count_positive_kernel<<<B, NT, 0, st>>>(logits, N, counts);
   return hipGetLastError();
 }
 

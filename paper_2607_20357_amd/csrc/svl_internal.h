@@ -111,6 +111,8 @@ struct NormArgs {
 
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipSuccess or the launch error).
+hipError_t launch_count_positive(const float* logits, int32_t B, int32_t N, int32_t* counts,
+                                 hipStream_t st);
 hipError_t launch_select(const float* scores, int32_t B, int32_t N, const int32_t* keep_dev,
                          int32_t* kept_idx, hipStream_t st);
 hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const int32_t* cu_dev,

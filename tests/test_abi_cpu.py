@@ -145,3 +145,70 @@ def test_workspace_bytes_monotone():
     c = svl.svl_workspace_bytes(cfg, 4, 1000)
     assert 0 < a < b <= c
     assert svl.load_library().svl_workspace_bytes(None, 1, 1) == 0
+
+
+# --------------------------------------------------------------------------- budget projection
+from oracle import budget as obudget  # noqa: E402
+
+BUDGET_SHAPES = [
+    ModelShape(n_layers=6, d_model=64, n_heads=8, n_kv_heads=8, head_dim=8, d_ffn=128,
+               n_groups=4, dtype="f32"),
+    ModelShape(n_layers=32, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128,
+               d_ffn=11008, n_groups=4, dtype="bf16"),
+    ModelShape(n_layers=28, d_model=3584, n_heads=28, n_kv_heads=4, head_dim=128,
+               d_ffn=18944, n_groups=4, dtype="bf16"),
+]
+
+
+@pytest.mark.parametrize("si", range(len(BUDGET_SHAPES)))
+def test_budget_projection_matches_oracle(si):
+    """svl_budget_project (host code of the library) against the oracle:
+    identical keep counts and projected masks, for budgets from 0.002 to 1.2,
+    with and without FFN gating and gate logits, vocab 0 and 32000."""
+    shape = BUDGET_SHAPES[si]
+    cfg = svl.make_config(shape)
+    L, A, G = shape.n_layers, shape.n_heads, shape.n_groups
+    rng = np.random.default_rng(si)
+    n_vision, n_text, B = (40, 7, 5) if si == 0 else (576, 64, 3)
+    reduced = 0
+    for trial in range(24):
+        counts = rng.integers(0, n_vision + 1, B).astype(np.int32)
+        counts[0] = n_vision
+        lm = (rng.random((B, L)) > 0.2).astype(np.uint8)
+        hm = (rng.random((B, L, A)) > 0.25).astype(np.uint8)
+        fm = (rng.random((B, L, G)) > 0.25).astype(np.uint8) if trial % 2 else None
+        gl = rng.normal(0, 1, (B, L, G)).astype(np.float32) if trial % 3 else None
+        budget = float(rng.choice([1.2, 1.0, 0.9, 0.5, 0.25, 0.12, 0.05, 0.02, 0.008, 0.002]))
+        vocab = 32000 if trial % 4 == 1 else 0
+        prefix = int(rng.integers(0, L // 2 + 1))
+        keep, lm2, hm2, fm2 = svl.svl_budget_project(cfg, counts, n_vision, n_text, budget, vocab,
+                                                     prefix, lm, hm, fm, gl)
+        # the oracle takes logits; any logits with these threshold counts will do
+        logits = np.full((B, n_vision), -1.0, np.float32)
+        for b in range(B):
+            logits[b, :counts[b]] = 1.0
+        wk, wlm, whm, wfm = obudget.project_batch(shape, logits, n_text, budget, vocab, prefix,
+                                                  lm, hm, fm, gl)
+        np.testing.assert_array_equal(keep, wk)
+        np.testing.assert_array_equal(lm2, wlm)
+        np.testing.assert_array_equal(hm2, whm)
+        if fm is not None:
+            np.testing.assert_array_equal(fm2, wfm)
+        reduced += int(not np.array_equal(hm2, hm))
+    assert reduced > 0          # the layer / head step was exercised
+
+
+def test_budget_projection_rejects_bad_arguments():
+    shape = BUDGET_SHAPES[0]
+    cfg = svl.make_config(shape)
+    L, A, G = shape.n_layers, shape.n_heads, shape.n_groups
+    lm, hm = np.ones((1, L), np.uint8), np.ones((1, L, A), np.uint8)
+    ok = dict(counts=[3], n_vision=10, n_text=2, budget=0.5, vocab=0, prefix=0,
+              layer_mask=lm, head_mask=hm)
+    svl.svl_budget_project(cfg, **ok)
+    for bad in (dict(budget=float("nan")), dict(budget=0.0), dict(budget=-1.0),
+                dict(budget=float("inf")), dict(vocab=-1), dict(prefix=L + 1), dict(counts=[11]),
+                dict(counts=[-1]), dict(head_mask=np.full((1, L, A), 2, np.uint8)),
+                dict(gate_logits=np.full((1, L, G), np.nan, np.float32))):
+        with pytest.raises(svl.SvlError):
+            svl.svl_budget_project(cfg, **{**ok, **bad})

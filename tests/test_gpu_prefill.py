@@ -195,6 +195,56 @@ def test_norm_row_groups(monkeypatch):
     assert max(errs) <= tol_for(w.shape), errs
 
 
+def test_threshold_budget_prefill():
+    """Threshold selection and the budget projection feeding the prefill
+    (Sec. 3.1, Sec. 3.3): GPU threshold counts, the library's projection and
+    the prefill on the projected keep counts and masks, against the oracle's
+    projection and prefill; kept indices exact, hidden states within the
+    tolerance."""
+    import dataclasses
+    from oracle import budget as obudget
+    cases = (("tiny_f32", None, (0.5, 0.08)),
+             ("llava7b_b8_ragged", dict(n_layers=4, d_model=512, n_heads=8, n_kv_heads=8,
+                                        d_ffn=1024, name="thr"), (0.4, 0.1)))
+    bound = reduced = 0
+    for name, scale, budgets in cases:
+        w = W.get_workload(name)
+        if scale:
+            w = W.scaled(w, **scale)
+        inp = W.draw_inputs(w, 5, device="cuda")
+        layers = [W.draw_layer_weights(w, l, 5, device="cuda") for l in range(w.shape.n_layers)]
+        B, N = inp.scores.shape
+        rng = np.random.default_rng(5)
+        logits = (rng.standard_normal((B, N)) - 0.3).astype(np.float32)
+        logits[0, :3] = 0.0
+        logits[-1, 5] = np.nan
+        ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+        counts = svl.svl_count_positive(torch.from_numpy(logits).cuda(), ws)
+        np.testing.assert_array_equal(counts, [obudget.threshold_count(logits[b]) for b in range(B)])
+        cfg = svl.make_config(w.shape)
+        P = w.shape.n_layers // 2
+        for budget in budgets:
+            keep, lm, hm, fm = svl.svl_budget_project(cfg, counts, N, w.n_text, budget, 0, P,
+                                                      inp.layer_mask, inp.head_mask, inp.ffn_mask)
+            wk, wlm, whm, wfm = obudget.project_batch(w.shape, logits, w.n_text, budget, 0, P,
+                                                      inp.layer_mask, inp.head_mask, inp.ffn_mask)
+            np.testing.assert_array_equal(keep, wk)
+            np.testing.assert_array_equal(hm, whm)
+            bound += int(np.any(keep < counts))
+            reduced += int(not np.array_equal(hm, inp.head_mask))
+            inp2 = dataclasses.replace(inp, scores=logits, keep=keep, layer_mask=lm, head_mask=hm,
+                                       ffn_mask=fm)
+            print(f"{name} budget {budget}: counts {counts.tolist()} keep {keep.tolist()}", flush=True)
+            kept, cu, got, _ = gpu_prefill(w, inp2, layers)
+            ref = oracle_prefill(w, inp2, layers)
+            np.testing.assert_array_equal(kept, ref.kept_idx)
+            np.testing.assert_array_equal(cu, ref.cu_seqlens)
+            errs = rel_err_per_sample(got, ref.resid, cu)
+            print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+            assert max(errs) <= tol_for(w.shape), errs
+    assert bound > 0 and reduced > 0
+
+
 def test_prefill_deterministic_and_flops():
     w = W.get_workload("llava7b_b8_ragged")
     w = W.scaled(w, n_layers=3, d_model=512, n_heads=4, n_kv_heads=4, d_ffn=1024, name="det")

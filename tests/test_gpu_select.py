@@ -108,3 +108,20 @@ def test_dropped_rows_are_not_read():
     text = torch.randn(B, T, D).to(torch.bfloat16)
     kept, cu, resid = _run(cfg, keep, scores, vision.cuda(), text.cuda())
     assert np.isfinite(resid).all()
+
+
+def test_count_positive_exact():
+    """Threshold counts (sigma(z) > 0.5, i.e. z > 0) on the GPU equal the
+    oracle's, including zeros, -0, NaN, +-inf and ragged lengths."""
+    from oracle import budget as obudget
+    rng = np.random.default_rng(21)
+    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    for N in [1, 7, 255, 256, 257, 576, 3136]:
+        for kind in ["special", "lognormal", "negative", "ties"]:
+            B = 5
+            z = _scores(kind, B, N, rng)
+            if kind == "ties":
+                z = z - 0.5                 # values in {-0.5, -0.25, 0, 0.25, 0.5}
+            got = svl.svl_count_positive(torch.from_numpy(z).cuda(), ws)
+            want = np.array([obudget.threshold_count(z[b]) for b in range(B)])
+            np.testing.assert_array_equal(got, want)
