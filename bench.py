@@ -51,6 +51,11 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run one plain device copy of COPY_BYTES (the known-size kernel "
                         "that scales the FETCH_SIZE / WRITE_SIZE counters of a --pmc run)")
+    p.add_argument("--threshold-budget", type=float, default=None, metavar="B",
+                   help="instead of the integer keep budget: threshold selection (logits > 0) "
+                        "and the budget projection to B * C_full inside each step, on the "
+                        "headline shapes and masks with logits N(0,1) - 0.674 (a quarter of "
+                        "the tokens positive)")
     p.add_argument("--memory-sweep", action="store_true",
                    help="instead of the step benchmark: HBM rate of the memory-bound kernels "
                         "(select, gather, residual norm) on the headline per-row structure "
@@ -312,10 +317,37 @@ def main():
     ws = svl.alloc_workspace(cfg, B, R, dev)
     stream = torch.cuda.current_stream()
 
-    def step():
-        svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
-                        inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
-                        want_flops=False)
+    keep_run, lm_run, hm_run, fm_run = inp.keep, inp.layer_mask, inp.head_mask, inp.ffn_mask
+    if args.threshold_budget is not None:
+        # logits of the token controller (seeded; a quarter positive) and the
+        # projection's cost terms: no LM head (V = 0), prefix P = L / 2
+        rng = np.random.default_rng([args.seed, 7])
+        logits_np = (rng.standard_normal((B, N)) - 0.6745).astype(np.float32)
+        scores = torch.from_numpy(logits_np).to(dev)
+        count_ws = torch.empty(max(256, 4 * B), dtype=torch.uint8, device=dev)
+        prefix = shape.n_layers // 2
+
+        def project():
+            counts = svl.svl_count_positive(scores, count_ws, stream=stream)
+            return counts, svl.svl_budget_project(cfg, counts, N, w.n_text, args.threshold_budget,
+                                                  0, prefix, inp.layer_mask, inp.head_mask,
+                                                  inp.ffn_mask)
+
+        counts0, (keep_run, lm_run, hm_run, fm_run) = project()
+        seqlens = (np.asarray(keep_run) + w.n_text).astype(np.int64)
+        R = int(seqlens.sum())
+        resid = torch.empty((R, shape.d_model), dtype=torch.float32, device=dev)
+        ws = svl.alloc_workspace(cfg, B, R, dev)
+
+        def step():
+            _, (k, lm, hm, fm) = project()
+            svl.svl_prefill(cfg, table, k, scores, inp.vision, inp.text, lm, hm, fm, kept, resid,
+                            ws, stream=stream, want_flops=False)
+    else:
+        def step():
+            svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
+                            inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
+                            want_flops=False)
 
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -348,15 +380,15 @@ def main():
     svl.svl_timing_enable(False)
     ktime = {k: svl.svl_timing_read(k) for k in svl.KCLASS}
 
-    flops = svl.svl_count_flops(cfg, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    flops = svl.svl_count_flops(cfg, seqlens, lm_run, hm_run, fm_run)
     gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
     gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / args.steps
     attn_ms = ktime["attention"][0] / args.steps
     tokens = B * (w.n_vision + w.n_text)
     value = tokens / (ms * 1e-3)
 
-    bytes_, launches = gemm_bytes(shape, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
-    traffic = measured_traffic() if w.name == W.HEADLINE else None
+    bytes_, launches = gemm_bytes(shape, seqlens, lm_run, hm_run, fm_run)
+    traffic = measured_traffic() if w.name == W.HEADLINE and args.threshold_budget is None else None
     gu_ms, gu_n = ktime["gemm_gate_up"]
     gu_avg_ms = gu_ms / max(1, gu_n)
     gu_bytes_per_launch = bytes_["gu"] / max(1, launches["gu"])
@@ -365,7 +397,10 @@ def main():
                   for k, v in ktime.items() if v[1]}
 
     result = {
-        "metric": "effective prefill tokens/s + MFMA util (% peak), 7B-shaped, keep 0.25",
+        "metric": ("effective prefill tokens/s + MFMA util (% peak), 7B-shaped, keep 0.25"
+                   if args.threshold_budget is None else
+                   f"effective prefill tokens/s, 7B-shaped, threshold selection + budget "
+                   f"projection to {args.threshold_budget} of C_full"),
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -379,9 +414,11 @@ def main():
         "dtype": "f16" if shape.dtype == "bf16" else "f32",
         "storage_dtype": shape.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "batch": B, "n_vision": w.n_vision, "n_text": w.n_text,
-                   "keep": [int(k) for k in inp.keep], "kept_tokens": R,
-                   "layers_executed_per_sample": [int(x) for x in inp.layer_mask.sum(1)],
+        "config": {"workload": w.name if args.threshold_budget is None else
+                   f"{w.name}_threshold_b{args.threshold_budget}",
+                   "batch": B, "n_vision": w.n_vision, "n_text": w.n_text,
+                   "keep": [int(k) for k in keep_run], "kept_tokens": R,
+                   "layers_executed_per_sample": [int(x) for x in np.asarray(lm_run).sum(1)],
                    "n_layers": shape.n_layers, "d_model": shape.d_model,
                    "heads": shape.n_heads, "kv_heads": shape.n_kv_heads,
                    "d_ffn": shape.d_ffn, "parallelism": "none (1 GPU)"},
@@ -404,7 +441,14 @@ def main():
             "traffic_source": os.path.relpath(TRAFFIC_FILE, ROOT) if traffic else None,
         },
     }
-    if not args.no_cpu_baseline:
+    if args.threshold_budget is not None:
+        result["threshold"] = {"positive_logits": [int(c) for c in counts0], "budget": args.threshold_budget,
+                               "vocab_term": 0, "prefix_layers": shape.n_layers // 2,
+                               "groups_dropped_by_projection":
+                                   int(np.sum(np.asarray(inp.head_mask) != np.asarray(hm_run)) //
+                                       (shape.n_heads // shape.n_groups)),
+                               "step": "count kernel + host sync + projection + prefill"}
+    if not args.no_cpu_baseline and args.threshold_budget is None:
         result["cpu_baseline"] = cpu_baseline(w, inp, layers, args.cpu_layers)
     print(json.dumps(result))
 

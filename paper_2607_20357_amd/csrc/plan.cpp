@@ -30,6 +30,16 @@ struct ImageWriter {
     if (!v.empty()) std::memcpy(img->data() + off, v.data(), v.size() * sizeof(T));
     return off;
   }
+  // room for n records of T at the end of the image (filled by the caller
+  // through at<T>() before the next append)
+  template <class T>
+  int64_t reserve(int64_t n) {
+    int64_t off = align16((int64_t)img->size());
+    img->resize(off + n * (int64_t)sizeof(T));
+    return off;
+  }
+  template <class T>
+  T* at(int64_t off) { return reinterpret_cast<T*>(img->data() + off); }
 };
 
 struct Range {
@@ -123,36 +133,42 @@ struct MmBuild {
   // evenly; tiles that share weight blocks (M tiles) and split-K pieces are
   // consecutive, so they land on one XCD.
   GemmLaunch finish(ImageWriter& w, int32_t bpt, int32_t nb, int32_t nsplit) {
-    std::vector<MmTile> tiles;
+    GemmLaunch L;
+    L.groups_off = w.append(groups);
+    int64_t count = 0;
+    for (const auto& g : groups)
+      count += (int64_t)cdiv(g.nblocks, bpt) * cdiv(g.nrows, MFMA_BM) * nsplit;
+    L.tiles_off = w.reserve<MmTile>(count);
+    MmTile* out = w.at<MmTile>(L.tiles_off);
+    int64_t n = 0;
+    int32_t kc[MFMA_MAX_SPLIT + 1];
     for (int32_t gi = 0; gi < (int32_t)groups.size(); ++gi) {
       const MmGroup& g = groups[gi];
       const int32_t nt = cdiv(g.nblocks, bpt), nm = cdiv(g.nrows, MFMA_BM);
+      for (int32_t p = 0; p <= nsplit; ++p) kc[p] = (int32_t)((int64_t)g.kc_cnt * p / nsplit);
+      MmTile t{};   // the fields shared by the group's tiles
+      t.wsel = g.wsel; t.wrow0 = g.wrow0; t.ocol0 = g.ocol0; t.rope = g.rope; t.group = gi;
+      int32_t b0 = 0;
       for (int32_t q = 0; q < nt; ++q) {
-        const int32_t b0 = (int32_t)((int64_t)q * g.nblocks / nt);
         const int32_t b1 = (int32_t)((int64_t)(q + 1) * g.nblocks / nt);
-        for (int32_t mt = 0; mt < nm; ++mt)
+        t.b0 = b0; t.nblk = b1 - b0;
+        for (int32_t mt = 0; mt < nm; ++mt) {
+          const int32_t m0 = mt * MFMA_BM;
+          t.arow = g.arow0 + m0; t.orow = g.orow0 + m0;
+          t.mcnt = std::min(MFMA_BM, g.nrows - m0); t.pos0 = m0;
           for (int32_t p = 0; p < nsplit; ++p) {
-            MmTile t{};
-            const int32_t m0 = mt * MFMA_BM;
-            const int32_t kc0 = (int32_t)((int64_t)g.kc_cnt * p / nsplit);
-            t.arow = g.arow0 + m0; t.orow = g.orow0 + m0;
-            t.mcnt = std::min(MFMA_BM, g.nrows - m0); t.pos0 = m0;
-            t.wsel = g.wsel; t.wrow0 = g.wrow0; t.ocol0 = g.ocol0; t.rope = g.rope;
-            t.chunk0 = g.kc_off + kc0;
-            t.kcn = (int32_t)((int64_t)g.kc_cnt * (p + 1) / nsplit) - kc0;
-            t.kdense = g.kdense >= 0 ? g.kdense + MFMA_BK * kc0 : -1;
-            t.b0 = b0; t.nblk = b1 - b0;
+            t.chunk0 = g.kc_off + kc[p];
+            t.kcn = kc[p + 1] - kc[p];
+            t.kdense = g.kdense >= 0 ? g.kdense + MFMA_BK * kc[p] : -1;
             t.slice = p;
-            t.group = gi;
-            tiles.push_back(t);
+            out[n++] = t;
           }
+        }
+        b0 = b1;
       }
     }
-    GemmLaunch L;
-    L.groups_off = w.append(groups);
-    L.tiles_off = w.append(tiles);
     L.ngroups = (int32_t)groups.size();
-    L.ntiles = (int32_t)tiles.size();
+    L.ntiles = (int32_t)count;
     L.nb = nb;
     L.nsplit = nsplit;
     return L;
