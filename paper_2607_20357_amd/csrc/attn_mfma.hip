@@ -97,6 +97,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < GT; ++j) {
       const int kv0 = g0 + j * BKV;
+      if (kv0 >= kv_end) break;   // past the query tile's causal range (uniform)
 #pragma unroll
       for (int i = 0; i < KT; ++i) {
         const int task = min(tid + i * NT, KTASKS - 1), row = task / (D / 8), c = task % (D / 8);
@@ -115,9 +116,10 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
       }
     }
   };
-  auto store_group = [&]() __attribute__((always_inline)) {
+  auto store_group = [&](int g0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < GT; ++j) {
+      if (g0 + j * BKV >= kv_end) break;   // not loaded, not read
 #pragma unroll
       for (int i = 0; i < KT; ++i) {
         const int task = tid + i * NT, row = task / (D / 8), c = task % (D / 8);
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   load_group(0);
   for (int g0 = 0; g0 < kv_end; g0 += GT * BKV) {
     __syncthreads();   // the previous group's readers are done
-    store_group();
+    store_group(g0);
     __syncthreads();
     if (g0 + GT * BKV < kv_end) load_group(g0 + GT * BKV);
 #pragma unroll

@@ -115,8 +115,15 @@ __global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
 // with every load of a batch in flight at once, the row stays in registers
 // for the normed output, and the residual is written back once.  Slices are
 // added in slice order, as in the general kernel.
+#ifndef SVL_NORM_NT
+#define SVL_NORM_NT 1024
+#endif
+constexpr int NTR = SVL_NORM_NT;   // threads of the one-row-per-workgroup kernel (1024: the
+                                   // most loads of the row and its slices in flight at once)
+
 template <int OUT, int VPT>
-__global__ __launch_bounds__(NT) void resid_norm_reg_kernel(NormArgs a) {
+__global__ __launch_bounds__(NTR) void resid_norm_reg_kernel(NormArgs a) {
+  constexpr int NT = NTR;
   __shared__ float s_part[NT / 64];
   const int r = blockIdx.x;
   const NormSeg sg = find_seg(a, r);
@@ -304,10 +311,10 @@ hipError_t launch_norm(const NormArgs& a, hipStream_t st) {
       return hipGetLastError();
     }
   }
-  if (d4 <= NT) resid_norm_reg_kernel<OUT, 1><<<a.nrows, NT, 0, st>>>(a);
-  else if (d4 <= 2 * NT) resid_norm_reg_kernel<OUT, 2><<<a.nrows, NT, 0, st>>>(a);
-  else if (d4 <= 4 * NT) resid_norm_reg_kernel<OUT, 4><<<a.nrows, NT, 0, st>>>(a);
-  else if (d4 <= 8 * NT) resid_norm_reg_kernel<OUT, 8><<<a.nrows, NT, 0, st>>>(a);
+  if (d4 <= NTR) resid_norm_reg_kernel<OUT, 1><<<a.nrows, NTR, 0, st>>>(a);
+  else if (d4 <= 2 * NTR) resid_norm_reg_kernel<OUT, 2><<<a.nrows, NTR, 0, st>>>(a);
+  else if (d4 <= 4 * NTR) resid_norm_reg_kernel<OUT, 4><<<a.nrows, NTR, 0, st>>>(a);
+  else if (d4 <= 8 * NTR) resid_norm_reg_kernel<OUT, 8><<<a.nrows, NTR, 0, st>>>(a);
   else resid_norm_kernel<OUT><<<a.nrows, NT, 0, st>>>(a);
   return hipGetLastError();
 }
