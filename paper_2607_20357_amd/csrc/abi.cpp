@@ -328,12 +328,65 @@ svl_status hip_fail(hipError_t e, const char* where) {
   return fail(SVL_E_HIP, "%s: %s", where, hipGetErrorString(e));
 }
 
+// Plan uploads go through two pinned host buffers per thread, used in turn:
+// the image is copied into one (after the copy that last read it has
+// completed, which its event tells) and the stream copies it to the
+// workspace asynchronously, so the host does not stage pageable memory
+// while the GPU waits.  The buffers and events live until the process ends
+// (they are never released, so no teardown runs after the HIP runtime's).
+struct PinnedRing {
+  uint8_t* buf[2] = {nullptr, nullptr};
+  size_t cap[2] = {0, 0};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  bool pending[2] = {false, false};
+  int next = 0;
+  int device = -1;   // the events belong to this device
+};
+thread_local PinnedRing t_ring;
+
+hipError_t upload_plan(uint8_t* dst, const uint8_t* src, size_t n, hipStream_t st) {
+  PinnedRing& r = t_ring;
+  hipError_t e;
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if (dev != r.device) {
+    // another device: let the pending copies finish, then start fresh events
+    // (the old ones are left to the process end, like the buffers)
+    for (int j = 0; j < 2; ++j) {
+      if (r.pending[j] && (e = hipEventSynchronize(r.done[j])) != hipSuccess) return e;
+      r.pending[j] = false;
+      r.done[j] = nullptr;
+    }
+    r.device = dev;
+  }
+  const int i = r.next;
+  r.next ^= 1;
+  if (!r.done[i] && (e = hipEventCreateWithFlags(&r.done[i], hipEventDisableTiming)) != hipSuccess)
+    return e;
+  if (r.pending[i] && (e = hipEventSynchronize(r.done[i])) != hipSuccess) return e;
+  r.pending[i] = false;
+  if (r.cap[i] < n) {
+    if (r.buf[i] && (e = hipHostFree(r.buf[i])) != hipSuccess) return e;
+    r.buf[i] = nullptr;
+    r.cap[i] = 0;
+    const size_t cap = n + n / 2 + 4096;
+    void* p = nullptr;
+    if ((e = hipHostMalloc(&p, cap, hipHostMallocDefault)) != hipSuccess) return e;
+    r.buf[i] = static_cast<uint8_t*>(p);
+    r.cap[i] = cap;
+  }
+  std::memcpy(r.buf[i], src, n);
+  if ((e = hipMemcpyAsync(dst, r.buf[i], n, hipMemcpyHostToDevice, st)) != hipSuccess) return e;
+  if ((e = hipEventRecord(r.done[i], st)) != hipSuccess) return e;
+  r.pending[i] = true;
+  return hipSuccess;
+}
+
 // Copies the plan image and builds the RoPE table.
 svl_status stage(const Exec& ex, bool need_layers) {
   if ((int64_t)ex.plan.image.size() > ex.L.rope - ex.L.plan)
     return fail(SVL_E_SHAPE, "internal: plan image exceeds its workspace region");
-  hipError_t e = hipMemcpyAsync(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(),
-                                hipMemcpyHostToDevice, ex.st);
+  hipError_t e = upload_plan(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(), ex.st);
   if (e != hipSuccess) return hip_fail(e, "plan upload");
   if (need_layers) {
     e = timed(K_ROPE, ex.st, [&] {
