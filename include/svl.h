@@ -231,6 +231,58 @@ svl_status svl_budget_project(const svl_config *cfg, int32_t batch, int32_t n_vi
                               int32_t prefix, uint8_t *layer_mask, uint8_t *head_mask,
                               uint8_t *ffn_mask, const float *gate_logits, int32_t *keep);
 
+/* ---- decode on the pruned and gated KV cache ----------------------------
+ * After the prefill, tokens are generated one at a time; the paper leaves
+ * this stage to future work (Sec. 5).  The cache holds only what the prefill
+ * computed: the kept tokens' rows (the compressed sequence of Sec. 3.1) and,
+ * per layer, only the active K/V heads of samples that run the layer
+ * (Sec. 3.2).  A decode step runs the same decoder, under the sample's same
+ * masks, on one new token per sample at position p = the sample's cached
+ * length: its queries attend to the cached keys / values of positions 0..p-1
+ * and to its own.  Its result equals the last row of a prefill over the
+ * sequence extended by that token (causal attention).  16-bit path only
+ * (SVL_BF16 storage; SVL_E_DTYPE otherwise).
+ *
+ * Cache layout (dev, activation type: fp16, or bf16 with SVL_COMPUTE_BF16):
+ *   [n_layers][batch][n_kv_heads][2 (K, V)][max_len][head_dim], K rotated
+ *   (RoPE at its position).  Entries of skipped layers and inactive heads
+ *   are neither written nor read. */
+
+/* Bytes of a cache for `batch` samples of up to `max_len` positions (0 on bad
+ * arguments; max_len <= 32768). */
+size_t svl_kv_cache_bytes(const svl_config *cfg, int32_t batch, int32_t max_len);
+
+/* The whole prefill (as svl_prefill) that also writes every layer's K / V of
+ * the executed rows into the cache at positions 0..S_b-1.  max_len >= every
+ * S_b (else SVL_E_SHAPE). */
+svl_status svl_prefill_cache(const svl_config *cfg, const svl_layer_weights *layers,
+                             const svl_batch *batch, const float *scores, const void *vision,
+                             const void *text, const uint8_t *layer_mask,
+                             const uint8_t *head_mask, const uint8_t *ffn_mask,
+                             int32_t *kept_idx, float *resid, int32_t *cu_seqlens,
+                             void *kv_cache, int32_t max_len, void *ws, size_t ws_bytes,
+                             void *stream);
+
+/* Workspace bytes of svl_decode_step for `batch` samples and caches of up to
+ * `max_len` positions (0 on bad arguments). */
+size_t svl_decode_workspace_bytes(const svl_config *cfg, int32_t batch, int32_t max_len);
+
+/* One decode step: sample b's new token at position cache_len[b].
+ *   layers     host array of cfg->n_layers svl_layer_weights
+ *   x          dev float [batch][D]: the new tokens' hidden states in, their
+ *              residual after the last layer out (no final norm, no LM head)
+ *   cache_len  host int32 [batch]: positions already cached, each < max_len;
+ *              the step writes position cache_len[b] of every executed layer
+ *              (the caller then advances cache_len)
+ *   layer_mask, head_mask, ffn_mask: as svl_prefill (the sample's masks)
+ *   kv_cache, max_len: as svl_prefill_cache
+ *   ws/ws_bytes: at least svl_decode_workspace_bytes(cfg, batch, max_len). */
+svl_status svl_decode_step(const svl_config *cfg, const svl_layer_weights *layers,
+                           int32_t batch, float *x, const int32_t *cache_len,
+                           const uint8_t *layer_mask, const uint8_t *head_mask,
+                           const uint8_t *ffn_mask, void *kv_cache, int32_t max_len,
+                           void *ws, size_t ws_bytes, void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *svl_last_error(void);
 
@@ -243,10 +295,11 @@ int32_t svl_abi_version(void);
  * returns the summed kernel time (ms) and launch count of one kernel class,
  * then forgets them.  Timing adds event records between launches, so time
  * whole calls with timing off.
- * Kernel classes: 0 select, 1 gather, 2 rmsnorm, 3 qkv gemm, 4 attention,
- * 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope table, 9 split-K finish
- * (QKV and gate/up launches whose K was split). */
-#define SVL_KCLASS_COUNT 10
+ * Kernel classes: 0 select, 1 gather, 2 rmsnorm, 3 qkv gemm, 4 attention
+ * (prefill and decode), 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope
+ * table, 9 split-K finish (QKV and gate/up launches whose K was split),
+ * 10 KV-cache append. */
+#define SVL_KCLASS_COUNT 11
 svl_status svl_timing_enable(int32_t on);
 svl_status svl_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);
 

@@ -8,5 +8,6 @@ from .binding import (  # noqa: F401
     KCLASS, SVL_BF16, SVL_COMPUTE_BF16, SVL_COMPUTE_F16, SVL_F32, LayerTable, SvlError, alloc_workspace, layer_weights,
     load_library, make_config, svl_abi_version, svl_budget_project, svl_count_flops,
     svl_count_positive, svl_layer_forward, svl_prefill, svl_select_tokens, svl_timing_enable,
-    svl_timing_read, svl_workspace_bytes,
+    svl_timing_read, svl_workspace_bytes, alloc_kv_cache, alloc_decode_workspace,
+    svl_kv_cache_bytes, svl_prefill_cache, svl_decode_step,
 )

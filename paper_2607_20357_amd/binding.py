@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libsvl.so")
 SVL_F32, SVL_BF16 = 0, 1
 SVL_COMPUTE_F16, SVL_COMPUTE_BF16 = 0, 1
 KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
-          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9}
+          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9, "kv_append": 10}
 STATUS = {0: "SVL_OK", 1: "SVL_E_NULL", 2: "SVL_E_SHAPE", 3: "SVL_E_VALUE", 4: "SVL_E_WORKSPACE",
           5: "SVL_E_DTYPE", 6: "SVL_E_HIP", 7: "SVL_E_ALIGN"}
 WEIGHT_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
@@ -81,6 +81,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                 P, P, P, P, P, P, P, P, ctypes.POINTER(i32),
                                 ctypes.POINTER(svl_flops), P, sz, P]
     lib.svl_count_positive.argtypes = [i32, i32, P, P, P, sz, P]
+    lib.svl_prefill_cache.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), ctypes.POINTER(svl_batch),
+                                      P, P, P, P, P, P, P, P, ctypes.POINTER(i32), P, i32, P, sz, P]
+    lib.svl_decode_step.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), i32, P, P, P, P, P, P,
+                                    i32, P, sz, P]
+    lib.svl_kv_cache_bytes.argtypes = [cfgp, i32, i32]
+    lib.svl_kv_cache_bytes.restype = sz
+    lib.svl_decode_workspace_bytes.argtypes = [cfgp, i32, i32]
+    lib.svl_decode_workspace_bytes.restype = sz
     lib.svl_budget_project.argtypes = [cfgp, i32, i32, i32, P, ctypes.c_float, ctypes.c_int64,
                                        i32, P, P, P, P, P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
@@ -93,7 +101,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.svl_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_int64)]
     for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
-              "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project"):
+              "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
+              "svl_prefill_cache", "svl_decode_step"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -275,6 +284,61 @@ def svl_prefill(cfg: svl_config, layers, keep, scores: torch.Tensor, vision: tor
         _dev(resid, "resid"), cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
         ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
     return cu, (fl.as_dict() if want_flops else None)
+
+
+def svl_kv_cache_bytes(cfg: svl_config, batch: int, max_len: int) -> int:
+    return int(load_library().svl_kv_cache_bytes(ctypes.byref(cfg), int(batch), int(max_len)))
+
+
+def alloc_kv_cache(cfg: svl_config, batch: int, max_len: int, device="cuda") -> torch.Tensor:
+    """Caller-owned KV cache (torch provides the device memory)."""
+    n = svl_kv_cache_bytes(cfg, batch, max_len)
+    if n == 0:
+        raise SvlError(2, "bad KV cache shape")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def alloc_decode_workspace(cfg: svl_config, batch: int, max_len: int, device="cuda") -> torch.Tensor:
+    n = int(load_library().svl_decode_workspace_bytes(ctypes.byref(cfg), int(batch), int(max_len)))
+    if n == 0:
+        raise SvlError(2, "bad decode workspace shape")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def svl_prefill_cache(cfg: svl_config, layers, keep, scores: torch.Tensor, vision: torch.Tensor,
+                      text: torch.Tensor, layer_mask, head_mask, ffn_mask, kept_idx: torch.Tensor,
+                      resid: torch.Tensor, kv_cache: torch.Tensor, max_len: int, ws: torch.Tensor,
+                      stream=None) -> np.ndarray:
+    """The prefill that also fills the KV cache; returns cu_seqlens."""
+    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
+    kp, kpp = _host_i32(keep)
+    B, N = scores.shape
+    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
+    lm, lmp = _host_u8(layer_mask, "layer_mask")
+    hm, hmp = _host_u8(head_mask, "head_mask")
+    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    cu = np.zeros(B + 1, dtype=np.int32)
+    _check(load_library().svl_prefill_cache(
+        ctypes.byref(cfg), table.array, ctypes.byref(batch), _dev(scores, "scores"),
+        _dev(vision, "vision"), _dev(text, "text"), lmp, hmp, fmp, _dev(kept_idx, "kept_idx"),
+        _dev(resid, "resid"), cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+        _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), ws.numel(), _stream(stream)))
+    return cu
+
+
+def svl_decode_step(cfg: svl_config, layers, x: torch.Tensor, cache_len, layer_mask, head_mask,
+                    ffn_mask, kv_cache: torch.Tensor, max_len: int, ws: torch.Tensor,
+                    stream=None) -> None:
+    """One decode step, x [B][D] float32 updated in place; the caller advances cache_len."""
+    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
+    cl, clp = _host_i32(cache_len)
+    lm, lmp = _host_u8(layer_mask, "layer_mask")
+    hm, hmp = _host_u8(head_mask, "head_mask")
+    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    _check(load_library().svl_decode_step(
+        ctypes.byref(cfg), table.array, int(x.shape[0]), _dev(x, "x"),
+        clp, lmp, hmp, fmp, _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), ws.numel(),
+        _stream(stream)))
 
 
 def svl_timing_enable(on: bool) -> None:

@@ -72,7 +72,8 @@ hipError_t timed(int cls, hipStream_t st, F&& f) {
   return r;
 }
 
-enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_FINISH };
+enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_FINISH,
+              K_KV_APPEND };
 
 // ------------------------------------------------------------------ validation
 svl_status check_config(const svl_config* c, bool for_kernels = true) {
@@ -123,7 +124,8 @@ struct WsLayout {
 
 // Activation buffers use the padded row space (16-row blocks per sample on
 // the 16-bit MFMA path); the partial region holds the float32 split-K slices.
-WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
+// pos_rows: RoPE table rows (positions) when they exceed R (decode: max_len).
+WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows = 0) {
   const int64_t es = c.dtype == SVL_BF16 ? 2 : 4;
   const int64_t prow = std::max<int64_t>(padded_rows_bound(c, B, R), 16);
   WsLayout L{};
@@ -134,7 +136,7 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R) {
     return o;
   };
   L.plan = take(plan_bytes_bound(c, B, R, c.n_layers));
-  L.rope = take(std::max<int64_t>(R, 1) * (c.head_dim / 2) * 8);
+  L.rope = take(std::max<int64_t>(std::max(R, pos_rows), 1) * (c.head_dim / 2) * 8);
   L.partial = take(partial_floats_bound(c, B, R) * 4);
   L.partial_slice = (int64_t)R * c.d_model;
   L.prows = prow;
@@ -154,6 +156,11 @@ struct Exec {
   WsLayout L;
   const Plan& plan;
   float* resid;
+  // KV cache (decode stage): [layers][batch][KV][2][max_len][d]; nullptr: none
+  uint8_t* cache = nullptr;
+  int32_t max_len = 0;
+  int32_t batch = 0;
+  bool decode = false;   // one new row per sample: attention over the cache
 
   template <class T>
   const T* at(int64_t off) const { return reinterpret_cast<const T*>(ws + L.plan + off); }
@@ -253,7 +260,7 @@ struct Exec {
   // pieces into the partial slices the next residual-finish launch adds.
   static int resid_epi(const GemmLaunch& g) { return g.nsplit > 1 ? EPI_PARTIAL : EPI_RESID; }
 
-  hipError_t layer(const LayerPlan& P, const svl_layer_weights& w) const {
+  hipError_t layer(const LayerPlan& P, const svl_layer_weights& w, int32_t l = 0) const {
     const int A = c.n_heads, KV = c.n_kv_heads, d = c.head_dim, D = c.d_model, F = c.d_ffn;
     const int qkv_w = (A + 2 * KV) * d;
     const bool mfma = c.dtype == SVL_BF16;
@@ -283,7 +290,17 @@ struct Exec {
       a.ldo = A * d;
       a.rope = reinterpret_cast<const float2*>(ws + L.rope);
       a.scale = 1.0f / std::sqrt((float)d);
+      if (cache) {
+        // this call's K / V rows into the cache, before the attention reads it
+        a.cache = cache + (size_t)l * batch * KV * 2 * (size_t)max_len * d * 2;
+        a.max_len = max_len;
+        a.kvhead_table = at<int32_t>(P.attn.kvheads_off);
+        a.max_kv_cnt = P.attn.max_kv_cnt;
+        e = timed(K_KV_APPEND, st, [&] { return launch_kv_append(a, d, st); });
+        if (e != hipSuccess) return e;
+      }
       e = timed(K_ATTN, st, [&] {
+        if (decode) return launch_attn_decode(a, d, c.compute == SVL_COMPUTE_F16, st);
         return mfma ? launch_attn_mfma(a, d, c.compute == SVL_COMPUTE_F16, st)
                     : launch_attn_f32(a, d, st);
       });
@@ -390,7 +407,7 @@ svl_status stage(const Exec& ex, bool need_layers) {
   if (e != hipSuccess) return hip_fail(e, "plan upload");
   if (need_layers) {
     e = timed(K_ROPE, ex.st, [&] {
-      return launch_rope_table(reinterpret_cast<float2*>(ex.ws + ex.L.rope), ex.plan.max_seq,
+      return launch_rope_table(reinterpret_cast<float2*>(ex.ws + ex.L.rope), ex.plan.max_pos,
                                ex.c.head_dim, ex.c.rope_theta, ex.st);
     });
     if (e != hipSuccess) return hip_fail(e, "rope table");
@@ -572,21 +589,27 @@ svl_status svl_layer_forward(const svl_config* cfg, int32_t layer, const svl_lay
   return SVL_OK;
 }
 
-svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, const svl_batch* batch,
-                       const float* scores, const void* vision, const void* text,
-                       const uint8_t* layer_mask, const uint8_t* head_mask, const uint8_t* ffn_mask,
-                       int32_t* kept_idx, float* resid, int32_t* cu_seqlens, svl_flops* flops,
-                       void* ws, size_t ws_bytes, void* stream) {
-  svl_status s = check_config(cfg);
-  if (s != SVL_OK) return s;
-  if ((s = check_batch(*cfg, batch)) != SVL_OK) return s;
-  if (!layers || !layer_mask || !head_mask || !cu_seqlens) return fail(SVL_E_NULL, "NULL argument");
-  const int32_t B = batch->batch, L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
-  std::vector<int32_t> seq(B);
-  int32_t R = 0;
-  for (int32_t b = 0; b < B; ++b) { seq[b] = batch->keep[b] + batch->n_text; R += seq[b]; }
-  if ((s = check_data(*batch, R, scores, vision, text, kept_idx, resid)) != SVL_OK) return s;
+// Host masks [B][L][...] -> per-layer LayerMasks (lon: the transposed layer mask).
+static void layer_masks(const svl_config& c, int32_t B, const uint8_t* layer_mask,
+                        const uint8_t* head_mask, const uint8_t* ffn_mask,
+                        std::vector<LayerMasks>& masks, std::vector<uint8_t>& lon) {
+  const int32_t L = c.n_layers, A = c.n_heads, G = c.n_groups;
+  masks.assign(L, LayerMasks{});
+  lon.assign((size_t)L * B, 0);
   for (int32_t l = 0; l < L; ++l) {
+    // row b of layer l starts at (b*L + l) * width
+    masks[l].head_mask = head_mask + (int64_t)l * A;
+    masks[l].head_stride = (int64_t)L * A;
+    masks[l].ffn_mask = ffn_mask ? ffn_mask + (int64_t)l * G : nullptr;
+    masks[l].ffn_stride = (int64_t)L * G;
+    for (int32_t b = 0; b < B; ++b) lon[(size_t)l * B + b] = layer_mask[(int64_t)b * L + l];
+    masks[l].layer_on = lon.data() + (size_t)l * B;
+  }
+}
+
+static svl_status check_layers(const svl_config& c, const svl_layer_weights* layers) {
+  if (!layers) return fail(SVL_E_NULL, "layers is NULL");
+  for (int32_t l = 0; l < c.n_layers; ++l) {
     const svl_layer_weights& w = layers[l];
     const void* wp[9] = {w.attn_norm, w.wq, w.wk, w.wv, w.wo, w.ffn_norm, w.w_gate, w.w_up, w.w_down};
     for (const void* p : wp) {
@@ -594,24 +617,41 @@ svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, c
       if (!aligned16(p)) return fail(SVL_E_ALIGN, "weight pointer of layer %d not 16-byte aligned", l);
     }
   }
+  return SVL_OK;
+}
+
+// The prefill, optionally writing every layer's K / V rows into a cache.
+static svl_status prefill_impl(const svl_config* cfg, const svl_layer_weights* layers,
+                               const svl_batch* batch, const float* scores, const void* vision,
+                               const void* text, const uint8_t* layer_mask,
+                               const uint8_t* head_mask, const uint8_t* ffn_mask,
+                               int32_t* kept_idx, float* resid, int32_t* cu_seqlens,
+                               svl_flops* flops, void* ws, size_t ws_bytes, void* stream,
+                               void* cache, int32_t max_len) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  if ((s = check_batch(*cfg, batch)) != SVL_OK) return s;
+  if (!layer_mask || !head_mask || !cu_seqlens) return fail(SVL_E_NULL, "NULL argument");
+  const int32_t B = batch->batch, L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
+  std::vector<int32_t> seq(B);
+  int32_t R = 0;
+  for (int32_t b = 0; b < B; ++b) { seq[b] = batch->keep[b] + batch->n_text; R += seq[b]; }
+  if ((s = check_data(*batch, R, scores, vision, text, kept_idx, resid)) != SVL_OK) return s;
+  if ((s = check_layers(*cfg, layers)) != SVL_OK) return s;
   if ((s = check_mask(layer_mask, (int64_t)B * L, "layer_mask")) != SVL_OK) return s;
   if ((s = check_mask(head_mask, (int64_t)B * L * A, "head_mask")) != SVL_OK) return s;
   if (ffn_mask && (s = check_mask(ffn_mask, (int64_t)B * L * G, "ffn_mask")) != SVL_OK) return s;
+  if (cache) {
+    if (cfg->dtype != SVL_BF16) return fail(SVL_E_DTYPE, "the KV cache is on the 16-bit path only");
+    if (!aligned16(cache)) return fail(SVL_E_ALIGN, "kv_cache not 16-byte aligned");
+    if (max_len <= 0 || max_len > 32768) return fail(SVL_E_SHAPE, "max_len outside [1, 32768]");
+    for (int32_t b = 0; b < B; ++b)
+      if (seq[b] > max_len) return fail(SVL_E_SHAPE, "sample %d has %d rows > max_len %d", b, seq[b], max_len);
+  }
   if ((s = check_ws(*cfg, B, R, ws, ws_bytes)) != SVL_OK) return s;
-  std::vector<LayerMasks> masks(L);
-  for (int32_t l = 0; l < L; ++l) {
-    // host masks are [B][L][...]: row b of layer l starts at (b*L + l) * width
-    masks[l].layer_on = nullptr;
-    masks[l].head_mask = head_mask + (int64_t)l * A;
-    masks[l].head_stride = (int64_t)L * A;
-    masks[l].ffn_mask = ffn_mask ? ffn_mask + (int64_t)l * G : nullptr;
-    masks[l].ffn_stride = (int64_t)L * G;
-  }
-  std::vector<uint8_t> lon((size_t)L * B);
-  for (int32_t l = 0; l < L; ++l) {
-    for (int32_t b = 0; b < B; ++b) lon[(size_t)l * B + b] = layer_mask[(int64_t)b * L + l];
-    masks[l].layer_on = lon.data() + (size_t)l * B;
-  }
+  std::vector<LayerMasks> masks;
+  std::vector<uint8_t> lon;
+  layer_masks(*cfg, B, layer_mask, head_mask, ffn_mask, masks, lon);
   std::string err;
   if (!build_plan(*cfg, B, batch->keep, seq.data(), L, masks.data(), &t_plan, &err))
     return fail(SVL_E_VALUE, "%s", err.c_str());
@@ -622,10 +662,90 @@ svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, c
     if (fs != SVL_OK) return fs;
   }
   Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), ws_layout(*cfg, B, R), t_plan, resid};
+  ex.cache = static_cast<uint8_t*>(cache);
+  ex.max_len = max_len;
+  ex.batch = B;
   if ((s = stage(ex, true)) != SVL_OK) return s;
   if ((s = select_and_gather(ex, *batch, scores, vision, text, kept_idx, R)) != SVL_OK) return s;
   for (int32_t l = 0; l < L; ++l) {
-    hipError_t e = ex.layer(t_plan.layers[l], layers[l]);
+    hipError_t e = ex.layer(t_plan.layers[l], layers[l], l);
+    if (e != hipSuccess) return hip_fail(e, "layer launch");
+  }
+  hipError_t e = ex.norm(t_plan.final_norm, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "final residual launch");
+  return SVL_OK;
+}
+
+svl_status svl_prefill(const svl_config* cfg, const svl_layer_weights* layers, const svl_batch* batch,
+                       const float* scores, const void* vision, const void* text,
+                       const uint8_t* layer_mask, const uint8_t* head_mask, const uint8_t* ffn_mask,
+                       int32_t* kept_idx, float* resid, int32_t* cu_seqlens, svl_flops* flops,
+                       void* ws, size_t ws_bytes, void* stream) {
+  return prefill_impl(cfg, layers, batch, scores, vision, text, layer_mask, head_mask, ffn_mask,
+                      kept_idx, resid, cu_seqlens, flops, ws, ws_bytes, stream, nullptr, 0);
+}
+
+svl_status svl_prefill_cache(const svl_config* cfg, const svl_layer_weights* layers,
+                             const svl_batch* batch, const float* scores, const void* vision,
+                             const void* text, const uint8_t* layer_mask,
+                             const uint8_t* head_mask, const uint8_t* ffn_mask,
+                             int32_t* kept_idx, float* resid, int32_t* cu_seqlens,
+                             void* kv_cache, int32_t max_len, void* ws, size_t ws_bytes,
+                             void* stream) {
+  if (!kv_cache) return fail(SVL_E_NULL, "kv_cache is NULL");
+  return prefill_impl(cfg, layers, batch, scores, vision, text, layer_mask, head_mask, ffn_mask,
+                      kept_idx, resid, cu_seqlens, nullptr, ws, ws_bytes, stream, kv_cache, max_len);
+}
+
+size_t svl_kv_cache_bytes(const svl_config* cfg, int32_t batch, int32_t max_len) {
+  if (check_config(cfg) != SVL_OK || batch <= 0 || max_len <= 0 || max_len > 32768) return 0;
+  return (size_t)cfg->n_layers * batch * cfg->n_kv_heads * 2 * (size_t)max_len * cfg->head_dim * 2;
+}
+
+size_t svl_decode_workspace_bytes(const svl_config* cfg, int32_t batch, int32_t max_len) {
+  if (check_config(cfg) != SVL_OK || batch <= 0 || max_len <= 0 || max_len > 32768) return 0;
+  return (size_t)ws_layout(*cfg, batch, batch, max_len).total;
+}
+
+svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layers, int32_t batch,
+                           float* x, const int32_t* cache_len, const uint8_t* layer_mask,
+                           const uint8_t* head_mask, const uint8_t* ffn_mask, void* kv_cache,
+                           int32_t max_len, void* ws, size_t ws_bytes, void* stream) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  if (cfg->dtype != SVL_BF16) return fail(SVL_E_DTYPE, "decode runs on the 16-bit path only");
+  if (batch <= 0) return fail(SVL_E_SHAPE, "batch must be positive");
+  if (!x || !cache_len || !layer_mask || !head_mask || !kv_cache || !ws)
+    return fail(SVL_E_NULL, "NULL argument");
+  if (!aligned16(x) || !aligned16(kv_cache) || !aligned16(ws))
+    return fail(SVL_E_ALIGN, "device pointers must be 16-byte aligned");
+  if (max_len <= 0 || max_len > 32768) return fail(SVL_E_SHAPE, "max_len outside [1, 32768]");
+  for (int32_t b = 0; b < batch; ++b)
+    if (cache_len[b] < 0 || cache_len[b] >= max_len)
+      return fail(SVL_E_VALUE, "cache_len[%d] = %d outside [0, max_len)", b, cache_len[b]);
+  const int32_t L = cfg->n_layers, A = cfg->n_heads, G = cfg->n_groups;
+  if ((s = check_layers(*cfg, layers)) != SVL_OK) return s;
+  if ((s = check_mask(layer_mask, (int64_t)batch * L, "layer_mask")) != SVL_OK) return s;
+  if ((s = check_mask(head_mask, (int64_t)batch * L * A, "head_mask")) != SVL_OK) return s;
+  if (ffn_mask && (s = check_mask(ffn_mask, (int64_t)batch * L * G, "ffn_mask")) != SVL_OK) return s;
+  const WsLayout WL = ws_layout(*cfg, batch, batch, max_len);
+  if ((int64_t)ws_bytes < WL.total)
+    return fail(SVL_E_WORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)WL.total);
+  std::vector<int32_t> seq(batch, 1);
+  std::vector<LayerMasks> masks;
+  std::vector<uint8_t> lon;
+  layer_masks(*cfg, batch, layer_mask, head_mask, ffn_mask, masks, lon);
+  std::string err;
+  if (!build_plan(*cfg, batch, nullptr, seq.data(), L, masks.data(), &t_plan, &err, cache_len))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  Exec ex{*cfg, (hipStream_t)stream, static_cast<uint8_t*>(ws), WL, t_plan, x};
+  ex.cache = static_cast<uint8_t*>(kv_cache);
+  ex.max_len = max_len;
+  ex.batch = batch;
+  ex.decode = true;
+  if ((s = stage(ex, true)) != SVL_OK) return s;
+  for (int32_t l = 0; l < L; ++l) {
+    hipError_t e = ex.layer(t_plan.layers[l], layers[l], l);
     if (e != hipSuccess) return hip_fail(e, "layer launch");
   }
   hipError_t e = ex.norm(t_plan.final_norm, nullptr);

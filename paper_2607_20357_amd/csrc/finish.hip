@@ -53,7 +53,7 @@ __global__ __launch_bounds__(NT) void qkv_finish_kernel(FinishArgs a) {
   }
   float o1[4] = {x1.x, x1.y, x1.z, x1.w}, o2[4] = {x2.x, x2.y, x2.z, x2.w};
   if (g.rope) {
-    const float2* cs = a.rope + (size_t)row * half + dim;   // row = position in the sample
+    const float2* cs = a.rope + (size_t)(g.pos_base + row) * half + dim;   // position of the row
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float2 c = cs[i];

@@ -105,9 +105,10 @@ struct MmBuild {
   int32_t max_rows = 0, min_chunks = 1 << 30;
   void add(int32_t arow0, int32_t orow0, int32_t nrows, int32_t wsel, int32_t wrow0,
            int32_t ocol0, int32_t nblocks, int32_t kc_off, int32_t kc_cnt, int32_t rope,
-           const std::vector<KChunk>& chunks) {
+           const std::vector<KChunk>& chunks, int32_t pos_base = 0) {
     if (nrows <= 0 || nblocks <= 0 || kc_cnt <= 0) return;
     MmGroup g{};
+    g.pos_base = pos_base;
     g.arow0 = arow0; g.orow0 = orow0; g.nrows = nrows; g.wsel = wsel; g.wrow0 = wrow0;
     g.ocol0 = ocol0; g.kc_off = kc_off; g.kc_cnt = kc_cnt; g.rope = rope; g.nblocks = nblocks;
     // contiguous full chunks: the kernel computes the offsets
@@ -155,7 +156,7 @@ struct MmBuild {
         for (int32_t mt = 0; mt < nm; ++mt) {
           const int32_t m0 = mt * MFMA_BM;
           t.arow = g.arow0 + m0; t.orow = g.orow0 + m0;
-          t.mcnt = std::min(MFMA_BM, g.nrows - m0); t.pos0 = m0;
+          t.mcnt = std::min(MFMA_BM, g.nrows - m0); t.pos0 = g.pos_base + m0;
           for (int32_t p = 0; p < nsplit; ++p) {
             t.chunk0 = g.kc_off + kc[p];
             t.kcn = kc[p + 1] - kc[p];
@@ -292,6 +293,7 @@ int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t R, int32_t nlay
   per_layer += tile_bound(B, D / 16);
   per_layer += B * (int64_t)sizeof(AttnGroup) + 16;
   per_layer += B * A * 4 + 16;
+  per_layer += B * KV * 4 + 16;              // active K/V heads (cache append)
   // chunks: dense D, per sample active head columns and FFN slices
   int64_t chunks = (D + bk - 1) / bk + B * A * ((d + bk - 1) / bk) +
                    B * G * ((F / G + bk - 1) / bk);
@@ -301,7 +303,8 @@ int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t R, int32_t nlay
 }
 
 bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int32_t* seqlens,
-                int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err) {
+                int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err,
+                const int32_t* pos_base) {
   const bool mfma = cfg.dtype == SVL_BF16;
   const int32_t A = cfg.n_heads, KV = cfg.n_kv_heads, G = cfg.n_groups, d = cfg.head_dim;
   const int32_t D = cfg.d_model, F = cfg.d_ffn, rep = A / KV, slice = F / G;
@@ -312,6 +315,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
   plan->layers.assign(nlayers, LayerPlan{});
   plan->final_norm = NormLaunch{};
   plan->max_seq = 0;
+  plan->max_pos = 0;
   ImageWriter w{&plan->image};
 
   std::vector<int32_t> cu(B + 1, 0), pcu(B + 1, 0);
@@ -320,6 +324,9 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     cu[b + 1] = cu[b] + seqlens[b];
     pcu[b + 1] = pcu[b] + (mfma ? (seqlens[b] + 15) / 16 * 16 : seqlens[b]);
     plan->max_seq = std::max(plan->max_seq, seqlens[b]);
+    const int32_t pb = pos_base ? pos_base[b] : 0;
+    if (pb < 0) { *err = "negative cached length"; return false; }
+    plan->max_pos = std::max(plan->max_pos, pb + seqlens[b]);
   }
   const int32_t R = cu[B];
   plan->padded_rows = pcu[B];
@@ -388,8 +395,8 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     GemmBuild qkv, o, gu, down;       // float32 path
     MmBuild mqkv, mo, mgu, mdown;     // 16-bit MFMA path
     std::vector<AttnGroup> ag;
-    std::vector<int32_t> heads;
-    int32_t attn_tiles = 0;
+    std::vector<int32_t> heads, kvheads;
+    int32_t attn_tiles = 0, max_kv_cnt = 0;
     for (int32_t b = 0; b < B; ++b) {
       run_attn[b] = run_ffn[b] = 0;
       const int32_t S = seqlens[b];
@@ -414,7 +421,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
           for (auto r : runs(sc.on, sc.n, d, 0)) {
             if (mfma)
               mqkv.add(pcu[b], pcu[b], S, sc.wsel, r.a, sc.col0 + r.a, (r.b - r.a) / 16, 0,
-                       dense_cnt, sc.wsel < 2 ? 1 : 0, chunks);
+                       dense_cnt, sc.wsel < 2 ? 1 : 0, chunks, pos_base ? pos_base[b] : 0);
             else
               qkv.add(pcu[b], pcu[b], S, sc.col0 + r.a, sc.col0 + r.b, 0, dense_cnt);
           }
@@ -429,7 +436,12 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
         AttnGroup g{};
         g.row0 = pcu[b]; g.S = S; g.h_off = (int32_t)heads.size(); g.h_cnt = nh;
         g.nqt = cdiv(S, ATTN_BQ); g.tile0 = attn_tiles;
+        g.sample = b; g.pos_base = pos_base ? pos_base[b] : 0;
+        g.kv_off = (int32_t)kvheads.size();
         for (int32_t h = 0; h < A; ++h) if (hm[h]) heads.push_back(h);
+        for (int32_t k = 0; k < KV; ++k) if (kv_on[k]) kvheads.push_back(k);
+        g.kv_cnt = (int32_t)kvheads.size() - g.kv_off;
+        max_kv_cnt = std::max(max_kv_cnt, g.kv_cnt);
         attn_tiles += g.nqt * nh;
         ag.push_back(g);
       }
@@ -468,8 +480,10 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     }
     LP.attn.groups_off = w.append(ag);
     LP.attn.heads_off = w.append(heads);
+    LP.attn.kvheads_off = w.append(kvheads);
     LP.attn.ngroups = (int32_t)ag.size();
     LP.attn.ntiles = attn_tiles;
+    LP.attn.max_kv_cnt = max_kv_cnt;
 
     // FFN sub-block
     LP.norm_ffn = norm_launch(run_ffn);

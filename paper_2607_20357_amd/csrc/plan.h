@@ -25,8 +25,9 @@ struct GemmLaunch {
 };
 
 struct AttnLaunch {
-  int64_t groups_off = 0, heads_off = 0;
+  int64_t groups_off = 0, heads_off = 0, kvheads_off = 0;
   int32_t ngroups = 0, ntiles = 0;
+  int32_t max_kv_cnt = 0;   // most active K/V heads of a group (cache append grid)
 };
 
 // A residual / RMSNorm launch: adds pending split-K partials (nsplit slices)
@@ -56,7 +57,8 @@ struct Plan {
   std::vector<LayerPlan> layers;
   NormLaunch final_norm;          // adds the last layer's pending partials
   int64_t keep_off = 0, cu_off = 0;
-  int32_t max_seq = 0;            // longest sequence (RoPE table rows)
+  int32_t max_seq = 0;            // most rows of one sample in this call
+  int32_t max_pos = 0;            // positions the RoPE table covers: max of pos_base + rows
   int32_t padded_rows = 0;        // rows of the activation buffers
 };
 
@@ -81,8 +83,11 @@ constexpr int32_t kNormRows8 = 2048;
 
 // Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks[l]
 // gives layer l's masks.  Returns false with a message on inconsistency.
+// pos_base (host [B] or nullptr = all 0): positions already cached per sample
+// (decode); the rows of sample b are positions pos_base[b] .. + seqlens[b]-1.
 bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int32_t* seqlens,
-                int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err);
+                int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err,
+                const int32_t* pos_base = nullptr);
 
 // Upper bound of the plan image for any masks (B samples, R packed rows).
 int64_t plan_bytes_bound(const svl_config& cfg, int32_t B, int32_t R, int32_t nlayers);

@@ -70,6 +70,8 @@ struct MmGroup {
   int32_t nblocks;      // 16-column blocks
   int32_t fitem0;       // split paired launches: first finish work item of the group
   int32_t kdense;       // >= 0: the group's chunk c starts at column kdense + 64 c
+  int32_t pos_base;     // QKV: RoPE position of the group's first row
+  int32_t pad0, pad1, pad2;
 };
 
 // One workgroup of a 16-bit MFMA GEMM launch: rows [m0, m0 + 256) of its
@@ -95,11 +97,16 @@ struct MmTile {
 static_assert(sizeof(MmTile) == 64, "one 64-byte record per workgroup");
 
 // One sample of an attention launch: one workgroup per (active head, q tile).
+// With a KV cache, the sample's rows are positions pos_base .. pos_base+S-1
+// of its cached sequence (prefill: pos_base = 0; decode: S = 1 new row).
 struct AttnGroup {
-  int32_t row0, S;      // first activation row of the sample, sequence length
+  int32_t row0, S;      // first activation row of the sample, rows in this call
   int32_t h_off, h_cnt; // active query heads: head_table[h_off .. h_off+h_cnt)
   int32_t nqt;          // query tiles
   int32_t tile0;        // first workgroup index of the group
+  int32_t sample;       // batch index (cache addressing)
+  int32_t pos_base;     // cached positions before this call's rows
+  int32_t kv_off, kv_cnt;   // active K/V heads: kvhead_table[kv_off .. kv_off+kv_cnt)
   int32_t pad0, pad1;
 };
 

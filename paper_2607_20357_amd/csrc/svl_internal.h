@@ -88,6 +88,12 @@ struct AttnArgs {
   int32_t ldo;
   const float2* rope;  // (cos, sin)[pos][d/2]; used by kernels that rotate on load
   float scale;         // 1/sqrt(d)
+  // KV cache of this layer (decode attention reads it, the append writes it):
+  // [batch][n_kv_heads][2][max_len][d], activation type
+  void* cache;
+  int32_t max_len;
+  const int32_t* kvhead_table;
+  int32_t max_kv_cnt;
 };
 
 constexpr int NORM_INLINE_SEGS = 8;
@@ -125,6 +131,9 @@ hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, 
 hipError_t launch_finish(const FinishArgs& a, int32_t epi, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
+// KV cache: append this call's K / V rows; decode attention over the cache.
+hipError_t launch_kv_append(const AttnArgs& a, int32_t head_dim, hipStream_t st);
+hipError_t launch_attn_decode(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);
 hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, float theta,
                              hipStream_t st);
