@@ -56,6 +56,10 @@ def parse():
                         "and the budget projection to B * C_full inside each step, on the "
                         "headline shapes and masks with logits N(0,1) - 0.674 (a quarter of "
                         "the tokens positive)")
+    p.add_argument("--decode", type=int, default=None, metavar="N",
+                   help="instead of the prefill step: N timed decode steps on the pruned and "
+                        "gated KV cache the workload's prefill leaves (one new token per sample "
+                        "per step)")
     p.add_argument("--memory-sweep", action="store_true",
                    help="instead of the step benchmark: HBM rate of the memory-bound kernels "
                         "(select, gather, residual norm) on the headline per-row structure "
@@ -281,6 +285,126 @@ def memory_sweep(args):
         torch.cuda.empty_cache()
 
 
+def decode_bench(args):
+    """Decode on the pruned and gated KV cache: the workload's prefill fills
+    the cache (untimed), then each step feeds one new token per sample (seeded
+    hidden states, bf16-rounded) through every layer under the sample's masks.
+    The step's HBM bytes are the active weights it streams (the GEMM classes
+    at one row per sample) plus the cached K / V it reads."""
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    w = W.get_workload(args.workload or W.HEADLINE)
+    shape = w.shape
+    print(f"# decode after workload {w.name}: {w.description}", file=sys.stderr, flush=True)
+    inp = W.draw_inputs(w, args.seed, device=dev)
+    layers = [W.draw_layer_weights(w, l, args.seed, device=dev) for l in range(shape.n_layers)]
+    table = svl.LayerTable(layers)
+    cfg = svl.make_config(shape)
+    B, N = inp.scores.shape
+    D, KV, d = shape.d_model, shape.n_kv_heads, shape.head_dim
+    seq = (np.asarray(inp.keep) + w.n_text).astype(np.int32)
+    R = int(seq.sum())
+    K, Wm = args.decode, args.warmup
+    total = Wm + 2 * K
+    max_len = int(seq.max()) + total + 1
+    cache = svl.alloc_kv_cache(cfg, B, max_len, dev)
+    ws = svl.alloc_workspace(cfg, B, R, dev)
+    scores = torch.from_numpy(inp.scores).to(dev)
+    kept = torch.empty((B, N), dtype=torch.int32, device=dev)
+    resid = torch.empty((R, D), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    svl.svl_prefill_cache(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
+                          inp.head_mask, inp.ffn_mask, kept, resid, cache, max_len, ws,
+                          stream=stream)
+    dws = svl.alloc_decode_workspace(cfg, B, max_len, dev)
+    g = torch.Generator(device=dev).manual_seed(args.seed + 100)
+    xs = torch.randn(total, B, D, generator=g, device=dev).to(torch.bfloat16).to(torch.float32)
+    x = torch.empty((B, D), dtype=torch.float32, device=dev)
+    cache_len = seq.copy()
+    lens_timed = []
+
+    def step(i):
+        x.copy_(xs[i])
+        svl.svl_decode_step(cfg, table, x, cache_len, inp.layer_mask, inp.head_mask, inp.ffn_mask,
+                            cache, max_len, dws, stream=stream)
+        cache_len[:] += 1
+
+    for i in range(Wm):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    evs[0].record(stream)
+    for i in range(K):
+        lens_timed.append(cache_len.copy())
+        step(Wm + i)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = evs[0].elapsed_time(evs[-1]) / K
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(K)])
+    svl.svl_timing_enable(True)
+    for i in range(K):
+        step(Wm + K + i)
+    torch.cuda.synchronize()
+    svl.svl_timing_enable(False)
+    ktime = {k: svl.svl_timing_read(k) for k in svl.KCLASS}
+    per_kernel = {k: {"ms_per_step": v[0] / K, "launches_per_step": v[1] / K}
+                  for k, v in ktime.items() if v[1]}
+
+    bytes_, launches = gemm_bytes(shape, np.ones(B, np.int64), inp.layer_mask, inp.head_mask,
+                                  inp.ffn_mask)
+    rep = shape.n_heads // KV
+    kv_bytes = 0.0
+    mean_len = np.mean(np.array(lens_timed), axis=0) + 1          # keys per sample incl. the new one
+    for l in range(shape.n_layers):
+        for b in range(B):
+            if not inp.layer_mask[b, l]:
+                continue
+            hm = inp.head_mask[b, l]
+            kact = sum(int(hm[k * rep:(k + 1) * rep].any()) for k in range(KV))
+            kv_bytes += kact * mean_len[b] * d * 2 * 2
+    step_bytes = sum(bytes_.values()) + kv_bytes
+    gu_ms, gu_n = ktime["gemm_gate_up"]
+    gu_avg_ms = gu_ms / max(1, gu_n)
+    gu_bytes = bytes_["gu"] / max(1, launches["gu"])
+    result = {
+        "metric": "decode tokens/s on the pruned and gated KV cache, 7B-shaped",
+        "value": round(B / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms, 4),
+        "ms_per_step_p10_p50_p90": [round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if shape.dtype == "bf16" else "f32",
+        "storage_dtype": shape.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}_decode", "batch": B, "prefill_rows": [int(v) for v in seq],
+                   "cached_positions_mean": [round(float(v), 1) for v in mean_len],
+                   "layers_executed_per_sample": [int(v) for v in inp.layer_mask.sum(1)],
+                   "parallelism": "none (1 GPU)"},
+        "step_hbm_bytes": int(step_bytes),
+        "step_hbm_gbs": round(step_bytes / (ms * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "per_kernel": per_kernel,
+        "roofline": {
+            "kernel": "gemm_mfma_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU, one row per sample)",
+            "bound": "hbm", "achieved": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": None, "avg_launch_ms": round(gu_avg_ms, 5),
+            "algorithmic_bytes_per_launch": int(gu_bytes),
+        },
+    }
+    print(json.dumps(result))
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -288,6 +412,12 @@ def main():
         return
     if args.memory_sweep:
         memory_sweep(args)
+        return
+    if args.decode is not None:
+        if args.gpus != 1:
+            print(json.dumps({"error": "this build runs on one GPU"}))
+            sys.exit(2)
+        decode_bench(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; multi-GPU runs are not part of "

@@ -291,13 +291,16 @@ struct Exec {
       a.rope = reinterpret_cast<const float2*>(ws + L.rope);
       a.scale = 1.0f / std::sqrt((float)d);
       if (cache) {
-        // this call's K / V rows into the cache, before the attention reads it
         a.cache = cache + (size_t)l * batch * KV * 2 * (size_t)max_len * d * 2;
         a.max_len = max_len;
         a.kvhead_table = at<int32_t>(P.attn.kvheads_off);
         a.max_kv_cnt = P.attn.max_kv_cnt;
-        e = timed(K_KV_APPEND, st, [&] { return launch_kv_append(a, d, st); });
-        if (e != hipSuccess) return e;
+        // prefill: this call's K / V rows into the cache (decode attention
+        // appends its one row itself)
+        if (!decode) {
+          e = timed(K_KV_APPEND, st, [&] { return launch_kv_append(a, d, st); });
+          if (e != hipSuccess) return e;
+        }
       }
       e = timed(K_ATTN, st, [&] {
         if (decode) return launch_attn_decode(a, d, c.compute == SVL_COMPUTE_F16, st);

@@ -6,9 +6,11 @@
 // row's position).  Only the active K/V heads of samples that run the layer
 // are written and read.
 //
-// Decode attention: one workgroup per (sample, active query head).  The new
-// row's position p = pos_base is already in the cache (the append runs
-// first), so the query attends to positions 0..p, all of them causal.
+// Decode attention: one workgroup per (sample, active query head).  The query
+// at position p = pos_base attends to positions 0..p: 0..p-1 from the cache,
+// p (its own key and value) from the Q/K/V rows of this step, which the
+// workgroup of the first active query head of each K/V head also appends to
+// the cache for the steps after (no separate append launch in decode).
 // Scores are float32 (log2 units, scale folded into q), the softmax is
 // max-subtracted, and the probability-weighted values are summed in float32
 // per 8-dim group over 16 key partitions, then combined in a fixed order.
@@ -75,13 +77,29 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
   const int t = blockIdx.x;
   if (t >= a.ntiles) return;
   const AttnGroup g = a.groups[find_group(a.groups, a.ngroups, t)];
-  const int h = a.head_table[g.h_off + (t - g.tile0)];
-  const int kvh = h / (a.n_heads / a.n_kv_heads);
+  const int hs = t - g.tile0;
+  const int rep = a.n_heads / a.n_kv_heads;
+  const int h = a.head_table[g.h_off + hs];
+  const int kvh = h / rep;
   const int len = g.pos_base + 1;
   const int tid = threadIdx.x;
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
-  const uint16_t* kc = static_cast<const uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 0, 0, D);
-  const uint16_t* vc = static_cast<const uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 1, 0, D);
+  uint16_t* kcw = static_cast<uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 0, 0, D);
+  uint16_t* vcw = static_cast<uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 1, 0, D);
+  const uint16_t* kc = kcw;
+  const uint16_t* vc = vcw;
+  const uint16_t* knew = qkv + (size_t)g.row0 * a.ldq + (a.n_heads + kvh) * D;   // position p
+  const uint16_t* vnew = qkv + (size_t)g.row0 * a.ldq + (a.n_heads + a.n_kv_heads + kvh) * D;
+  // active heads are listed in ascending order, so the heads of one K/V head
+  // are adjacent: the first of them appends position p for later steps
+  if (hs == 0 || a.head_table[g.h_off + hs - 1] / rep != kvh) {
+    if (tid < 2 * (D / 8)) {
+      const int c = tid % (D / 8);
+      const bool v = tid >= D / 8;
+      *reinterpret_cast<uint4*>((v ? vcw : kcw) + (size_t)g.pos_base * D + 8 * c) =
+          *reinterpret_cast<const uint4*>((v ? vnew : knew) + 8 * c);
+    }
+  }
   const float sl2 = a.scale * 1.4426950408889634f;   // scores in log2 units
   if (tid < D) s_q[tid] = act_bits_to_f32<F16>(qkv[(size_t)g.row0 * a.ldq + h * D + tid]) * sl2;
   __syncthreads();
@@ -89,7 +107,7 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
   // scores: thread j takes keys j, j + NT, ...
   float mloc = -3.0e38f;
   for (int j = tid; j < len; j += NT) {
-    const uint4* kr = reinterpret_cast<const uint4*>(kc + (size_t)j * D);
+    const uint4* kr = reinterpret_cast<const uint4*>(j == g.pos_base ? knew : kc + (size_t)j * D);
     float s = 0.f;
 #pragma unroll
     for (int c = 0; c < DG; ++c) {
@@ -118,7 +136,7 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
   for (int j = pt; j < len; j += NP) {
-    const uint4 v = *reinterpret_cast<const uint4*>(vc + (size_t)j * D + 8 * dg);
+    const uint4 v = *reinterpret_cast<const uint4*>((j == g.pos_base ? vnew : vc + (size_t)j * D) + 8 * dg);
     const float p = s_p[j];
     const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
