@@ -36,7 +36,10 @@ Readings (the paper does not fix these; listed in the design notes):
     runs again with the reduced alphas.  A layer whose groups are all dropped
     is skipped (alpha_l = 0).  If dropping every eligible group still leaves
     C(0) > b * C_full, the sample keeps no visual tokens and no eligible group
-    (the budget cannot be met).
+    (the budget cannot be met);
+  * with the layer controller (one gate per layer, units = 1) the unit the
+    reduction drops is a whole layer, in the same order (lowest gate logit
+    first, ties: the later layer).
 
 Every function below cites the passage it follows.
 """
@@ -96,10 +99,13 @@ def _max_tokens(shape, n_text: int, cap: int, alphas, vocab: int, limit: Fractio
 
 def project_sample(shape, logits: np.ndarray, n_text: int, budget: float, vocab: int,
                    prefix: int, layer_on: np.ndarray, head_on: np.ndarray,
-                   ffn_on: Optional[np.ndarray], gate_logits: Optional[np.ndarray]
+                   ffn_on: Optional[np.ndarray], gate_logits: Optional[np.ndarray],
+                   units: Optional[int] = None
                    ) -> Tuple[int, np.ndarray, np.ndarray, Optional[np.ndarray]]:
     """Threshold selection and the budget projection for one sample (Sec. 3.3).
 
+    units: gates per layer, n_groups (layer-head controller, the default) or
+    1 (layer controller: gate_logits [L][1], whole layers are the units).
     Returns (keep count, layer_on, head_on, ffn_on) after the projection; the
     kept tokens are then the `keep` largest logits (select_topk)."""
     N = int(np.asarray(logits).size)
@@ -117,20 +123,25 @@ def project_sample(shape, logits: np.ndarray, n_text: int, budget: float, vocab:
     if s >= 0:
         return s, layer_on, head_on, ffn_on
     # token-level adjustment alone is not enough: drop whole head groups
-    hg = A // G
-    units = []
+    # (layer controller: whole layers)
+    per_layer = G if units is None else units
+    hg = A // per_layer
+    order = []
     for l in range(prefix, L):
         if not layer_on[l]:
             continue
-        for j in range(G):
+        for j in range(per_layer):
             if np.any(head_on[l, j * hg:(j + 1) * hg]):
                 conf = float(gate_logits[l, j]) if gate_logits is not None else 0.0
-                units.append((conf, -l, -j, l, j))
-    units.sort()
-    for _, _, _, l, j in units:
+                order.append((conf, -l, -j, l, j))
+    order.sort()
+    for _, _, _, l, j in order:
         head_on[l, j * hg:(j + 1) * hg] = 0
         if ffn_on is not None:
-            ffn_on[l, j] = 0
+            if per_layer == 1:
+                ffn_on[l, :] = 0
+            else:
+                ffn_on[l, j] = 0
         if not np.any(head_on[l]):
             layer_on[l] = 0
         alphas = layer_alphas(shape, layer_on, head_on)

@@ -57,3 +57,11 @@ def oracle_prefill(w, inp, layers, samples=None):
                           np.asarray(inp.keep)[sel], W.as_f32(inp.vision[sel]),
                           W.as_f32(inp.text[sel]), lm, inp.head_mask[sel],
                           None if inp.ffn_mask is None else inp.ffn_mask[sel])
+
+
+def host_controller(draw):
+    """oracle.controller.Controller with the drawn controller's values (fp32 widened)."""
+    from oracle.controller import Controller
+    t = {k: W.as_f32(v).astype(np.float64) for k, v in draw.tensors.items()}
+    return Controller(prefix=draw.prefix, units=draw.units, pe_scale=float(np.float32(draw.pe_scale)),
+                      pe_base=float(np.float32(draw.pe_base)), **t)

@@ -7,12 +7,13 @@ CPU oracle can take their inputs from it without sharing any computation.
 """
 from .configs import ModelShape, Workload, WORKLOADS, HEADLINE, get_workload, keep_count, scaled
 from .generate import (
-    WEIGHT_NAMES, Inputs, as_f32, draw_hidden, draw_inputs, draw_layer_weights, draw_masks,
-    draw_scores, round_to_bf16, storage_dtype,
+    CONTROLLER_NAMES, WEIGHT_NAMES, ControllerDraw, Inputs, as_f32, draw_controller, draw_hidden,
+    draw_inputs, draw_layer_weights, draw_masks, draw_scores, round_to_bf16, storage_dtype,
 )
 
 __all__ = [
     "ModelShape", "Workload", "WORKLOADS", "HEADLINE", "get_workload", "keep_count", "scaled",
-    "WEIGHT_NAMES", "Inputs", "as_f32", "draw_hidden", "draw_inputs", "draw_layer_weights",
-    "draw_masks", "draw_scores", "round_to_bf16", "storage_dtype",
+    "CONTROLLER_NAMES", "ControllerDraw", "draw_controller", "WEIGHT_NAMES", "Inputs", "as_f32",
+    "draw_hidden", "draw_inputs", "draw_layer_weights", "draw_masks", "draw_scores",
+    "round_to_bf16", "storage_dtype",
 ]

@@ -13,6 +13,13 @@ scores) can be regenerated alone, on the host or on a GPU.
 Laws (recipe stated once for all workloads):
   linear weights  N(0, 0.02^2);  norm gains 1 + N(0, 0.02^2);
   vision / text hidden states N(0, 1);
+  compute controller (budget MLP, token-count MLP, gating head): first
+  linears N(0, 2/E) with E the encoding width, second linears N(0, 1/H) with
+  H the hidden width, their biases N(0, 0.1^2); gating weights
+  N(0, gate_std^2 / D); gating biases c = +-(0.5 + spacing * rank) with rank
+  a random permutation of the units and the sign + with probability p_on,
+  so the bias fixes each unit's on/off decision and every pair of logits
+  stays apart by about `spacing`;
   bf16 workloads round every weight and hidden value to bfloat16
   (round-to-nearest-even) -- the oracle sees the same values widened to fp32;
   scores stay fp32.
@@ -31,6 +38,7 @@ STREAM_SCORES = 1
 STREAM_HIDDEN = 2
 STREAM_MASKS = 3
 STREAM_WEIGHTS = 4
+STREAM_CONTROLLER = 5
 
 WEIGHT_NAMES = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 
@@ -193,3 +201,47 @@ def draw_inputs(w: Workload, seed: int = 0, device="cpu") -> Inputs:
 def as_f32(t: torch.Tensor) -> np.ndarray:
     """Host fp32 copy of a tensor (bf16 widens exactly)."""
     return t.detach().to("cpu", torch.float32).numpy()
+
+
+# --------------------------------------------------------------------------- controller
+CONTROLLER_NAMES = ("llm_w1", "llm_b1", "llm_w2", "llm_b2", "kap_w1", "kap_b1", "kap_w2",
+                    "kap_b2", "gate_w", "gate_b")
+
+
+@dataclass
+class ControllerDraw:
+    prefix: int
+    units: int
+    pe_dim: int
+    hidden: int
+    pe_scale: float
+    pe_base: float
+    tensors: Dict[str, torch.Tensor]     # CONTROLLER_NAMES, storage dtype, [out][in]
+
+
+def draw_controller(w: Workload, seed: int = 0, device="cpu", *, prefix: Optional[int] = None,
+                    units: Optional[int] = None, pe_dim: int = 256, hidden: Optional[int] = None,
+                    pe_scale: float = 1000.0, pe_base: float = 10000.0, p_on: float = 0.75,
+                    spacing: float = 0.1, gate_std: float = 0.002) -> ControllerDraw:
+    """Compute-controller parameters of a workload's decoder (law above)."""
+    s = w.shape
+    P = s.prefix if prefix is None else prefix
+    U = s.n_groups if units is None else units
+    H = s.d_model if hidden is None else hidden
+    D, n = s.d_model, (s.n_layers - P) * U
+    dt = storage_dtype(w)
+    shapes = {"llm_w1": (H, pe_dim), "llm_b1": (H,), "llm_w2": (D, H), "llm_b2": (D,),
+              "kap_w1": (H, pe_dim), "kap_b1": (H,), "kap_w2": (D, H), "kap_b2": (D,),
+              "gate_w": (n, D)}
+    stds = {"llm_w1": (2.0 / pe_dim) ** 0.5, "kap_w1": (2.0 / pe_dim) ** 0.5,
+            "llm_w2": (1.0 / H) ** 0.5, "kap_w2": (1.0 / H) ** 0.5, "gate_w": gate_std / D ** 0.5}
+    out = {}
+    for i, name in enumerate(CONTROLLER_NAMES[:-1]):
+        sd = _seed(seed, STREAM_CONTROLLER, i)
+        out[name] = _randn(shapes[name], sd, device, std=stds.get(name, 0.1)).to(dt).contiguous()
+    rng = _np_rng(seed, STREAM_CONTROLLER, 99)
+    mag = 0.5 + spacing * rng.permutation(n)
+    sign = np.where(rng.random(n) < p_on, 1.0, -1.0)
+    gb = torch.from_numpy((sign * mag).astype(np.float32))
+    out["gate_b"] = gb.to(device=device, dtype=dt).contiguous()
+    return ControllerDraw(P, U, pe_dim, H, pe_scale, pe_base, out)
