@@ -56,6 +56,12 @@ def parse():
                         "and the budget projection to B * C_full inside each step, on the "
                         "headline shapes and masks with logits N(0,1) - 0.674 (a quarter of "
                         "the tokens positive)")
+    p.add_argument("--controller", type=float, default=None, metavar="B",
+                   help="instead of the given keep budget and masks: the controlled prefill "
+                        "(threshold selection on logits N(0,1) - 0.674, the budget token, "
+                        "P = L/2 prefix layers, the compute controller's masks, the budget "
+                        "projection to B * C_full at the prefix boundary) with seeded "
+                        "controller weights (encoding width 256, hidden width d_model)")
     p.add_argument("--decode", type=int, default=None, metavar="N",
                    help="instead of the prefill step: N timed decode steps on the pruned and "
                         "gated KV cache the workload's prefill leaves (one new token per sample "
@@ -473,6 +479,22 @@ def main():
             _, (k, lm, hm, fm) = project()
             svl.svl_prefill(cfg, table, k, scores, inp.vision, inp.text, lm, hm, fm, kept, resid,
                             ws, stream=stream, want_flops=False)
+    elif args.controller is not None:
+        rng = np.random.default_rng([args.seed, 7])
+        logits_np = (rng.standard_normal((B, N)) - 0.6745).astype(np.float32)
+        scores = torch.from_numpy(logits_np).to(dev)
+        draw = W.draw_controller(w, args.seed, device=dev, prefix=shape.n_layers // 2)
+        ctrl = svl.Controller(draw.prefix, draw.units, draw.pe_dim, draw.hidden, draw.pe_scale,
+                              draw.pe_base, draw.tensors)
+        resid = torch.empty((B * (N + w.n_text + 1), shape.d_model), dtype=torch.float32,
+                            device=dev)
+        ws = svl.alloc_controlled_workspace(cfg, ctrl, B, N, w.n_text, dev)
+        state = {}
+
+        def step():
+            state["out"] = svl.svl_prefill_controlled(cfg, table, ctrl, scores, inp.vision,
+                                                      inp.text, args.controller, 0, kept, resid,
+                                                      ws, stream=stream)
     else:
         def step():
             svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
@@ -510,15 +532,36 @@ def main():
     svl.svl_timing_enable(False)
     ktime = {k: svl.svl_timing_read(k) for k in svl.KCLASS}
 
-    flops = svl.svl_count_flops(cfg, seqlens, lm_run, hm_run, fm_run)
+    if args.controller is not None:
+        # two phases: the prefix layers at the threshold lengths, the others at
+        # the projected ones
+        out = state["out"]
+        P = shape.n_layers // 2
+        counts0 = (logits_np > 0).sum(1)
+        keep_run, lm_run, hm_run, fm_run = out["keep"], out["layer_mask"], out["head_mask"], out["ffn_mask"]
+        seq1 = (counts0 + w.n_text + 1).astype(np.int64)
+        seqlens = (np.asarray(keep_run) + w.n_text + 1).astype(np.int64)
+        R = int(seqlens.sum())
+        lm1 = np.zeros_like(lm_run)
+        lm1[:, :P] = 1
+        lm2 = lm_run.copy()
+        lm2[:, :P] = 0
+        flops = out["flops"]
+        b1, n1 = gemm_bytes(shape, seq1, lm1, hm_run, fm_run)
+        b2, n2 = gemm_bytes(shape, seqlens, lm2, hm_run, fm_run)
+        bytes_ = {k: b1[k] + b2[k] for k in b1}
+        launches = {k: n1[k] + n2[k] for k in n1}
+    else:
+        flops = svl.svl_count_flops(cfg, seqlens, lm_run, hm_run, fm_run)
+        bytes_, launches = gemm_bytes(shape, seqlens, lm_run, hm_run, fm_run)
     gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
     gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / args.steps
     attn_ms = ktime["attention"][0] / args.steps
     tokens = B * (w.n_vision + w.n_text)
     value = tokens / (ms * 1e-3)
 
-    bytes_, launches = gemm_bytes(shape, seqlens, lm_run, hm_run, fm_run)
-    traffic = measured_traffic() if w.name == W.HEADLINE and args.threshold_budget is None else None
+    default_mode = args.threshold_budget is None and args.controller is None
+    traffic = measured_traffic() if w.name == W.HEADLINE and default_mode else None
     gu_ms, gu_n = ktime["gemm_gate_up"]
     gu_avg_ms = gu_ms / max(1, gu_n)
     gu_bytes_per_launch = bytes_["gu"] / max(1, launches["gu"])
@@ -526,11 +569,20 @@ def main():
     per_kernel = {k: {"ms_per_step": v[0] / args.steps, "launches_per_step": v[1] / args.steps}
                   for k, v in ktime.items() if v[1]}
 
+    if args.controller is not None:
+        metric = (f"effective prefill tokens/s, 7B-shaped, compute controller after "
+                  f"{shape.n_layers // 2} prefix layers + threshold selection + budget "
+                  f"projection to {args.controller} of C_full")
+        workload = f"{w.name}_controller_b{args.controller}"
+    elif args.threshold_budget is not None:
+        metric = (f"effective prefill tokens/s, 7B-shaped, threshold selection + budget "
+                  f"projection to {args.threshold_budget} of C_full")
+        workload = f"{w.name}_threshold_b{args.threshold_budget}"
+    else:
+        metric = "effective prefill tokens/s + MFMA util (% peak), 7B-shaped, keep 0.25"
+        workload = w.name
     result = {
-        "metric": ("effective prefill tokens/s + MFMA util (% peak), 7B-shaped, keep 0.25"
-                   if args.threshold_budget is None else
-                   f"effective prefill tokens/s, 7B-shaped, threshold selection + budget "
-                   f"projection to {args.threshold_budget} of C_full"),
+        "metric": metric,
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -544,8 +596,7 @@ def main():
         "dtype": "f16" if shape.dtype == "bf16" else "f32",
         "storage_dtype": shape.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name if args.threshold_budget is None else
-                   f"{w.name}_threshold_b{args.threshold_budget}",
+        "config": {"workload": workload,
                    "batch": B, "n_vision": w.n_vision, "n_text": w.n_text,
                    "keep": [int(k) for k in keep_run], "kept_tokens": R,
                    "layers_executed_per_sample": [int(x) for x in np.asarray(lm_run).sum(1)],
@@ -578,7 +629,16 @@ def main():
                                    int(np.sum(np.asarray(inp.head_mask) != np.asarray(hm_run)) //
                                        (shape.n_heads // shape.n_groups)),
                                "step": "count kernel + host sync + projection + prefill"}
-    if not args.no_cpu_baseline and args.threshold_budget is None:
+    if args.controller is not None:
+        result["controller"] = {
+            "positive_logits": [int(c) for c in counts0], "budget": args.controller,
+            "vocab_term": 0, "prefix_layers": shape.n_layers // 2, "units": "head groups",
+            "gate_logits_positive": int((out["gate_logits"] > 0).sum()),
+            "gate_logits": int(out["gate_logits"].size),
+            "layers_skipped": int((lm_run == 0).sum()),
+            "step": "stats kernel + sync + prefix layers + controller head + sync + projection "
+                    "+ row compaction + remaining layers"}
+    if not args.no_cpu_baseline and default_mode:
         result["cpu_baseline"] = cpu_baseline(w, inp, layers, args.cpu_layers)
     print(json.dumps(result))
 

@@ -24,7 +24,8 @@
  * Streams.  `stream` is a hipStream_t passed as void* (NULL: the null
  *   stream).  All device work is enqueued on it; device outputs are valid once
  *   the stream reaches that point.  No call synchronises the stream, except
- *   svl_count_positive (its counts are host outputs).
+ *   svl_count_positive and svl_prefill_controlled (host outputs that the
+ *   host plans from).
  * Dtypes.  `svl_config.dtype` selects the storage type of weights and of the
  *   vision / text hidden states: SVL_F32 (float) or SVL_BF16 (bfloat16).  The
  *   residual stream `resid` is always float32.  SVL_BF16 runs 16-bit MFMA
@@ -231,6 +232,85 @@ svl_status svl_budget_project(const svl_config *cfg, int32_t batch, int32_t n_vi
                               int32_t prefix, uint8_t *layer_mask, uint8_t *head_mask,
                               uint8_t *ffn_mask, const float *gate_logits, int32_t *keep);
 
+/* ---- compute controller and the controlled prefill ----------------------
+ * The LLM-side compute controller (Sec. 3.2) decides, per sample, which
+ * layers and head groups run after the P prefix layers:
+ *   e_b = MLP_LLM(PE(b)), the budget token, is appended after the text
+ *   tokens and runs through the prefix layers with the rest of the sequence;
+ *   kappa = sum_i sigma(z_i) / N, the soft survival rate of the visual
+ *   tokens, is encoded and added to the budget token's state after the
+ *   prefix: h~ = h_b^(P) + MLP_kappa(PE(kappa)) (Eq. (7));
+ *   the gating head's logits W_h h~ + c_h switch a unit on iff > 0 (sigma >
+ *   0.5, Gumbel noise removed at inference).  Layer-head controller: one
+ *   unit per (dynamic layer, head group j), gating heads [j A/G, (j+1) A/G)
+ *   and FFN slice j, a layer with every group off is skipped; layer
+ *   controller: one unit per dynamic layer (full capacity or bypassed).
+ * PE(x) of width E: entry 2i = sin(x s w_i), entry 2i+1 = cos(x s w_i),
+ * w_i = base^(-2i/E), s = pe_scale.  MLP: Linear(E -> H) + bias, GELU
+ * (erf form), Linear(H -> D) + bias.  The controller's products run in
+ * float32 (weights widened from the storage dtype); the encodings and
+ * kappa in float64. */
+typedef struct {
+  int32_t prefix;     /* P: layers 0..P-1 run at full capacity, 0 <= P < n_layers */
+  int32_t units;      /* gates per dynamic layer: n_groups (layer-head) or 1 (layer) */
+  int32_t pe_dim;     /* E: encoding width, a multiple of 8 in [8, 65536] */
+  int32_t hidden;     /* H: hidden width of both MLPs, a multiple of 8 in [8, 65536] */
+  float pe_scale;     /* s: the encoded scalar is multiplied by s (finite) */
+  float pe_base;      /* frequency base (finite, > 0; 10000 in the Transformer encoding) */
+  /* dev, config dtype, [out][in] rows 16-byte aligned:
+   *   llm_w1, kap_w1 [H][E];  llm_b1, kap_b1 [H];  llm_w2, kap_w2 [D][H];
+   *   llm_b2, kap_b2 [D];  gate_w [(L-P)*units][D];  gate_b [(L-P)*units]. */
+  const void *llm_w1, *llm_b1, *llm_w2, *llm_b2;
+  const void *kap_w1, *kap_b1, *kap_w2, *kap_b2;
+  const void *gate_w, *gate_b;
+} svl_controller;
+
+/* Workspace bytes of svl_prefill_controlled (0 on bad arguments). */
+size_t svl_controlled_workspace_bytes(const svl_config *cfg, const svl_controller *ctrl,
+                                      int32_t batch, int32_t n_vision, int32_t n_text);
+
+/* The controlled prefill (Sec. 3.1-3.3 at inference), per sample b:
+ *   1. threshold selection: the visual tokens with logits[b][i] > 0 (their
+ *      count c_b) in ascending index order, then the text tokens, then the
+ *      budget token: c_b + n_text + 1 rows;
+ *   2. layers 0..P-1 at full capacity;
+ *   3. the controller's gate logits and masks (above);
+ *   4. budget < 1: the budget projection of svl_budget_project (counts c_b,
+ *      the controller's masks, its gate logits as the confidence order, with
+ *      units = whole layers for the layer controller); the visual tokens it
+ *      discards (the lowest logits) leave the sequence here, the remaining
+ *      rows keep their order and are numbered 0..S'-1 for RoPE from layer P
+ *      on (Eq. (8)'s S counts text and visual tokens, not the budget token);
+ *   5. layers P..L-1 under the final masks.
+ * Arguments:
+ *   logits     dev float [B][N]: the token controller's logits z
+ *   vision     dev dtype [B][N][D];  text dev dtype [B][T][D]
+ *   budget     b, finite and > 0 (>= 1: no projection); vocab: V of Eq. (8)
+ *   kept_idx   dev int32 [B][N] (out): final kept tokens ascending, rest -1
+ *   resid      dev float, room for B*(N+T+1) rows (out): the final packed
+ *              sequences [kept vision ; text ; budget token] after layer L-1
+ *   cu_seqlens host int32 [B+1] (out) of the final sequences
+ *   keep       host int32 [B] (out): final visual tokens per sample
+ *   layer_mask host uint8 [B][L], head_mask [B][L][A], ffn_mask [B][L][G]
+ *              (out): the masks the layers ran with
+ *   gate_logits host float [B][(L-P)*units] (out, may be NULL): the raw
+ *              gate logits, layer-major
+ *   flops      host (out, may be NULL): executed layer FLOPs (the prefix
+ *              layers at the threshold lengths, the others at the final ones)
+ *   ws/ws_bytes: at least svl_controlled_workspace_bytes(...).
+ * Like svl_count_positive, this call synchronises `stream` twice: after
+ * the threshold counts and after the gate logits, which the host needs to
+ * plan the launches.  An error found after the first synchronisation (a HIP
+ * error) leaves the outputs undefined. */
+svl_status svl_prefill_controlled(const svl_config *cfg, const svl_layer_weights *layers,
+                                  const svl_controller *ctrl, int32_t batch, int32_t n_vision,
+                                  int32_t n_text, float budget, int64_t vocab,
+                                  const float *logits, const void *vision, const void *text,
+                                  int32_t *kept_idx, float *resid, int32_t *cu_seqlens,
+                                  int32_t *keep, uint8_t *layer_mask, uint8_t *head_mask,
+                                  uint8_t *ffn_mask, float *gate_logits, svl_flops *flops,
+                                  void *ws, size_t ws_bytes, void *stream);
+
 /* ---- decode on the pruned and gated KV cache ----------------------------
  * After the prefill, tokens are generated one at a time; the paper leaves
  * this stage to future work (Sec. 5).  The cache holds only what the prefill
@@ -298,8 +378,9 @@ int32_t svl_abi_version(void);
  * Kernel classes: 0 select, 1 gather, 2 rmsnorm, 3 qkv gemm, 4 attention
  * (prefill and decode), 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope
  * table, 9 split-K finish (QKV and gate/up launches whose K was split),
- * 10 KV-cache append. */
-#define SVL_KCLASS_COUNT 11
+ * 10 KV-cache append, 11 compute controller (statistics, encodings, its
+ * matrix-vector products, budget rows and row compaction). */
+#define SVL_KCLASS_COUNT 12
 svl_status svl_timing_enable(int32_t on);
 svl_status svl_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);
 

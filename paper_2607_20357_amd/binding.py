@@ -22,10 +22,13 @@ LIB_PATH = os.path.join(_HERE, "libsvl.so")
 SVL_F32, SVL_BF16 = 0, 1
 SVL_COMPUTE_F16, SVL_COMPUTE_BF16 = 0, 1
 KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
-          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9, "kv_append": 10}
+          "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9, "kv_append": 10,
+          "controller": 11}
 STATUS = {0: "SVL_OK", 1: "SVL_E_NULL", 2: "SVL_E_SHAPE", 3: "SVL_E_VALUE", 4: "SVL_E_WORKSPACE",
           5: "SVL_E_DTYPE", 6: "SVL_E_HIP", 7: "SVL_E_ALIGN"}
 WEIGHT_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+CONTROLLER_FIELDS = ("llm_w1", "llm_b1", "llm_w2", "llm_b2", "kap_w1", "kap_b1", "kap_w2",
+                     "kap_b2", "gate_w", "gate_b")
 
 
 class SvlError(RuntimeError):
@@ -50,6 +53,12 @@ class svl_layer_weights(ctypes.Structure):
 class svl_batch(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_vision", ctypes.c_int32),
                 ("n_text", ctypes.c_int32), ("keep", ctypes.POINTER(ctypes.c_int32))]
+
+
+class svl_controller(ctypes.Structure):
+    _fields_ = [("prefix", ctypes.c_int32), ("units", ctypes.c_int32), ("pe_dim", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("pe_scale", ctypes.c_float),
+                ("pe_base", ctypes.c_float)] + [(n, ctypes.c_void_p) for n in CONTROLLER_FIELDS]
 
 
 class svl_flops(ctypes.Structure):
@@ -91,6 +100,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.svl_decode_workspace_bytes.restype = sz
     lib.svl_budget_project.argtypes = [cfgp, i32, i32, i32, P, ctypes.c_float, ctypes.c_int64,
                                        i32, P, P, P, P, P]
+    lib.svl_controlled_workspace_bytes.argtypes = [cfgp, ctypes.POINTER(svl_controller), i32, i32,
+                                                   i32]
+    lib.svl_controlled_workspace_bytes.restype = sz
+    lib.svl_prefill_controlled.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights),
+                                           ctypes.POINTER(svl_controller), i32, i32, i32,
+                                           ctypes.c_float, ctypes.c_int64, P, P, P, P, P, P, P,
+                                           P, P, P, P, ctypes.POINTER(svl_flops), P, sz, P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_workspace_bytes.restype = sz
     lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
@@ -102,7 +118,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(ctypes.c_int64)]
     for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
               "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
-              "svl_prefill_cache", "svl_decode_step"):
+              "svl_prefill_cache", "svl_decode_step", "svl_prefill_controlled"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -351,3 +367,60 @@ def svl_timing_read(kernel_class: str):
     n = ctypes.c_int64()
     _check(load_library().svl_timing_read(KCLASS[kernel_class], ctypes.byref(ms), ctypes.byref(n)))
     return float(ms.value), int(n.value)
+
+
+class Controller:
+    """Compute-controller parameters as an svl_controller (keeps the tensors alive).
+
+    tensors: CONTROLLER_FIELDS -> GPU tensors in the storage dtype."""
+
+    def __init__(self, prefix: int, units: int, pe_dim: int, hidden: int, pe_scale: float,
+                 pe_base: float, tensors: Dict[str, torch.Tensor]):
+        self.tensors = dict(tensors)
+        self.struct = svl_controller(int(prefix), int(units), int(pe_dim), int(hidden),
+                                     float(pe_scale), float(pe_base),
+                                     *[_dev(self.tensors[n], n) for n in CONTROLLER_FIELDS])
+
+
+def svl_controlled_workspace_bytes(cfg: svl_config, ctrl: Controller, batch: int, n_vision: int,
+                                   n_text: int) -> int:
+    n = load_library().svl_controlled_workspace_bytes(ctypes.byref(cfg), ctypes.byref(ctrl.struct),
+                                                      int(batch), int(n_vision), int(n_text))
+    if n == 0:
+        raise SvlError(2, "svl_controlled_workspace_bytes: invalid arguments")
+    return int(n)
+
+
+def alloc_controlled_workspace(cfg: svl_config, ctrl: Controller, batch: int, n_vision: int,
+                               n_text: int, device="cuda") -> torch.Tensor:
+    return torch.empty(svl_controlled_workspace_bytes(cfg, ctrl, batch, n_vision, n_text),
+                       dtype=torch.uint8, device=device)
+
+
+def svl_prefill_controlled(cfg: svl_config, layers, ctrl: Controller, logits: torch.Tensor,
+                           vision: torch.Tensor, text: torch.Tensor, budget: float, vocab: int,
+                           kept_idx: torch.Tensor, resid: torch.Tensor, ws: torch.Tensor,
+                           stream=None, want_flops: bool = True) -> Dict[str, object]:
+    """The controlled prefill (synchronises the stream twice).  resid needs room
+    for B (N + T + 1) rows.  Returns the host outputs: cu_seqlens, keep,
+    layer_mask, head_mask, ffn_mask, gate_logits and flops."""
+    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
+    B, N = logits.shape
+    T = int(text.shape[1])
+    L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    nl = (L - ctrl.struct.prefix) * ctrl.struct.units
+    out = {"cu_seqlens": np.zeros(B + 1, np.int32), "keep": np.zeros(B, np.int32),
+           "layer_mask": np.zeros((B, L), np.uint8), "head_mask": np.zeros((B, L, A), np.uint8),
+           "ffn_mask": np.zeros((B, L, G), np.uint8),
+           "gate_logits": np.zeros((B, max(nl, 0)), np.float32)}
+    vp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    fl = svl_flops()
+    _check(load_library().svl_prefill_controlled(
+        ctypes.byref(cfg), table.array, ctypes.byref(ctrl.struct), int(B), int(N), T,
+        ctypes.c_float(budget), ctypes.c_int64(int(vocab)), _dev(logits, "logits"),
+        _dev(vision, "vision"), _dev(text, "text"), _dev(kept_idx, "kept_idx"),
+        _dev(resid, "resid"), vp(out["cu_seqlens"]), vp(out["keep"]), vp(out["layer_mask"]),
+        vp(out["head_mask"]), vp(out["ffn_mask"]), vp(out["gate_logits"]),
+        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
+    out["flops"] = fl.as_dict() if want_flops else None
+    return out

@@ -73,7 +73,7 @@ hipError_t timed(int cls, hipStream_t st, F&& f) {
 }
 
 enum KClass { K_SELECT = 0, K_GATHER, K_NORM, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_ROPE, K_FINISH,
-              K_KV_APPEND };
+              K_KV_APPEND, K_CTRL };
 
 // ------------------------------------------------------------------ validation
 svl_status check_config(const svl_config* c, bool for_kernels = true) {
@@ -801,7 +801,303 @@ svl_status svl_budget_project(const svl_config* cfg, int32_t batch, int32_t n_vi
     keep[b] = project_budget_sample(*cfg, n_vision, n_text, counts[b], budget, vocab, prefix,
                                     layer_mask + b * L, head_mask + b * L * A,
                                     ffn_mask ? ffn_mask + b * L * G : nullptr,
-                                    gate_logits ? gate_logits + b * L * G : nullptr);
+                                    gate_logits ? gate_logits + b * L * G : nullptr, (int32_t)G);
+  return SVL_OK;
+}
+
+// ------------------------------------------------------------ controlled prefill
+// Workspace: the prefill's regions for the longest possible packing
+// (B (N + T + 1) rows), then the controller's buffers.
+struct CtrlLayout {
+  int64_t counts, kappa, old_cu, kidx, pe, hid, eb, htil, glog, rcopy, total;
+};
+
+static CtrlLayout ctrl_layout(const svl_config& c, const svl_controller& k, int32_t B, int32_t N,
+                              int32_t Rmax) {
+  CtrlLayout L{};
+  int64_t off = ws_layout(c, B, Rmax).total;
+  auto take = [&](int64_t bytes) {
+    const int64_t o = off;
+    off = align256(off + std::max<int64_t>(bytes, 1));
+    return o;
+  };
+  const int64_t E = k.pe_dim, H = k.hidden, D = c.d_model;
+  const int64_t nl = (int64_t)(c.n_layers - k.prefix) * k.units;
+  L.counts = take(4LL * B);
+  L.kappa = take(8LL * B);
+  L.old_cu = take(4LL * (B + 1));
+  L.kidx = take(4LL * B * std::max(N, 1));
+  L.pe = take(4LL * B * E);
+  L.hid = take(4LL * B * H);
+  L.eb = take(4LL * D);
+  L.htil = take(4LL * B * D);
+  L.glog = take(4LL * B * nl);
+  L.rcopy = take(4LL * Rmax * D);
+  L.total = off;
+  return L;
+}
+
+static svl_status check_controller(const svl_config& c, const svl_controller* k) {
+  if (!k) return fail(SVL_E_NULL, "ctrl is NULL");
+  if (k->prefix < 0 || k->prefix >= c.n_layers)
+    return fail(SVL_E_VALUE, "ctrl->prefix %d outside [0, n_layers)", k->prefix);
+  if (k->units != c.n_groups && k->units != 1)
+    return fail(SVL_E_VALUE, "ctrl->units must be n_groups (layer-head) or 1 (layer)");
+  if (k->units > 1 && c.n_heads % k->units)
+    return fail(SVL_E_SHAPE, "n_heads %% n_groups != 0 (head groups)");
+  if (k->pe_dim < 8 || k->pe_dim > 65536 || k->pe_dim % 8)
+    return fail(SVL_E_SHAPE, "ctrl->pe_dim must be a multiple of 8 in [8, 65536]");
+  if (k->hidden < 8 || k->hidden > 65536 || k->hidden % 8)
+    return fail(SVL_E_SHAPE, "ctrl->hidden must be a multiple of 8 in [8, 65536]");
+  if (c.d_model % 8) return fail(SVL_E_SHAPE, "the controller needs d_model %% 8 == 0");
+  if (!std::isfinite(k->pe_scale)) return fail(SVL_E_VALUE, "ctrl->pe_scale must be finite");
+  if (!std::isfinite(k->pe_base) || !(k->pe_base > 0.f))
+    return fail(SVL_E_VALUE, "ctrl->pe_base must be finite and > 0");
+  const void* w[10] = {k->llm_w1, k->llm_b1, k->llm_w2, k->llm_b2, k->kap_w1,
+                       k->kap_b1, k->kap_w2, k->kap_b2, k->gate_w, k->gate_b};
+  for (int i = 0; i < 10; ++i) {
+    if (!w[i]) return fail(SVL_E_NULL, "NULL controller weight pointer");
+    if (i % 2 == 0 && !aligned16(w[i]))
+      return fail(SVL_E_ALIGN, "controller weight matrices must be 16-byte aligned");
+  }
+  return SVL_OK;
+}
+
+size_t svl_controlled_workspace_bytes(const svl_config* cfg, const svl_controller* ctrl,
+                                      int32_t batch, int32_t n_vision, int32_t n_text) {
+  if (check_config(cfg) != SVL_OK || check_controller(*cfg, ctrl) != SVL_OK) return 0;
+  if (batch <= 0 || n_vision < 0 || n_text < 0) return 0;
+  const int64_t rmax = (int64_t)batch * ((int64_t)n_vision + n_text + 1);
+  if (rmax > INT32_MAX) return 0;
+  return (size_t)ctrl_layout(*cfg, *ctrl, batch, n_vision, (int32_t)rmax).total;
+}
+
+svl_status svl_prefill_controlled(const svl_config* cfg, const svl_layer_weights* layers,
+                                  const svl_controller* ctrl, int32_t batch, int32_t n_vision,
+                                  int32_t n_text, float budget, int64_t vocab,
+                                  const float* logits, const void* vision, const void* text,
+                                  int32_t* kept_idx, float* resid, int32_t* cu_seqlens,
+                                  int32_t* keep, uint8_t* layer_mask, uint8_t* head_mask,
+                                  uint8_t* ffn_mask, float* gate_logits, svl_flops* flops,
+                                  void* ws, size_t ws_bytes, void* stream) {
+  svl_status s = check_config(cfg);
+  if (s != SVL_OK) return s;
+  const svl_config& c = *cfg;
+  if ((s = check_layers(c, layers)) != SVL_OK) return s;
+  if ((s = check_controller(c, ctrl)) != SVL_OK) return s;
+  const svl_controller& k = *ctrl;
+  if (batch <= 0 || n_vision < 0 || n_text < 0)
+    return fail(SVL_E_SHAPE, "batch must be positive, token counts >= 0");
+  if (!std::isfinite(budget) || !(budget > 0.f)) return fail(SVL_E_VALUE, "budget must be finite and > 0");
+  if (vocab < 0) return fail(SVL_E_VALUE, "vocab must be >= 0");
+  const int64_t rmax = (int64_t)batch * ((int64_t)n_vision + n_text + 1);
+  if (rmax > INT32_MAX) return fail(SVL_E_SHAPE, "too many packed rows");
+  if (!resid || !cu_seqlens || !keep || !layer_mask || !head_mask || !ffn_mask || !ws)
+    return fail(SVL_E_NULL, "NULL argument");
+  if (n_vision > 0 && (!logits || !vision || !kept_idx))
+    return fail(SVL_E_NULL, "logits, vision and kept_idx are required when n_vision > 0");
+  if (n_text > 0 && !text) return fail(SVL_E_NULL, "text is required when n_text > 0");
+  for (const void* p : {(const void*)logits, vision, text, (const void*)kept_idx,
+                        (const void*)resid, (const void*)ws})
+    if (p && !aligned16(p)) return fail(SVL_E_ALIGN, "device pointers must be 16-byte aligned");
+  const int32_t B = batch, N = n_vision, T = n_text, L = c.n_layers, A = c.n_heads;
+  const int32_t G = c.n_groups, D = c.d_model, P = k.prefix, U = k.units;
+  const int32_t E = k.pe_dim, H = k.hidden, nl = (L - P) * U, Rmax = (int32_t)rmax;
+  const CtrlLayout CL = ctrl_layout(c, k, B, N, Rmax);
+  if ((int64_t)ws_bytes < CL.total)
+    return fail(SVL_E_WORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)CL.total);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  int32_t* counts_dev = reinterpret_cast<int32_t*>(wsb + CL.counts);
+  double* kappa_dev = reinterpret_cast<double*>(wsb + CL.kappa);
+  int32_t* old_cu_dev = reinterpret_cast<int32_t*>(wsb + CL.old_cu);
+  int32_t* kidx_dev = reinterpret_cast<int32_t*>(wsb + CL.kidx);
+  float* pe_dev = reinterpret_cast<float*>(wsb + CL.pe);
+  float* hid_dev = reinterpret_cast<float*>(wsb + CL.hid);
+  float* eb_dev = reinterpret_cast<float*>(wsb + CL.eb);
+  float* htil_dev = reinterpret_cast<float*>(wsb + CL.htil);
+  float* glog_dev = reinterpret_cast<float*>(wsb + CL.glog);
+  float* rcopy_dev = reinterpret_cast<float*>(wsb + CL.rcopy);
+  const bool bf16 = c.dtype == SVL_BF16;
+  auto linear = [&](const void* W, const void* bias, int32_t in, int32_t out, int32_t nvec,
+                    int32_t act, const float* x, int64_t ldx, const float* add,
+                    const int32_t* add_cu, float* y, int64_t ldy) {
+    CtrlLinearArgs a{};
+    a.W = W; a.bias = bias; a.in = in; a.out = out; a.nvec = nvec; a.act = act;
+    a.x = x; a.ldx = ldx; a.add = add; a.add_cu = add_cu; a.ldadd = D; a.y = y; a.ldy = ldy;
+    return timed(K_CTRL, st, [&] { return launch_ctrl_linear(a, bf16, st); });
+  };
+  hipError_t e;
+
+  // 1. threshold counts and kappa
+  e = timed(K_CTRL, st, [&] { return launch_ctrl_stats(logits, B, N, counts_dev, kappa_dev, st); });
+  if (e != hipSuccess) return hip_fail(e, "controller statistics");
+  std::vector<int32_t> counts(B);
+  if ((e = hipMemcpyAsync(counts.data(), counts_dev, 4 * (size_t)B, hipMemcpyDeviceToHost, st)) !=
+          hipSuccess ||
+      (e = hipStreamSynchronize(st)) != hipSuccess)
+    return hip_fail(e, "threshold counts");
+
+  // 2. [kept vision ; text ; budget token] through the prefix layers at full capacity
+  std::vector<int32_t> seq(B);
+  int32_t R1 = 0;
+  for (int32_t b = 0; b < B; ++b) { seq[b] = counts[b] + T + 1; R1 += seq[b]; }
+  std::vector<uint8_t> all_on((size_t)B * A, 1);
+  std::vector<LayerMasks> full(std::max(P, 1));
+  for (auto& m : full) m = LayerMasks{all_on.data(), all_on.data(), A, nullptr, 0};
+  std::string err;
+  if (!build_plan(c, B, counts.data(), seq.data(), P, full.data(), &t_plan, &err))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  const WsLayout WL = ws_layout(c, B, Rmax);
+  WsLayout WL1 = WL;
+  WL1.partial_slice = (int64_t)R1 * D;
+  Exec ex1{c, st, wsb, WL1, t_plan, resid};
+  if ((s = stage(ex1, true)) != SVL_OK) return s;
+  const int32_t* keep1_dev = ex1.at<int32_t>(t_plan.keep_off);
+  const int32_t* cu1_dev = ex1.at<int32_t>(t_plan.cu_off);
+  e = timed(K_SELECT, st, [&] { return launch_select(logits, B, N, keep1_dev, kidx_dev, st); });
+  if (e == hipSuccess)
+    e = timed(K_GATHER, st, [&] {
+      return launch_gather(kidx_dev, keep1_dev, cu1_dev, B, N, T, D, R1, vision, text, c.dtype,
+                           resid, st);
+    });
+  if (e == hipSuccess)
+    e = timed(K_CTRL, st, [&] {
+      return launch_pe(nullptr, (double)budget, 1, E, (double)k.pe_scale, (double)k.pe_base,
+                       pe_dev, st);
+    });
+  if (e == hipSuccess)
+    e = linear(k.llm_w1, k.llm_b1, E, H, 1, CTRL_ACT_GELU, pe_dev, E, nullptr, nullptr, hid_dev, H);
+  if (e == hipSuccess)
+    e = linear(k.llm_w2, k.llm_b2, H, D, 1, CTRL_ACT_NONE, hid_dev, H, nullptr, nullptr, eb_dev, D);
+  if (e == hipSuccess)
+    e = timed(K_CTRL, st, [&] { return launch_budget_rows(eb_dev, cu1_dev, B, D, resid, st); });
+  for (int32_t l = 0; l < P && e == hipSuccess; ++l) e = ex1.layer(t_plan.layers[l], layers[l], l);
+  if (e == hipSuccess) e = ex1.norm(t_plan.final_norm, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "prefix launch");
+
+  // 3. gate logits: W_h (h_b^(P) + MLP_kappa(PE(kappa))) + c_h
+  e = timed(K_CTRL, st, [&] {
+    return launch_pe(kappa_dev, 0.0, B, E, (double)k.pe_scale, (double)k.pe_base, pe_dev, st);
+  });
+  if (e == hipSuccess)
+    e = linear(k.kap_w1, k.kap_b1, E, H, B, CTRL_ACT_GELU, pe_dev, E, nullptr, nullptr, hid_dev, H);
+  if (e == hipSuccess)
+    e = linear(k.kap_w2, k.kap_b2, H, D, B, CTRL_ACT_NONE, hid_dev, H, resid, cu1_dev, htil_dev, D);
+  if (e == hipSuccess)
+    e = linear(k.gate_w, k.gate_b, D, nl, B, CTRL_ACT_NONE, htil_dev, D, nullptr, nullptr, glog_dev,
+               nl);
+  // the old packing's row offsets, kept for the compaction below
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(old_cu_dev, cu1_dev, 4 * (size_t)(B + 1), hipMemcpyDeviceToDevice, st);
+  std::vector<float> gl((size_t)B * nl);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(gl.data(), glog_dev, 4 * gl.size(), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "gate logits");
+  for (size_t i = 0; i < gl.size(); ++i)
+    if (!std::isfinite(gl[i])) return fail(SVL_E_VALUE, "gate logit %zu is not finite", i);
+
+  // 4. masks (a unit is on iff its logit > 0), then the budget projection
+  std::vector<float> conf((size_t)L * U, 0.f);
+  std::vector<int32_t> keep2(counts);
+  for (int32_t b = 0; b < B; ++b) {
+    uint8_t* lm = layer_mask + (int64_t)b * L;
+    uint8_t* hm = head_mask + (int64_t)b * L * A;
+    uint8_t* fm = ffn_mask + (int64_t)b * L * G;
+    const float* g = gl.data() + (size_t)b * nl;
+    for (int32_t l = 0; l < L; ++l) {
+      if (l < P) {
+        lm[l] = 1;
+        std::fill(hm + (int64_t)l * A, hm + (int64_t)(l + 1) * A, 1);
+        std::fill(fm + (int64_t)l * G, fm + (int64_t)(l + 1) * G, 1);
+        continue;
+      }
+      const float* gu = g + (size_t)(l - P) * U;
+      if (U == 1) {
+        const uint8_t on = gu[0] > 0.f ? 1 : 0;
+        lm[l] = on;
+        std::fill(hm + (int64_t)l * A, hm + (int64_t)(l + 1) * A, on);
+        std::fill(fm + (int64_t)l * G, fm + (int64_t)(l + 1) * G, on);
+      } else {
+        uint8_t any = 0;
+        const int32_t hg = A / G;
+        for (int32_t j = 0; j < G; ++j) {
+          const uint8_t on = gu[j] > 0.f ? 1 : 0;
+          std::fill(hm + (int64_t)l * A + j * hg, hm + (int64_t)l * A + (j + 1) * hg, on);
+          fm[(int64_t)l * G + j] = on;
+          any |= on;
+        }
+        lm[l] = any;
+      }
+    }
+    if (budget < 1.0f) {
+      std::copy(g, g + nl, conf.begin() + (size_t)P * U);
+      keep2[b] = project_budget_sample(c, N, T, counts[b], budget, vocab, P, lm, hm, fm,
+                                       conf.data(), U);
+    }
+  }
+
+  // 5. the discarded tokens leave at the prefix boundary; layers P..L-1
+  bool compact = false;
+  int32_t R2 = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    compact = compact || keep2[b] < counts[b];
+    seq[b] = keep2[b] + T + 1;
+    R2 += seq[b];
+  }
+  if (compact &&
+      (e = hipMemcpyAsync(rcopy_dev, resid, (size_t)R1 * D * 4, hipMemcpyDeviceToDevice, st)) !=
+          hipSuccess)
+    return hip_fail(e, "row copy");
+  std::vector<LayerMasks> masks;
+  std::vector<uint8_t> lon;
+  layer_masks(c, B, layer_mask, head_mask, ffn_mask, masks, lon);
+  if (!build_plan(c, B, keep2.data(), seq.data(), L - P, masks.data() + P, &t_plan, &err))
+    return fail(SVL_E_VALUE, "%s", err.c_str());
+  WsLayout WL2 = WL;
+  WL2.partial_slice = (int64_t)R2 * D;
+  Exec ex2{c, st, wsb, WL2, t_plan, resid};
+  if ((s = stage(ex2, true)) != SVL_OK) return s;
+  const int32_t* keep2_dev = ex2.at<int32_t>(t_plan.keep_off);
+  const int32_t* cu2_dev = ex2.at<int32_t>(t_plan.cu_off);
+  e = timed(K_SELECT, st, [&] { return launch_select(logits, B, N, keep2_dev, kept_idx, st); });
+  if (e == hipSuccess && compact) {
+    CompactArgs ca{rcopy_dev, resid, old_cu_dev, counts_dev, kidx_dev, cu2_dev, keep2_dev, kept_idx,
+                   B, N, D};
+    e = timed(K_CTRL, st, [&] { return launch_compact_rows(ca, R2, st); });
+  }
+  for (int32_t l = P; l < L && e == hipSuccess; ++l)
+    e = ex2.layer(t_plan.layers[l - P], layers[l], l);
+  if (e == hipSuccess) e = ex2.norm(t_plan.final_norm, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "layer launch");
+
+  cu_seqlens[0] = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    cu_seqlens[b + 1] = cu_seqlens[b] + seq[b];
+    keep[b] = keep2[b];
+  }
+  if (gate_logits) std::copy(gl.begin(), gl.end(), gate_logits);
+  if (flops) {
+    // prefix layers at the threshold lengths, the others at the final ones
+    std::vector<uint8_t> lm1((size_t)B * L, 0), lm2(layer_mask, layer_mask + (size_t)B * L);
+    std::vector<int32_t> seq1(B);
+    for (int32_t b = 0; b < B; ++b) {
+      seq1[b] = counts[b] + T + 1;
+      for (int32_t l = 0; l < P; ++l) { lm1[(size_t)b * L + l] = 1; lm2[(size_t)b * L + l] = 0; }
+    }
+    svl_flops f1{}, f2{};
+    if ((s = svl_count_flops(cfg, B, seq1.data(), lm1.data(), head_mask, ffn_mask, &f1)) != SVL_OK ||
+        (s = svl_count_flops(cfg, B, seq.data(), lm2.data(), head_mask, ffn_mask, &f2)) != SVL_OK)
+      return s;
+    flops->q = f1.q + f2.q;
+    flops->kv = f1.kv + f2.kv;
+    flops->o = f1.o + f2.o;
+    flops->attn = f1.attn + f2.attn;
+    flops->ffn = f1.ffn + f2.ffn;
+    flops->total = f1.total + f2.total;
+  }
   return SVL_OK;
 }
 

@@ -71,29 +71,33 @@ int32_t max_tokens(const svl_config& c, int32_t n_text, int32_t n_pos, int64_t s
 int32_t project_budget_sample(const svl_config& c, int32_t n_vision, int32_t n_text,
                               int32_t n_pos, float budget, int64_t vocab, int32_t prefix,
                               uint8_t* layer_on, uint8_t* head_on, uint8_t* ffn_on,
-                              const float* gate_logits) {
+                              const float* gate_logits, int32_t units) {
   if (budget >= 1.0f) return n_pos;
-  const int64_t L = c.n_layers, A = c.n_heads, G = c.n_groups, hg = A / G;
+  const int64_t L = c.n_layers, A = c.n_heads, G = units, hg = A / G;
   const i128 full = cost_times_heads(c, (int64_t)n_text + n_vision, L * A, vocab);
   int64_t sum_a = active_heads(c, layer_on, head_on);
   const int32_t s = max_tokens(c, n_text, n_pos, sum_a, vocab, budget, full);
   if (s >= 0) return s;
   // Even no visual token fits: switch off whole head groups of layers at or
   // after the prefix, lowest gate logit first (ties: later layer, higher group).
-  std::vector<std::tuple<float, int64_t, int64_t>> units;   // (logit, -layer, -group)
+  // With one unit per layer (layer controller) a unit is the whole layer.
+  std::vector<std::tuple<float, int64_t, int64_t>> order;   // (logit, -layer, -group)
   for (int64_t l = prefix; l < L; ++l) {
     if (!layer_on[l]) continue;
     for (int64_t j = 0; j < G; ++j) {
       bool any = false;
       for (int64_t h = j * hg; h < (j + 1) * hg; ++h) any = any || head_on[l * A + h];
-      if (any) units.emplace_back(gate_logits ? gate_logits[l * G + j] : 0.0f, -l, -j);
+      if (any) order.emplace_back(gate_logits ? gate_logits[l * G + j] : 0.0f, -l, -j);
     }
   }
-  std::sort(units.begin(), units.end());
-  for (const auto& u : units) {
+  std::sort(order.begin(), order.end());
+  for (const auto& u : order) {
     const int64_t l = -std::get<1>(u), j = -std::get<2>(u);
     for (int64_t h = j * hg; h < (j + 1) * hg; ++h) head_on[l * A + h] = 0;
-    if (ffn_on) ffn_on[l * G + j] = 0;
+    if (ffn_on) {
+      if (G == 1) { for (int64_t q = 0; q < c.n_groups; ++q) ffn_on[l * c.n_groups + q] = 0; }
+      else ffn_on[l * G + j] = 0;
+    }
     bool any = false;
     for (int64_t h = 0; h < A; ++h) any = any || head_on[l * A + h];
     if (!any) layer_on[l] = 0;

@@ -163,6 +163,7 @@ __global__ __launch_bounds__(NT) void gather_kernel(const int32_t* kept_idx, con
     if (cu[mid] <= r) lo = mid; else hi = mid - 1;
   }
   const int b = lo, i = r - cu[b], k = keep[b];
+  if (i >= k + T) return;   // rows past the text (the controlled prefill's budget token)
   size_t src_row;
   const void* src;
   if (i < k) {

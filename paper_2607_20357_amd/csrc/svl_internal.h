@@ -115,6 +115,39 @@ struct NormArgs {
   float eps;
 };
 
+// Small matrix-vector products of the compute controller:
+// y[r][o] = act(sum_i W[o][i] x[r][i] + bias[o]) (+ add[row(r)][o]) for
+// r < nvec, W [out][in] in the storage dtype (in % 8 == 0, rows 16-byte
+// aligned), x / y / add float32.  add_cu: row(r) = add_cu[r+1] - 1 (the last
+// packed row of sample r), else row(r) = r.
+enum CtrlAct : int32_t { CTRL_ACT_NONE = 0, CTRL_ACT_GELU = 1 };
+struct CtrlLinearArgs {
+  const void* W;
+  const void* bias;     // [out] or nullptr
+  int32_t in, out, nvec, act;
+  const float* x;
+  int64_t ldx;
+  const float* add;
+  const int32_t* add_cu;
+  int64_t ldadd;
+  float* y;
+  int64_t ldy;
+};
+
+// Row moves of the controlled prefill: new packing from the old one after
+// the budget projection shortened the visual blocks.
+struct CompactArgs {
+  const float* src;          // old packed rows [old rows][D]
+  float* dst;                // new packed rows [new rows][D]
+  const int32_t* old_cu;     // [B+1]
+  const int32_t* old_keep;   // [B]
+  const int32_t* old_kidx;   // [B][N], ascending kept indices
+  const int32_t* new_cu;
+  const int32_t* new_keep;
+  const int32_t* new_kidx;   // subset of old_kidx per sample
+  int32_t B, N, D;
+};
+
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipSuccess or the launch error).
 hipError_t launch_count_positive(const float* logits, int32_t B, int32_t N, int32_t* counts,
@@ -137,6 +170,15 @@ hipError_t launch_attn_decode(const AttnArgs& a, int32_t head_dim, bool f16, hip
 hipError_t launch_attn_f32(const AttnArgs& a, int32_t head_dim, hipStream_t st);
 hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, float theta,
                              hipStream_t st);
+// Compute controller.
+hipError_t launch_ctrl_stats(const float* z, int32_t B, int32_t N, int32_t* counts, double* kappa,
+                             hipStream_t st);
+hipError_t launch_pe(const double* xs, double x0, int32_t nvec, int32_t E, double scale,
+                     double base, float* out, hipStream_t st);
+hipError_t launch_ctrl_linear(const CtrlLinearArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_budget_rows(const float* eb, const int32_t* cu, int32_t B, int32_t D,
+                              float* resid, hipStream_t st);
+hipError_t launch_compact_rows(const CompactArgs& a, int32_t rows, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t st);
 
 }  // namespace svl

@@ -212,3 +212,60 @@ def test_budget_projection_rejects_bad_arguments():
                 dict(gate_logits=np.full((1, L, G), np.nan, np.float32))):
         with pytest.raises(svl.SvlError):
             svl.svl_budget_project(cfg, **{**ok, **bad})
+
+
+# --------------------------------------------------------------------------- controlled prefill
+def _fake_controller(**kw):
+    base = dict(prefix=1, units=2, pe_dim=16, hidden=32, pe_scale=1000.0, pe_base=10000.0)
+    base.update({k: v for k, v in kw.items() if k in base})
+    ptrs = [kw.get(n, 16 * 4096 * (i + 1)) for i, n in enumerate(binding.CONTROLLER_FIELDS)]
+    return binding.svl_controller(base["prefix"], base["units"], base["pe_dim"], base["hidden"],
+                                  base["pe_scale"], base["pe_base"], *ptrs)
+
+
+def _call_controlled(cfg, ctrl, B=2, N=8, T=3, budget=0.5, ws_bytes=None):
+    lib = svl.load_library()
+    L = cfg.n_layers
+    layers = (binding.svl_layer_weights * L)(
+        *[binding.svl_layer_weights(*[16 * 4096 * (j + 20)] * 9) for j in range(L)])
+    n = lib.svl_controlled_workspace_bytes(ctypes.byref(cfg), ctypes.byref(ctrl), B, N, T)
+    ws_bytes = (n - 1 if n else 1 << 20) if ws_bytes is None else ws_bytes
+    host = [np.zeros(s, t) for s, t in (((B + 1,), np.int32), ((B,), np.int32),
+                                         ((B, L), np.uint8), ((B, L, cfg.n_heads), np.uint8),
+                                         ((B, L, cfg.n_groups), np.uint8))]
+    vp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    dev = 16 * 4096 * 100
+    st = lib.svl_prefill_controlled(ctypes.byref(cfg), layers, ctypes.byref(ctrl), B, N, T,
+                                    ctypes.c_float(budget), ctypes.c_int64(0), dev, dev, dev, dev,
+                                    dev, *[vp(h) for h in host], None, None, dev, ws_bytes, None)
+    return st, lib.svl_last_error().decode()
+
+
+def test_controlled_prefill_rejects_bad_arguments():
+    """Every case fails a host-side check before the first launch (a workspace
+    one byte short of svl_controlled_workspace_bytes is the last check)."""
+    cfg = _cfg()
+    st, msg = _call_controlled(cfg, _fake_controller())
+    assert st == 4, msg
+    cases = [(dict(prefix=2), 3), (dict(prefix=-1), 3), (dict(units=3), 3), (dict(pe_dim=12), 2),
+             (dict(hidden=0), 2), (dict(pe_base=0.0), 3), (dict(pe_scale=float("inf")), 3),
+             (dict(llm_w2=None), 1), (dict(gate_b=None), 1), (dict(kap_w1=16 * 4096 + 8), 7)]
+    for kw, want in cases:
+        st, msg = _call_controlled(cfg, _fake_controller(**kw))
+        assert st == want, (kw, st, msg)
+    for budget in (float("nan"), 0.0, -0.5, float("inf")):
+        st, _ = _call_controlled(cfg, _fake_controller(), budget=budget)
+        assert st == 3
+    st, _ = _call_controlled(cfg, _fake_controller(), B=0)
+    assert st == 2
+
+
+def test_controlled_workspace_covers_the_prefill_workspace():
+    cfg = _cfg()
+    lib = svl.load_library()
+    ctrl = _fake_controller()
+    for B, N, T in ((1, 8, 3), (3, 100, 20), (2, 0, 5)):
+        n = lib.svl_controlled_workspace_bytes(ctypes.byref(cfg), ctypes.byref(ctrl), B, N, T)
+        assert n >= svl.svl_workspace_bytes(cfg, B, B * (N + T + 1)) + 4 * B * (N + T + 1) * 128
+    assert lib.svl_controlled_workspace_bytes(ctypes.byref(cfg), ctypes.byref(
+        _fake_controller(units=3)), 1, 8, 3) == 0
