@@ -102,7 +102,12 @@ __device__ __forceinline__ float load_w1(const void* W, size_t off) {
   else return static_cast<const float*>(W)[off];
 }
 
-// One wave per output row o (4 rows per workgroup).
+// One wave per output row o (4 rows per workgroup).  Each lane takes 8
+// consecutive inputs per 512-input step and issues the weight loads of LIN_U
+// steps before using them, so every wave keeps LIN_U 1 KiB row pieces in
+// flight.
+constexpr int LIN_U = 4;
+
 template <bool BF16>
 __global__ __launch_bounds__(NT) void linear_kernel(CtrlLinearArgs a) {
   const int lane = threadIdx.x & 63;
@@ -114,16 +119,27 @@ __global__ __launch_bounds__(NT) void linear_kernel(CtrlLinearArgs a) {
     float acc[LIN_NV];
 #pragma unroll
     for (int r = 0; r < LIN_NV; ++r) acc[r] = 0.f;
-    for (int k = lane * 8; k < a.in; k += 64 * 8) {
-      float w[8];
-      load_w8<BF16>(a.W, wrow + k, w);
+    for (int k0 = lane * 8; k0 < a.in; k0 += 64 * 8 * LIN_U) {
+      float w[LIN_U][8];
+#pragma unroll
+      for (int u = 0; u < LIN_U; ++u) {
+        const int k = k0 + u * 64 * 8;
+        if (k < a.in) load_w8<BF16>(a.W, wrow + k, w[u]);
+      }
 #pragma unroll
       for (int r = 0; r < LIN_NV; ++r) {
         if (r < nv) {
-          const float4* xp = reinterpret_cast<const float4*>(a.x + (size_t)(r0 + r) * a.ldx + k);
-          const float4 x0 = xp[0], x1 = xp[1];
-          acc[r] += w[0] * x0.x + w[1] * x0.y + w[2] * x0.z + w[3] * x0.w +
-                    w[4] * x1.x + w[5] * x1.y + w[6] * x1.z + w[7] * x1.w;
+          const float* xr = a.x + (size_t)(r0 + r) * a.ldx;
+#pragma unroll
+          for (int u = 0; u < LIN_U; ++u) {
+            const int k = k0 + u * 64 * 8;
+            if (k < a.in) {
+              const float4* xp = reinterpret_cast<const float4*>(xr + k);
+              const float4 x0 = xp[0], x1 = xp[1];
+              acc[r] += w[u][0] * x0.x + w[u][1] * x0.y + w[u][2] * x0.z + w[u][3] * x0.w +
+                        w[u][4] * x1.x + w[u][5] * x1.y + w[u][6] * x1.z + w[u][7] * x1.w;
+            }
+          }
         }
       }
     }
