@@ -311,6 +311,48 @@ svl_status svl_prefill_controlled(const svl_config *cfg, const svl_layer_weights
                                   uint8_t *ffn_mask, float *gate_logits, svl_flops *flops,
                                   void *ws, size_t ws_bytes, void *stream);
 
+/* ---- training-time budget term -------------------------------------------
+ * During training the controllers' decisions are Gumbel-sigmoid
+ * straight-through masks (Eq. (6)): y = sigma((z + xi) / tau), mask =
+ * 1[y > 0.5] in the forward pass, dy/dz in the backward pass.  The budget
+ * term (Sec. 3.3) prices them with Eq. (8) at the soft visual count
+ * S~ = sum_i sigma(z_i) (S = n_text + S~) and the layer activities
+ * alpha_l = (units on) / U of the unit masks (prefix layers at 1):
+ *   r = C^ / C_full,
+ *   loss = lambda_t (w_over max(0, r - b)^2 + w_under max(0, (b - margin) - r))
+ * (Eq. (9), the budget part of Eq. (10)).  svl_budget_loss gives, per sample,
+ * the forward masks, r, the loss and its gradient with respect to the token
+ * logits (through S~; the token masks act on the prediction loss only) and
+ * to the gate logits (straight-through: dalpha_l/dg = (1/U) y (1 - y) /
+ * tau_comp).  The hinge's derivative at its kink is taken as 0.  Sums run in
+ * float64; outputs are float32. */
+typedef struct {
+  float budget;      /* b, finite and > 0 */
+  float margin;      /* mu >= 0: zero-loss band [b - mu, b] */
+  float w_over, w_under;  /* >= 0 */
+  float lambda_t;    /* warm-up factor lambda(t) = min(1, t / T_warmup), >= 0 */
+  float tau_tok;     /* token temperature (> 0; the decision z + xi > 0 does not depend on it) */
+  float tau_comp;    /* compute temperature (> 0) */
+  int32_t prefix;    /* P, 0 <= P < n_layers */
+  int32_t units;     /* n_groups (layer-head controller) or 1 (layer controller) */
+  int64_t vocab;     /* V of Eq. (8), >= 0 */
+} svl_budget_loss_params;
+
+/* Per sample b (all pointers dev):
+ *   logits      float [B][N]: token logits z;  token_noise float [B][N] or NULL
+ *   gate_logits float [B][(L-P) units];  gate_noise same or NULL
+ *   token_mask  uint8 [B][N] (out): 1 iff z + xi > 0
+ *   unit_mask   uint8 [B][(L-P) units] (out): 1 iff g + xi > 0
+ *   ratio, loss float [B] (out);  grad_logits float [B][N] (out): dloss/dz;
+ *   grad_gate   float [B][(L-P) units] (out): dloss/dg.
+ * n_vision + n_text > 0.  Enqueued on `stream`; no workspace. */
+svl_status svl_budget_loss(const svl_config *cfg, const svl_budget_loss_params *params,
+                           int32_t batch, int32_t n_vision, int32_t n_text,
+                           const float *logits, const float *token_noise,
+                           const float *gate_logits, const float *gate_noise,
+                           uint8_t *token_mask, uint8_t *unit_mask, float *ratio, float *loss,
+                           float *grad_logits, float *grad_gate, void *stream);
+
 /* ---- decode on the pruned and gated KV cache ----------------------------
  * After the prefill, tokens are generated one at a time; the paper leaves
  * this stage to future work (Sec. 5).  The cache holds only what the prefill
@@ -379,7 +421,8 @@ int32_t svl_abi_version(void);
  * (prefill and decode), 5 o-proj gemm, 6 gate/up gemm, 7 down gemm, 8 rope
  * table, 9 split-K finish (QKV and gate/up launches whose K was split),
  * 10 KV-cache append, 11 compute controller (statistics, encodings, its
- * matrix-vector products, budget rows and row compaction). */
+ * matrix-vector products, budget rows and row compaction) and the
+ * training-time budget term. */
 #define SVL_KCLASS_COUNT 12
 svl_status svl_timing_enable(int32_t on);
 svl_status svl_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);

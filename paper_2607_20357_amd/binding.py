@@ -61,6 +61,14 @@ class svl_controller(ctypes.Structure):
                 ("pe_base", ctypes.c_float)] + [(n, ctypes.c_void_p) for n in CONTROLLER_FIELDS]
 
 
+class svl_budget_loss_params(ctypes.Structure):
+    _fields_ = [("budget", ctypes.c_float), ("margin", ctypes.c_float),
+                ("w_over", ctypes.c_float), ("w_under", ctypes.c_float),
+                ("lambda_t", ctypes.c_float), ("tau_tok", ctypes.c_float),
+                ("tau_comp", ctypes.c_float), ("prefix", ctypes.c_int32),
+                ("units", ctypes.c_int32), ("vocab", ctypes.c_int64)]
+
+
 class svl_flops(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in ("q", "kv", "o", "attn", "ffn", "total")]
 
@@ -107,6 +115,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                            ctypes.POINTER(svl_controller), i32, i32, i32,
                                            ctypes.c_float, ctypes.c_int64, P, P, P, P, P, P, P,
                                            P, P, P, P, ctypes.POINTER(svl_flops), P, sz, P]
+    lib.svl_budget_loss.argtypes = [cfgp, ctypes.POINTER(svl_budget_loss_params), i32, i32, i32,
+                                    P, P, P, P, P, P, P, P, P, P, P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_workspace_bytes.restype = sz
     lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
@@ -118,7 +128,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(ctypes.c_int64)]
     for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
               "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
-              "svl_prefill_cache", "svl_decode_step", "svl_prefill_controlled"):
+              "svl_prefill_cache", "svl_decode_step", "svl_prefill_controlled",
+              "svl_budget_loss"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -423,4 +434,29 @@ def svl_prefill_controlled(cfg: svl_config, layers, ctrl: Controller, logits: to
         vp(out["head_mask"]), vp(out["ffn_mask"]), vp(out["gate_logits"]),
         ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
     out["flops"] = fl.as_dict() if want_flops else None
+    return out
+
+
+def svl_budget_loss(cfg: svl_config, params: svl_budget_loss_params, logits: torch.Tensor,
+                    gate_logits: torch.Tensor, n_text: int, token_noise=None, gate_noise=None,
+                    stream=None) -> Dict[str, torch.Tensor]:
+    """Training-time budget term on the GPU; returns device tensors token_mask,
+    unit_mask, ratio, loss, grad_logits, grad_gate (enqueued on the stream)."""
+    B, N = logits.shape
+    nl = gate_logits.shape[1]
+    dev = logits.device
+    out = {"token_mask": torch.empty((B, N), dtype=torch.uint8, device=dev),
+           "unit_mask": torch.empty((B, nl), dtype=torch.uint8, device=dev),
+           "ratio": torch.empty(B, dtype=torch.float32, device=dev),
+           "loss": torch.empty(B, dtype=torch.float32, device=dev),
+           "grad_logits": torch.empty((B, N), dtype=torch.float32, device=dev),
+           "grad_gate": torch.empty((B, nl), dtype=torch.float32, device=dev)}
+    opt = lambda t, n: None if t is None else _dev(t, n)
+    _check(load_library().svl_budget_loss(
+        ctypes.byref(cfg), ctypes.byref(params), int(B), int(N), int(n_text),
+        _dev(logits, "logits"), opt(token_noise, "token_noise"), _dev(gate_logits, "gate_logits"),
+        opt(gate_noise, "gate_noise"), _dev(out["token_mask"], "token_mask"),
+        _dev(out["unit_mask"], "unit_mask"), _dev(out["ratio"], "ratio"), _dev(out["loss"], "loss"),
+        _dev(out["grad_logits"], "grad_logits"), _dev(out["grad_gate"], "grad_gate"),
+        _stream(stream)))
     return out

@@ -1101,6 +1101,55 @@ svl_status svl_prefill_controlled(const svl_config* cfg, const svl_layer_weights
   return SVL_OK;
 }
 
+// ------------------------------------------------------------ training-time budget term
+svl_status svl_budget_loss(const svl_config* cfg, const svl_budget_loss_params* p, int32_t batch,
+                           int32_t n_vision, int32_t n_text, const float* logits,
+                           const float* token_noise, const float* gate_logits,
+                           const float* gate_noise, uint8_t* token_mask, uint8_t* unit_mask,
+                           float* ratio, float* loss, float* grad_logits, float* grad_gate,
+                           void* stream) {
+  svl_status s = check_config(cfg, false);
+  if (s != SVL_OK) return s;
+  if (!p) return fail(SVL_E_NULL, "params is NULL");
+  const svl_config& c = *cfg;
+  if (batch <= 0 || n_vision < 0 || n_text < 0 || (int64_t)n_vision + n_text == 0)
+    return fail(SVL_E_SHAPE, "batch must be positive, token counts >= 0 with n_vision + n_text > 0");
+  if (p->prefix < 0 || p->prefix >= c.n_layers)
+    return fail(SVL_E_VALUE, "prefix %d outside [0, n_layers)", p->prefix);
+  if (p->units != c.n_groups && p->units != 1)
+    return fail(SVL_E_VALUE, "units must be n_groups (layer-head) or 1 (layer)");
+  if (p->vocab < 0) return fail(SVL_E_VALUE, "vocab must be >= 0");
+  const float pos[3] = {p->budget, p->tau_tok, p->tau_comp};
+  for (float v : pos)
+    if (!std::isfinite(v) || !(v > 0.f))
+      return fail(SVL_E_VALUE, "budget and temperatures must be finite and > 0");
+  const float nonneg[4] = {p->margin, p->w_over, p->w_under, p->lambda_t};
+  for (float v : nonneg)
+    if (!std::isfinite(v) || v < 0.f)
+      return fail(SVL_E_VALUE, "margin, loss weights and lambda must be finite and >= 0");
+  if (!ratio || !loss || !gate_logits || !unit_mask || !grad_gate)
+    return fail(SVL_E_NULL, "NULL argument");
+  if (n_vision > 0 && (!logits || !token_mask || !grad_logits))
+    return fail(SVL_E_NULL, "logits, token_mask and grad_logits are required when n_vision > 0");
+  const double D = c.d_model, F = c.d_ffn, L = c.n_layers;
+  const double Sf = (double)n_text + n_vision;
+  BudgetLossArgs a{};
+  a.z = logits; a.xi_tok = token_noise; a.gl = gate_logits; a.xi_gate = gate_noise;
+  a.N = n_vision; a.T = n_text; a.L = c.n_layers; a.P = p->prefix; a.U = p->units;
+  a.c1 = 8.0 * D * D + 6.0 * D * F;
+  a.c2 = 4.0 * D;
+  a.lm = 2.0 * D * (double)p->vocab;
+  a.full = L * (a.c1 * Sf + a.c2 * Sf * Sf) + a.lm * Sf;
+  a.budget = p->budget; a.margin = p->margin; a.w_over = p->w_over; a.w_under = p->w_under;
+  a.lam = p->lambda_t; a.tau_comp = p->tau_comp;
+  a.tok_mask = token_mask; a.unit_mask = unit_mask; a.ratio = ratio; a.loss = loss;
+  a.grad_z = grad_logits; a.grad_gate = grad_gate;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(K_CTRL, st, [&] { return launch_budget_loss(a, batch, st); });
+  if (e != hipSuccess) return hip_fail(e, "budget loss");
+  return SVL_OK;
+}
+
 svl_status svl_timing_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.on = on != 0;

@@ -148,6 +148,25 @@ struct CompactArgs {
   int32_t B, N, D;
 };
 
+// Training-time budget term, per sample b (rows of N tokens / nl = (L-P) U
+// units).  Cost constants: c1 = 8 D^2 + 6 D F, c2 = 4 D, lm = 2 D V,
+// full = C_full; budget is the float32 budget's value.
+struct BudgetLossArgs {
+  const float* z;          // [B][N] token logits
+  const float* xi_tok;     // [B][N] noise or nullptr
+  const float* gl;         // [B][nl] gate logits
+  const float* xi_gate;    // [B][nl] noise or nullptr
+  int32_t N, T, L, P, U;
+  double c1, c2, lm, full;
+  double budget, margin, w_over, w_under, lam, tau_comp;
+  uint8_t* tok_mask;       // [B][N]
+  uint8_t* unit_mask;      // [B][nl]
+  float* ratio;            // [B]
+  float* loss;             // [B]
+  float* grad_z;           // [B][N]
+  float* grad_gate;        // [B][nl]
+};
+
 // ---------------------------------------------------------------------------
 // Launchers (each returns hipSuccess or the launch error).
 hipError_t launch_count_positive(const float* logits, int32_t B, int32_t N, int32_t* counts,
@@ -179,6 +198,7 @@ hipError_t launch_ctrl_linear(const CtrlLinearArgs& a, bool bf16, hipStream_t st
 hipError_t launch_budget_rows(const float* eb, const int32_t* cu, int32_t B, int32_t D,
                               float* resid, hipStream_t st);
 hipError_t launch_compact_rows(const CompactArgs& a, int32_t rows, hipStream_t st);
+hipError_t launch_budget_loss(const BudgetLossArgs& a, int32_t B, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t st);
 
 }  // namespace svl

@@ -269,3 +269,26 @@ def test_controlled_workspace_covers_the_prefill_workspace():
         assert n >= svl.svl_workspace_bytes(cfg, B, B * (N + T + 1)) + 4 * B * (N + T + 1) * 128
     assert lib.svl_controlled_workspace_bytes(ctypes.byref(cfg), ctypes.byref(
         _fake_controller(units=3)), 1, 8, 3) == 0
+
+
+def test_budget_loss_rejects_bad_arguments():
+    """Host-side checks of svl_budget_loss (no launch happens in these cases)."""
+    cfg = _cfg()
+    lib = svl.load_library()
+    dev = 16 * 4096 * 100
+
+    def call(B=2, N=8, T=3, **kw):
+        base = dict(budget=0.5, margin=0.1, w_over=1.0, w_under=1.0, lambda_t=1.0, tau_tok=1.0,
+                    tau_comp=1.0, prefix=1, units=2, vocab=0)
+        base.update(kw)
+        prm = binding.svl_budget_loss_params(*base.values())
+        st = lib.svl_budget_loss(ctypes.byref(cfg), ctypes.byref(prm), B, N, T, dev, None, dev,
+                                 None, dev, dev, dev, dev, dev, dev, None)
+        return st
+    for kw, want in ((dict(budget=float("nan")), 3), (dict(budget=0.0), 3), (dict(tau_tok=0.0), 3),
+                     (dict(tau_comp=-1.0), 3), (dict(margin=-0.1), 3), (dict(w_over=float("inf")), 3),
+                     (dict(lambda_t=-1.0), 3), (dict(prefix=2), 3), (dict(units=3), 3),
+                     (dict(vocab=-5), 3), (dict(B=0), 2), (dict(N=0, T=0), 2)):
+        assert call(**kw) == want, kw
+    assert lib.svl_budget_loss(ctypes.byref(cfg), None, 1, 1, 1, dev, None, dev, None, dev, dev,
+                               dev, dev, dev, dev, None) == 1
