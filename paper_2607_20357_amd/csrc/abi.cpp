@@ -204,6 +204,12 @@ struct Exec {
     a.head_dim = c.head_dim;
     a.partial = reinterpret_cast<float*>(ws + L.partial);
     const bool f16 = c.compute == SVL_COMPUTE_F16;
+    if (decode) {
+      // one row per sample: row-vector products over the groups' blocks
+      a.ngroups = g.ngroups;
+      a.nblocks = g.nblocks;
+      return timed(cls, st, [&] { return launch_gemv(a, epi, f16, st); });
+    }
     const bool paired = epi == EPI_QKV || epi == EPI_SWIGLU;
     if (paired && g.nsplit > 1) {
       // split pieces: float32 slices [nsplit][padded rows][pld], then the finish
@@ -244,6 +250,7 @@ struct Exec {
     a.nrows = n.nrows;
     a.ngroups8 = n.ngroups8;
     a.rows8 = n.rows8 ? 1 : 0;
+    a.rowmajor = decode ? 1 : 0;   // decode: row-vector products read row-major rows
     a.x = resid;
     a.partial = reinterpret_cast<const float*>(ws + L.partial);
     a.nsplit = n.nsplit;

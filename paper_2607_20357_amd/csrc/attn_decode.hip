@@ -159,8 +159,9 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
     }
     const uint4 w = make_uint4(pack_act2<F16>(r[0], r[1]), pack_act2<F16>(r[2], r[3]),
                                pack_act2<F16>(r[4], r[5]), pack_act2<F16>(r[6], r[7]));
+    // row-major [rows][A d]: the decode step's output projection reads it row by row
     uint16_t* out = static_cast<uint16_t*>(a.out);
-    *reinterpret_cast<uint4*>(out + packed_index((int64_t)g.row0, h * D + 8 * dg, a.ldo)) = w;
+    *reinterpret_cast<uint4*>(out + (size_t)g.row0 * a.ldo + h * D + 8 * dg) = w;
   }
 }
 

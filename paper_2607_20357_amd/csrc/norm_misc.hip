@@ -82,7 +82,8 @@ __global__ __launch_bounds__(NT) void resid_norm_kernel(NormArgs a) {
                                  pack_act2<OUT == 2>(v0.z * inv * g[2], v0.w * inv * g[3]),
                                  pack_act2<OUT == 2>(v1.x * inv * g[4], v1.y * inv * g[5]),
                                  pack_act2<OUT == 2>(v1.z * inv * g[6], v1.w * inv * g[7]));
-      *reinterpret_cast<uint4*>(out + packed_index((int64_t)prow, 8 * c, D)) = o;
+      *reinterpret_cast<uint4*>(out + (a.rowmajor ? (int64_t)prow * D + 8 * c
+                                                  : packed_index((int64_t)prow, 8 * c, D))) = o;
     }
   } else {
     const float4* gain = reinterpret_cast<const float4*>(a.gain);
@@ -195,7 +196,9 @@ __global__ __launch_bounds__(NTR) void resid_norm_reg_kernel(NormArgs a) {
       const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
       const uint2 o = make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
                                  pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + packed_index((int64_t)prow, 4 * c, a.D)) = o;
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) +
+                                (a.rowmajor ? (int64_t)prow * a.D + 4 * c
+                                            : packed_index((int64_t)prow, 4 * c, a.D))) = o;
     } else {
       const float4 g = gv[i];
       reinterpret_cast<float4*>(static_cast<float*>(a.out) + prow * a.D)[c] =

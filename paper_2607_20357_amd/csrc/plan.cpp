@@ -135,6 +135,10 @@ struct MmBuild {
   // consecutive, so they land on one XCD.
   GemmLaunch finish(ImageWriter& w, int32_t bpt, int32_t nb, int32_t nsplit) {
     GemmLaunch L;
+    for (auto& g : groups) {   // block numbering of the row-vector launches
+      g.pad0 = L.nblocks;
+      L.nblocks += g.nblocks;
+    }
     L.groups_off = w.append(groups);
     int64_t count = 0;
     for (const auto& g : groups)
@@ -240,9 +244,10 @@ struct MmBuild {
   // Output and down projections: 4-block tiles; a skinny launch splits K
   // into float32 partial slices (at least 2 chunks per piece, the slices
   // within the partial buffer).
-  GemmLaunch finish_plain(ImageWriter& w, int32_t R, int32_t D, int64_t cap_floats) {
+  GemmLaunch finish_plain(ImageWriter& w, int32_t R, int32_t D, int64_t cap_floats,
+                          bool rowvec = false) {
     int32_t s = 1;
-    if (!groups.empty() && max_rows <= kSkinnyRows) {
+    if (!rowvec && !groups.empty() && max_rows <= kSkinnyRows) {
       int64_t base = 0;
       for (const auto& g : groups) base += (int64_t)cdiv(g.nrows, MFMA_BM) * cdiv(g.nblocks, 4);
       s = (int32_t)std::max<int64_t>(1, kTargetTiles / std::max<int64_t>(1, base));
@@ -306,6 +311,10 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
                 int32_t nlayers, const LayerMasks* masks, Plan* plan, std::string* err,
                 const int32_t* pos_base) {
   const bool mfma = cfg.dtype == SVL_BF16;
+  // decode (cached positions given): one row per sample, so the 16-bit GEMMs
+  // run as row-vector launches over the groups' blocks and the output / down
+  // projections add straight into the residual (no split-K)
+  const bool rowvec = pos_base != nullptr;
   const int32_t A = cfg.n_heads, KV = cfg.n_kv_heads, G = cfg.n_groups, d = cfg.head_dim;
   const int32_t D = cfg.d_model, F = cfg.d_ffn, rep = A / KV, slice = F / G;
   const int32_t BM = mfma ? MFMA_BM : F32_BM;
@@ -377,7 +386,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     L.nsegs = (int32_t)segs.size();
     L.nrows = prefix;
     L.ngroups8 = gprefix;
-    L.rows8 = rows8_ok && prefix > 0 && prefix >= rows8_min;
+    L.rows8 = rows8_ok && !rowvec && prefix > 0 && prefix >= rows8_min;
     L.nsplit = pending_split > 1 ? pending_split : 0;
     std::fill(pending.begin(), pending.end(), 0);
     pending_split = 0;
@@ -468,7 +477,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     LP.norm_attn = norm_launch(run_attn);
     if (mfma) {
       LP.qkv = mqkv.finish_paired(w, qkv_width, cap, plan->padded_rows, 2, force_split);
-      LP.o = mo.finish_plain(w, R, D, cap);
+      LP.o = mo.finish_plain(w, R, D, cap, rowvec);
       const int32_t so = LP.o.nsplit;
       if (so > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_attn[b];
@@ -489,7 +498,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     LP.norm_ffn = norm_launch(run_ffn);
     if (mfma) {
       LP.gu = mgu.finish_paired(w, 2 * F, cap, plan->padded_rows, 1, force_split);
-      LP.down = mdown.finish_plain(w, R, D, cap);
+      LP.down = mdown.finish_plain(w, R, D, cap, rowvec);
       const int32_t sd = LP.down.nsplit;
       if (sd > 1) {
         for (int32_t b = 0; b < B; ++b) pending[b] = run_ffn[b];

@@ -22,6 +22,8 @@ struct GemmLaunch {
   int32_t nb = 0;           // 16-bit MFMA path: kernel block count (tiles hold <= nb)
   int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
   int32_t nitems = 0;       // split QKV / gate-up launches: finish kernel work items
+  int32_t nblocks = 0;      // 16-bit path: the groups' 16-column blocks (each group's
+                            // first block in MmGroup::pad0)
 };
 
 struct AttnLaunch {

@@ -61,6 +61,8 @@ struct MmArgs {
                          // pld; SWIGLU: gate columns, then up columns at pld / 2)
                          // for the finish kernel; PARTIAL: row stride ldo
   int32_t pld;
+  int32_t ngroups;       // row-vector launches (decode): groups, and the blocks
+  int32_t nblocks;       // of all groups (a group's first block in its pad0)
 };
 
 // Finish of a split QKV / gate-up launch: sums the split slices in order,
@@ -105,6 +107,7 @@ struct NormArgs {
   NormSeg inl[NORM_INLINE_SEGS];
   int32_t ngroups8;    // 8-row groups (row-group kernel grid)
   int32_t rows8;       // 1: the 8-row-group kernel (16-bit output)
+  int32_t rowmajor;    // 1: 16-bit output row-major [rows][D] (decode), else packed
   float* x;            // residual [rows][D] (written back when partials are added)
   const float* partial;  // split-K slices to add: slice p at partial + p * pslice
   int32_t nsplit;
@@ -181,6 +184,8 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
 hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st);
 hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st);
 hipError_t launch_finish(const FinishArgs& a, int32_t epi, bool f16, hipStream_t st);
+// Decode: one-row groups, one workgroup per 16-column block (QKV, SWIGLU, RESID).
+hipError_t launch_gemv(const MmArgs& a, int32_t epi, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);
 // KV cache: append this call's K / V rows; decode attention over the cache.
