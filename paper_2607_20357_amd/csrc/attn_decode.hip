@@ -50,6 +50,7 @@ __global__ __launch_bounds__(NT) void kv_append_kernel(AttnArgs a) {
   }
 }
 
+template <int NTB>
 __device__ __forceinline__ float block_reduce(float v, bool is_max, float* s_red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
@@ -62,18 +63,27 @@ __device__ __forceinline__ float block_reduce(float v, bool is_max, float* s_red
   __syncthreads();
   float r = s_red[0];
 #pragma unroll
-  for (int i = 1; i < NT / 64; ++i) r = is_max ? fmaxf(r, s_red[i]) : r + s_red[i];
+  for (int i = 1; i < NTB / 64; ++i) r = is_max ? fmaxf(r, s_red[i]) : r + s_red[i];
   return r;
 }
 
+// 1024 threads: TPK = D / 32 threads per key in the score pass (32 dims each),
+// and in the value pass thread t takes dim group t % (D / 8) of the keys
+// j = t / (D / 8) (mod NT / (D / 8)); the partitions of a wave are summed with
+// shuffles, then the waves' partials in LDS in wave order.
+constexpr int NTD = 1024;
+
 template <int D, bool F16>
-__global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
-  constexpr int DG = D / 8;          // 8-dim groups of a row
-  constexpr int NP = NT / DG;        // key partitions of the value pass
+__global__ __launch_bounds__(NTD) void attn_decode_kernel(AttnArgs a) {
+  constexpr int DG = D / 8;           // 8-dim groups of a row
+  constexpr int NP = NTD / DG;        // key partitions of the value pass
+  constexpr int PW = 64 / DG;         // partitions per wave
+  constexpr int TPK = D / 32;         // threads per key in the score pass
+  constexpr int KPP = NTD / TPK;      // keys per score pass
   __shared__ float s_p[MAX_KEYS];
   __shared__ float s_q[D];
-  __shared__ float s_red[NT / 64];
-  __shared__ float s_o[NP][D];
+  __shared__ float s_red[NTD / 64];
+  __shared__ float s_o[NTD / 64][D];
   const int t = blockIdx.x;
   if (t >= a.ntiles) return;
   const AttnGroup g = a.groups[find_group(a.groups, a.ngroups, t)];
@@ -82,7 +92,7 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
   const int h = a.head_table[g.h_off + hs];
   const int kvh = h / rep;
   const int len = g.pos_base + 1;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
   uint16_t* kcw = static_cast<uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 0, 0, D);
   uint16_t* vcw = static_cast<uint16_t*>(a.cache) + cache_index(a, g.sample, kvh, 1, 0, D);
@@ -101,41 +111,82 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
     }
   }
   const float sl2 = a.scale * 1.4426950408889634f;   // scores in log2 units
+  // Loads that do not depend on the scores go out first: this thread's key
+  // piece of the first score pass and its first NPF value rows, so their
+  // latency overlaps the query load, the scores and the softmax.
+  const int sub = tid % TPK;
+  const int dg = tid % DG, pt = tid / DG;
+  constexpr int NPF = 4;
+  uint4 kpre[4], vpre[NPF];
+  {
+    const int j = tid / TPK;
+    if (j < len) {
+      const uint4* kr = reinterpret_cast<const uint4*>((j == g.pos_base ? knew : kc + (size_t)j * D) + 32 * sub);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) kpre[c] = kr[c];
+    }
+#pragma unroll
+    for (int i = 0; i < NPF; ++i) {
+      const int jv = pt + i * NP;
+      vpre[i] = jv < len ? *reinterpret_cast<const uint4*>((jv == g.pos_base ? vnew : vc + (size_t)jv * D) + 8 * dg)
+                         : make_uint4(0, 0, 0, 0);
+    }
+  }
   if (tid < D) s_q[tid] = act_bits_to_f32<F16>(qkv[(size_t)g.row0 * a.ldq + h * D + tid]) * sl2;
   __syncthreads();
 
-  // scores: thread j takes keys j, j + NT, ...
+  // scores: TPK threads per key, 32 dims each, summed by shuffles
   float mloc = -3.0e38f;
-  for (int j = tid; j < len; j += NT) {
-    const uint4* kr = reinterpret_cast<const uint4*>(j == g.pos_base ? knew : kc + (size_t)j * D);
+  for (int j0 = 0; j0 < len; j0 += KPP) {
+    const int j = j0 + tid / TPK;
     float s = 0.f;
+    if (j < len) {
+      const uint4* kr = reinterpret_cast<const uint4*>((j == g.pos_base ? knew : kc + (size_t)j * D) + 32 * sub);
 #pragma unroll
-    for (int c = 0; c < DG; ++c) {
-      const uint4 v = kr[c];
-      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      for (int c = 0; c < 4; ++c) {
+        const uint4 v = j0 == 0 ? kpre[c] : kr[c];
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        s += act_bits_to_f32<F16>(wv[e] & 0xffffu) * s_q[8 * c + 2 * e];
-        s += act_bits_to_f32<F16>(wv[e] >> 16) * s_q[8 * c + 2 * e + 1];
+        for (int e = 0; e < 4; ++e) {
+          s += act_bits_to_f32<F16>(wv[e] & 0xffffu) * s_q[32 * sub + 8 * c + 2 * e];
+          s += act_bits_to_f32<F16>(wv[e] >> 16) * s_q[32 * sub + 8 * c + 2 * e + 1];
+        }
       }
     }
-    s_p[j] = s;
-    mloc = fmaxf(mloc, s);
+#pragma unroll
+    for (int o = 1; o < TPK; o <<= 1) s += __shfl_xor(s, o, 64);
+    if (j < len) {
+      if (sub == 0) s_p[j] = s;
+      mloc = fmaxf(mloc, s);
+    }
   }
-  const float m = block_reduce(mloc, true, s_red);
+  const float m = block_reduce<NTD>(mloc, true, s_red);
   float lsum = 0.f;
-  for (int j = tid; j < len; j += NT) {
+  for (int j = tid; j < len; j += NTD) {
     const float p = exp2f(s_p[j] - m);
     s_p[j] = p;
     lsum += p;
   }
-  const float l = block_reduce(lsum, false, s_red);   // its barriers also publish s_p
+  const float l = block_reduce<NTD>(lsum, false, s_red);   // its barriers also publish s_p
 
   // values: thread (partition pt, dim group dg) sums keys pt, pt + NP, ...
-  const int dg = tid % DG, pt = tid / DG;
+  // (the first NPF of them from the rows loaded up front)
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int j = pt; j < len; j += NP) {
+#pragma unroll
+  for (int i = 0; i < NPF; ++i) {
+    const int j = pt + i * NP;
+    if (j < len) {
+      const float p = s_p[j];
+      const uint32_t wv[4] = {vpre[i].x, vpre[i].y, vpre[i].z, vpre[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[2 * e] += p * act_bits_to_f32<F16>(wv[e] & 0xffffu);
+        o[2 * e + 1] += p * act_bits_to_f32<F16>(wv[e] >> 16);
+      }
+    }
+  }
+#pragma unroll 2
+  for (int j = pt + NPF * NP; j < len; j += NP) {
     const uint4 v = *reinterpret_cast<const uint4*>((j == g.pos_base ? vnew : vc + (size_t)j * D) + 8 * dg);
     const float p = s_p[j];
     const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
@@ -145,24 +196,32 @@ __global__ __launch_bounds__(NT) void attn_decode_kernel(AttnArgs a) {
       o[2 * e + 1] += p * act_bits_to_f32<F16>(wv[e] >> 16);
     }
   }
+  // the wave's PW partitions (lanes dg, dg + DG, ...) in a fixed order
 #pragma unroll
-  for (int e = 0; e < 8; ++e) s_o[pt][8 * dg + e] = o[e];
+  for (int e = 0; e < 8; ++e)
+#pragma unroll
+    for (int sft = DG; sft < 64; sft <<= 1) o[e] += __shfl_xor(o[e], sft, 64);
+  if (lane < DG) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s_o[wave][8 * dg + e] = o[e];
+  }
   __syncthreads();
-  if (pt == 0) {
+  if (tid < DG) {
     const float inv = 1.0f / l;
     float r[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       float acc = 0.f;
-      for (int q = 0; q < NP; ++q) acc += s_o[q][8 * dg + e];   // fixed order
+      for (int q = 0; q < NTD / 64; ++q) acc += s_o[q][8 * tid + e];   // fixed order
       r[e] = acc * inv;
     }
     const uint4 w = make_uint4(pack_act2<F16>(r[0], r[1]), pack_act2<F16>(r[2], r[3]),
                                pack_act2<F16>(r[4], r[5]), pack_act2<F16>(r[6], r[7]));
     // row-major [rows][A d]: the decode step's output projection reads it row by row
     uint16_t* out = static_cast<uint16_t*>(a.out);
-    *reinterpret_cast<uint4*>(out + (size_t)g.row0 * a.ldo + h * D + 8 * dg) = w;
+    *reinterpret_cast<uint4*>(out + (size_t)g.row0 * a.ldo + h * D + 8 * tid) = w;
   }
+  (void)PW;
 }
 
 }  // namespace
@@ -180,11 +239,11 @@ hipError_t launch_attn_decode(const AttnArgs& a, int32_t head_dim, bool f16, hip
   if (a.ntiles <= 0) return hipSuccess;
   if (a.max_len > MAX_KEYS) return hipErrorInvalidValue;
   if (head_dim == 128) {
-    if (f16) attn_decode_kernel<128, true><<<a.ntiles, NT, 0, st>>>(a);
-    else attn_decode_kernel<128, false><<<a.ntiles, NT, 0, st>>>(a);
+    if (f16) attn_decode_kernel<128, true><<<a.ntiles, NTD, 0, st>>>(a);
+    else attn_decode_kernel<128, false><<<a.ntiles, NTD, 0, st>>>(a);
   } else if (head_dim == 64) {
-    if (f16) attn_decode_kernel<64, true><<<a.ntiles, NT, 0, st>>>(a);
-    else attn_decode_kernel<64, false><<<a.ntiles, NT, 0, st>>>(a);
+    if (f16) attn_decode_kernel<64, true><<<a.ntiles, NTD, 0, st>>>(a);
+    else attn_decode_kernel<64, false><<<a.ntiles, NTD, 0, st>>>(a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -27,11 +27,13 @@ constexpr int GV_WAVES = 4, GV_NT = GV_WAVES * 64, GV_U = 4;
 
 // Workgroup x takes quarter q = x % 4 of block x / 4: columns 2q, 2q + 1 and
 // their partners 2q + 8, 2q + 9 (wave w: column (w & 1) + 2q + 8 (w >> 1)).
+constexpr int GV_MAX_CHUNKS = 1024;   // K chunks of a group (K <= 65536)
+
 template <int EPI, bool F16>
 __global__ __launch_bounds__(GV_NT) void gemv_kernel(MmArgs a) {
   __shared__ float s_v[GV_WAVES];
+  __shared__ int32_t s_k0[GV_MAX_CHUNKS];   // a chunk-list group's offsets (no dependent loads)
   const int blk = blockIdx.x >> 2, quarter = blockIdx.x & 3;
-  if (blk >= a.nblocks) return;
   int lo = 0, hi = a.ngroups - 1;   // the group whose first block (pad0) is the largest <= blk
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -57,26 +59,24 @@ __global__ __launch_bounds__(GV_NT) void gemv_kernel(MmArgs a) {
       static_cast<const uint16_t*>(m == 0 ? a.W[0] : (m == 1 ? a.W[1] : a.W[2])) + (size_t)row * a.ldw;
   const uint16_t* xr = static_cast<const uint16_t*>(a.A) + (size_t)g.arow0 * a.lda;
   const int nc = g.kc_cnt, cl = lane >> 3, off = (lane & 7) * 8;
+  const bool dense = g.kdense >= 0;   // uniform across the workgroup
+  if (!dense) {
+    // chunk-list groups (output / down projections under head or FFN gates)
+    // cover whole 64-column chunks: runs of heads (d in {64, 128}) and FFN
+    // slices (a multiple of 64)
+    for (int c = threadIdx.x; c < nc; c += GV_NT) s_k0[c] = a.chunks[g.kc_off + c].k0;
+    __syncthreads();
+  }
   float acc = 0.f;
   for (int s0 = 0; s0 < nc; s0 += 8 * GV_U) {
     uint4 wv[GV_U], xv[GV_U];
 #pragma unroll
     for (int u = 0; u < GV_U; ++u) {
       const int c = s0 + 8 * u + cl;
-      int k0 = 0, len = 0;
       if (c < nc) {
-        if (g.kdense >= 0) {
-          k0 = g.kdense + MFMA_BK * c;
-          len = MFMA_BK;
-        } else {
-          const KChunk ch = a.chunks[g.kc_off + c];
-          k0 = ch.k0;
-          len = ch.len;
-        }
-      }
-      if (off < len) {
-        wv[u] = *reinterpret_cast<const uint4*>(wr + k0 + off);
-        xv[u] = *reinterpret_cast<const uint4*>(xr + k0 + off);
+        const int k = (dense ? g.kdense + MFMA_BK * c : s_k0[c]) + off;
+        wv[u] = *reinterpret_cast<const uint4*>(wr + k);
+        xv[u] = *reinterpret_cast<const uint4*>(xr + k);
       } else {
         wv[u] = make_uint4(0, 0, 0, 0);
         xv[u] = make_uint4(0, 0, 0, 0);
@@ -137,6 +137,7 @@ hipError_t launch(const MmArgs& a, int32_t epi, hipStream_t st) {
 
 hipError_t launch_gemv(const MmArgs& a, int32_t epi, bool f16, hipStream_t st) {
   if (a.nblocks <= 0 || a.ngroups <= 0) return hipSuccess;
+  if (a.lda / MFMA_BK > GV_MAX_CHUNKS) return hipErrorInvalidValue;
   return f16 ? launch<true>(a, epi, st) : launch<false>(a, epi, st);
 }
 
