@@ -400,7 +400,7 @@ def decode_bench(args):
         "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "per_kernel": per_kernel,
         "roofline": {
-            "kernel": "gemm_mfma_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU, one row per sample)",
+            "kernel": "gemv_kernel<EPI_SWIGLU> (gate/up row-vector products + SwiGLU, one row per sample)",
             "bound": "hbm", "achieved": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
