@@ -141,6 +141,33 @@ def test_layer_full_size(name, compute):
     assert max(errs) <= tol_for(w.shape), errs
 
 
+@pytest.mark.parametrize("compute", ["f16", "bf16"])
+def test_layer_row_block_counts(compute):
+    """Single-tile samples of 64 to 208 rows (4 to 13 row blocks, odd block
+    counts and counts just past a multiple of 64) with K chunk lists of 1 to
+    9 chunks (one active head of 64 columns up to d_model 576, including a
+    K that is not a multiple of the 4-chunk weight stage)."""
+    rng = np.random.default_rng(5)
+    for D, A, seqlens in ((512, 8, [80, 144, 208, 65, 129, 193]),
+                          (576, 9, [70, 64, 81, 128, 145, 192, 200]),
+                          (1024, 16, [208, 140, 75])):
+        G = 4 if A % 4 == 0 else 3
+        shape = W.ModelShape(n_layers=1, d_model=D, n_heads=A, n_kv_heads=A, head_dim=64,
+                             d_ffn=G * 256, n_groups=G, dtype="bf16")
+        B = len(seqlens)
+        head_mask = (rng.random((B, A)) > 0.5).astype(np.uint8)
+        head_mask[0] = 0
+        head_mask[0, 1] = 1              # one active head: a one-chunk output projection
+        head_mask[1] = 1
+        ffn_mask = (rng.random((B, G)) > 0.3).astype(np.uint8)
+        ffn_mask[:, 0] = 1
+        print(f"row block counts d_model {D} compute={compute} rows {seqlens}", flush=True)
+        errs = _layer_case(shape, np.array(seqlens, np.int32), np.ones(B, np.uint8), head_mask,
+                           ffn_mask, compute=compute)
+        print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+        assert max(errs) <= tol_for(shape), errs
+
+
 @pytest.mark.parametrize("split", [2, 3])
 def test_layer_forced_paired_split(split, monkeypatch):
     """The split-K QKV and gate/up path (float32 slices, then the finish
