@@ -66,6 +66,11 @@ def parse():
                    help="instead of the prefill step: N timed decode steps on the pruned and "
                         "gated KV cache the workload's prefill leaves (one new token per sample "
                         "per step)")
+    p.add_argument("--library-gemms", action="store_true",
+                   help="instead of the step benchmark: torch's matmul (the vendor BLAS) "
+                        "at the headline's four GEMM shapes, in fp16 and bf16, "
+                        "next to this library's per-launch times of the same GEMMs; one JSON "
+                        "line")
     p.add_argument("--memory-sweep", action="store_true",
                    help="instead of the step benchmark: HBM rate of the memory-bound kernels "
                         "(select, gather, residual norm) on the headline per-row structure "
@@ -291,6 +296,87 @@ def memory_sweep(args):
         torch.cuda.empty_cache()
 
 
+def library_gemms(args):
+    """The headline's GEMM shapes (kept rows x active output columns x active
+    reduction width) through torch's matmul, which dispatches to the vendor
+    BLAS, fp16 and bf16, weights rotated over 8 copies so none is
+    cache-resident, 40 calls replayed from one captured graph; next to this
+    library's per-launch GEMM times over the same headline prefill (HIP
+    events the library records).  The library's
+    launches also apply RoPE / SwiGLU / the split-K partial store."""
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    w = W.get_workload(W.HEADLINE)
+    shape = w.shape
+    inp = W.draw_inputs(w, args.seed, device=dev)
+    l = next(l for l in range(shape.n_layers) if inp.layer_mask[0, l])
+    H = int(inp.head_mask[0, l].sum())
+    C = shape.d_ffn if inp.ffn_mask is None else int(inp.ffn_mask[0, l].sum()) * (shape.d_ffn // shape.n_groups)
+    M = int(inp.keep[0]) + w.n_text
+    D, d = shape.d_model, shape.head_dim
+    shapes = {"gemm_qkv": (M, 3 * H * d, D), "gemm_o": (M, D, H * d),
+              "gemm_gate_up": (M, 2 * C, D), "gemm_down": (M, D, C)}
+    layers = [W.draw_layer_weights(w, k, args.seed, device=dev) for k in range(shape.n_layers)]
+    table = svl.LayerTable(layers)
+    cfg = svl.make_config(shape)
+    B, N = inp.scores.shape
+    R = int((np.asarray(inp.keep) + w.n_text).sum())
+    scores = torch.from_numpy(inp.scores).to(dev)
+    kept = torch.empty((B, N), dtype=torch.int32, device=dev)
+    resid = torch.empty((R, D), dtype=torch.float32, device=dev)
+    ws = svl.alloc_workspace(cfg, B, R, dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
+                        inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
+                        want_flops=False)
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    svl.svl_timing_enable(True)
+    for _ in range(10):
+        step()
+    torch.cuda.synchronize()
+    svl.svl_timing_enable(False)
+    del layers, table, ws
+    torch.cuda.empty_cache()
+    out = {"library_gemms": True, "workload": w.name, "rows": M}
+    for k, (m, n, kk) in shapes.items():
+        ms, cnt = svl.svl_timing_read(k)
+        ours = 1e3 * ms / max(1, cnt)
+        line = {"m": m, "n": n, "k": kk, "svl_us": round(ours, 1)}
+        for dt, tag in ((torch.float16, "blas_f16_us"), (torch.bfloat16, "blas_bf16_us")):
+            x = torch.randn(m, kk, device=dev, dtype=dt)
+            wts = [torch.randn(n, kk, device=dev, dtype=dt) * 0.02 for _ in range(8)]
+            ys = [torch.nn.functional.linear(x, wts[i]) for i in range(8)]
+            torch.cuda.synchronize()
+            # 40 calls captured in one graph: a short call's host launch time
+            # would otherwise leave the GPU idle between kernels and be timed
+            graph = torch.cuda.CUDAGraph()
+            reps = 40
+            with torch.cuda.graph(graph):
+                for i in range(reps):
+                    torch.mm(x, wts[i % 8].t(), out=ys[i % 8])
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            graph.replay()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(2):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            line[tag] = round(e0.elapsed_time(e1) / (2 * reps) * 1e3, 1)
+            del x, wts, ys, graph
+            torch.cuda.empty_cache()
+        out[k] = line
+    print(json.dumps(out), flush=True)
+
+
 def decode_bench(args):
     """Decode on the pruned and gated KV cache: the workload's prefill fills
     the cache (untimed), then each step feeds one new token per sample (seeded
@@ -415,6 +501,9 @@ def main():
     args = parse()
     if args.traffic_from:
         write_traffic(args.traffic_from)
+        return
+    if args.library_gemms:
+        library_gemms(args)
         return
     if args.memory_sweep:
         memory_sweep(args)
