@@ -288,6 +288,7 @@ struct Exec {
       a.groups = at<AttnGroup>(P.attn.groups_off);
       a.ngroups = P.attn.ngroups;
       a.ntiles = P.attn.ntiles;
+      a.bq = P.attn.bq;
       a.head_table = at<int32_t>(P.attn.heads_off);
       a.qkv = ws + L.qkv;
       a.ldq = qkv_w;

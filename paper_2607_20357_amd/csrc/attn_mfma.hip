@@ -3,12 +3,14 @@
 // probabilities and the output are fp16 or bf16 (the activation type),
 // scores, softmax statistics and accumulators float32.
 //
-// One workgroup = one (sample, active query head, 64-row query tile); the
+// One workgroup = one (sample, active query head, BQ-row query tile); the
 // launch lists only active heads, so inactive heads are never read or
-// written.  8 waves: wave w owns 16 query rows (w % 4) and the key tiles of
-// parity w / 4; each half runs its own online softmax and the halves are
-// combined at the end, so a query tile's key range is walked two tiles at a
-// time.  Scores are formed
+// written.  8 waves: with BQ = 64, wave w owns 16 query rows (w % 4) and the
+// key tiles of parity w / 4; with BQ = 32 (launches too short to fill the
+// chip), wave w owns query rows (w % 2) and the key tiles t with
+// t % 4 == w / 2.  Each key partition runs its own online softmax and the
+// partitions are combined at the end in partition order, so a query tile's
+// key range is walked KP tiles at a time.  Scores are formed
 // transposed, S^T = K Q^T (kv rows x q columns), so that a lane's
 // accumulator entries all belong to one query (q = lane % 16): the softmax
 // row statistics stay per lane, and the probabilities already sit in the
@@ -27,12 +29,15 @@
 namespace svl {
 namespace {
 
-constexpr int BQ = ATTN_BQ, BKV = 64, NT = 512;
+constexpr int BKV = 64, NT = 512;
 constexpr int GT = 4;   // key tiles loaded together (one LDS buffer each)
 constexpr float NEG_BIG = -1.0e30f;
 
-template <int D, bool F16>
+template <int D, bool F16, int BQ>
 __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
+  constexpr int QG = BQ / 16;    // 16-row query groups
+  constexpr int KP = 8 / QG;     // key partitions
+  static_assert(BQ == 64 || BQ == 32, "query tile of 64 or 32 rows");
   constexpr int KS = D + 8;      // K tile row stride (elements)
   // transposed V tile row stride (elements): 160 bytes, so the 8-byte fragment
   // reads of 16 rows x 4 lane groups hit distinct banks
@@ -52,8 +57,8 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
   const int kvh = h / (a.n_heads / a.n_kv_heads);
   const int S = g.S, q0 = qt * BQ;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int qw = wave & 3;       // 16-row query group
-  const int half = wave >> 2;    // key tiles of parity `half`
+  const int qw = wave % QG;      // 16-row query group
+  const int part = wave / QG;    // key tiles t with t % KP == part
   const int gq = lane >> 4, lq = lane & 15;
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
   const size_t ldq = (size_t)a.ldq;
@@ -153,7 +158,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
     for (int j = 0; j < GT; ++j) {
     const int kv0 = g0 + j * BKV;
     if (kv0 >= kv_end) break;
-    if (((kv0 / BKV) & 1) != half) continue;   // the other half's tile
+    if ((kv0 / BKV) % KP != part) continue;   // another partition's tile
     const uint16_t* Kt = Ks[j];
     const uint16_t* Vtt = Vt[j];
     // S^T = K Q^T for the four 16-row kv blocks.
@@ -187,7 +192,7 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        // masked keys contribute exactly 0 (a half may see only masked keys)
+        // masked keys contribute exactly 0 (a partition may see only masked keys)
         const float p = st[i][r] > 0.5f * NEG_BIG ? exp2f(st[i][r] - m_new) : 0.f;
         st[i][r] = p;
         lsum += p;
@@ -215,31 +220,44 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
     }
   }
 
-  // Combine the two halves: the odd-tile waves hand (m, l, o) to the even
-  // ones through LDS (the K buffers, free after the barrier).
+  // Combine the partitions: partitions 1 .. KP-1 hand (m, l, o) to
+  // partition 0 through LDS (the K buffers, free after the barrier), which
+  // adds them in partition order.
   constexpr int CW = 2 + 4 * NB;   // floats per lane
-  static_assert(4 * 64 * CW * 4 <= (int)sizeof(Ks), "combine buffer");
-  float* comb = reinterpret_cast<float*>(&Ks[0][0]) + (qw * 64 + lane) * CW;
+  static_assert((KP - 1) * QG * 64 * CW * 4 <= (int)sizeof(Ks), "combine buffer");
+  float* comb = reinterpret_cast<float*>(&Ks[0][0]);
   __syncthreads();
-  if (half == 1) {
-    comb[0] = m_i;
-    comb[1] = l_i;
+  if (part > 0) {
+    float* c = comb + (((part - 1) * QG + qw) * 64 + lane) * CW;
+    c[0] = m_i;
+    c[1] = l_i;
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) comb[2 + 4 * b + r] = o[b][r];
+      for (int r = 0; r < 4; ++r) c[2 + 4 * b + r] = o[b][r];
   }
   __syncthreads();
-  if (half == 1) return;
+  if (part > 0) return;
   {
-    const float m1 = comb[0], l1 = comb[1];
-    const float m = fmaxf(m_i, m1);
-    const float a0 = exp2f(m_i - m), a1 = exp2f(m1 - m);
-    l_i = l_i * a0 + l1 * a1;
+    float m = m_i;
+#pragma unroll
+    for (int p = 1; p < KP; ++p) m = fmaxf(m, comb[((p - 1) * QG + qw) * 64 * CW + lane * CW]);
+    const float a0 = exp2f(m_i - m);
+    l_i *= a0;
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o[b][r] = o[b][r] * a0 + comb[2 + 4 * b + r] * a1;
+      for (int r = 0; r < 4; ++r) o[b][r] *= a0;
+#pragma unroll
+    for (int p = 1; p < KP; ++p) {
+      const float* c = comb + (((p - 1) * QG + qw) * 64 + lane) * CW;
+      const float ap = exp2f(c[0] - m);
+      l_i += c[1] * ap;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[b][r] += c[2 + 4 * b + r] * ap;
+    }
   }
   l_i += __shfl_xor(l_i, 16, 64);
   l_i += __shfl_xor(l_i, 32, 64);
@@ -262,12 +280,24 @@ __global__ __launch_bounds__(NT) void attn_mfma_kernel(AttnArgs a) {
 
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st) {
   if (a.ntiles <= 0) return hipSuccess;
+  if (a.bq != 64 && a.bq != 32) return hipErrorInvalidValue;
+  const bool s32 = a.bq == 32;
   if (head_dim == 128) {
-    if (f16) attn_mfma_kernel<128, true><<<a.ntiles, NT, 0, st>>>(a);
-    else attn_mfma_kernel<128, false><<<a.ntiles, NT, 0, st>>>(a);
+    if (s32) {
+      if (f16) attn_mfma_kernel<128, true, 32><<<a.ntiles, NT, 0, st>>>(a);
+      else attn_mfma_kernel<128, false, 32><<<a.ntiles, NT, 0, st>>>(a);
+    } else {
+      if (f16) attn_mfma_kernel<128, true, 64><<<a.ntiles, NT, 0, st>>>(a);
+      else attn_mfma_kernel<128, false, 64><<<a.ntiles, NT, 0, st>>>(a);
+    }
   } else if (head_dim == 64) {
-    if (f16) attn_mfma_kernel<64, true><<<a.ntiles, NT, 0, st>>>(a);
-    else attn_mfma_kernel<64, false><<<a.ntiles, NT, 0, st>>>(a);
+    if (s32) {
+      if (f16) attn_mfma_kernel<64, true, 32><<<a.ntiles, NT, 0, st>>>(a);
+      else attn_mfma_kernel<64, false, 32><<<a.ntiles, NT, 0, st>>>(a);
+    } else {
+      if (f16) attn_mfma_kernel<64, true, 64><<<a.ntiles, NT, 0, st>>>(a);
+      else attn_mfma_kernel<64, false, 64><<<a.ntiles, NT, 0, st>>>(a);
+    }
   } else {
     return hipErrorInvalidValue;
   }

@@ -487,6 +487,18 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
       LP.qkv = qkv.finish(w, BM, F32_BN, F32_BN, 1);
       LP.o = o.finish(w, BM, F32_BN, F32_BN, 1);
     }
+    // 16-bit prefill attention: 32-row query tiles when 64-row tiles would
+    // leave CUs idle (each workgroup then also splits its key range four
+    // ways instead of two, so the longest tile's critical path halves)
+    if (mfma && !rowvec && attn_tiles < kTargetTiles) {
+      attn_tiles = 0;
+      for (AttnGroup& g : ag) {
+        g.nqt = cdiv(g.S, ATTN_BQ_SHORT);
+        g.tile0 = attn_tiles;
+        attn_tiles += g.nqt * g.h_cnt;
+      }
+      LP.attn.bq = ATTN_BQ_SHORT;
+    }
     LP.attn.groups_off = w.append(ag);
     LP.attn.heads_off = w.append(heads);
     LP.attn.kvheads_off = w.append(kvheads);

@@ -30,6 +30,7 @@ struct AttnLaunch {
   int64_t groups_off = 0, heads_off = 0, kvheads_off = 0;
   int32_t ngroups = 0, ntiles = 0;
   int32_t max_kv_cnt = 0;   // most active K/V heads of a group (cache append grid)
+  int32_t bq = ATTN_BQ;     // query rows per workgroup (ATTN_BQ or ATTN_BQ_SHORT)
 };
 
 // A residual / RMSNorm launch: adds pending split-K partials (nsplit slices)

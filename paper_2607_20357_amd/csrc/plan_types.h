@@ -127,6 +127,7 @@ constexpr int MFMA_PARTIAL_ROWS = 4096;   // split pieces x rows the partial buf
 constexpr int F32_BM = 64, F32_BN = 64, F32_BK = 16;
 constexpr int F32_SWIGLU_CH = 32;
 constexpr int ATTN_BQ = 64;          // query rows per attention workgroup
+constexpr int ATTN_BQ_SHORT = 32;    // 16-bit path, launches too short to fill the chip
 
 // Fragment-packed activation layout (16-bit MFMA path).  A matrix with K
 // columns (K % 64 == 0) is stored as blocks of 16 rows x 64 columns, 2 KB

@@ -96,6 +96,7 @@ struct AttnArgs {
   int32_t max_len;
   const int32_t* kvhead_table;
   int32_t max_kv_cnt;
+  int32_t bq;          // query rows per workgroup of the 16-bit prefill attention
 };
 
 constexpr int NORM_INLINE_SEGS = 8;
