@@ -147,9 +147,11 @@ def measured_traffic():
 
 
 def gemm_bytes(shape, seqlens, layer_mask, head_mask, ffn_mask):
-    """Algorithmic HBM bytes of each GEMM class over one step: active weight
-    bytes + activation operand + output, bf16 (2 B) activations/weights and
-    float32 residual read-modify-write for the output / down projections."""
+    """Algorithmic HBM bytes of each GEMM class over one step: the weights of
+    the union of the samples' active heads / K-V heads / FFN slices (each
+    weight block read once; the headline has one sample), the activation
+    operand and the output, bf16 (2 B) activations / weights and float32
+    residual read-modify-write for the output / down projections."""
     D, A, KV, d, F, G = (shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                          shape.d_ffn, shape.n_groups)
     rep = A // KV
@@ -158,31 +160,39 @@ def gemm_bytes(shape, seqlens, layer_mask, head_mask, ffn_mask):
     B, L = layer_mask.shape
     for l in range(L):
         rows_a = rows_f = 0
-        qkv_cols = o_k = f_ch = 0
+        act_qkv = act_o = act_gu = act_down = 0
+        heads = np.zeros(A, bool)
+        kvs = np.zeros(KV, bool)
+        chans = np.zeros(G, bool)
         for b in range(B):
             if not layer_mask[b, l] or seqlens[b] == 0:
                 continue
-            hm = head_mask[b, l]
+            hm = head_mask[b, l].astype(bool)
             H = int(hm.sum())
-            K = sum(int(hm[g * rep:(g + 1) * rep].any()) for g in range(KV))
-            C = F if ffn_mask is None else int(ffn_mask[b, l].sum()) * (F // G)
+            kv = np.array([hm[g * rep:(g + 1) * rep].any() for g in range(KV)])
+            fm = np.ones(G, bool) if ffn_mask is None else ffn_mask[b, l].astype(bool)
+            C = int(fm.sum()) * (F // G)
+            S = int(seqlens[b])
             if H:
-                rows_a += seqlens[b]
-                # weights read once per launch when every sample shares the
-                # mask (the headline case); per sample otherwise
-                qkv_cols = max(qkv_cols, (H + 2 * K) * d)
-                o_k = max(o_k, H * d)
+                rows_a += S
+                heads |= hm
+                kvs |= kv
+                act_qkv += S * D * 2 + S * (H + 2 * int(kv.sum())) * d * 2
+                act_o += S * H * d * 2 + S * D * 8
             if C:
-                rows_f += seqlens[b]
-                f_ch = max(f_ch, C)
+                rows_f += S
+                chans |= fm
+                act_gu += S * D * 2 + S * C * 2
+                act_down += S * C * 2 + S * D * 8
         if rows_a:
-            out["qkv"] += qkv_cols * D * 2 + rows_a * D * 2 + rows_a * qkv_cols * 2
-            out["o"] += D * o_k * 2 + rows_a * o_k * 2 + rows_a * D * 8
+            out["qkv"] += (int(heads.sum()) + 2 * int(kvs.sum())) * d * D * 2 + act_qkv
+            out["o"] += D * int(heads.sum()) * d * 2 + act_o
             launches["qkv"] += 1
             launches["o"] += 1
         if rows_f:
-            out["gu"] += 2 * f_ch * D * 2 + rows_f * D * 2 + rows_f * f_ch * 2
-            out["down"] += D * f_ch * 2 + rows_f * f_ch * 2 + rows_f * D * 8
+            cu = int(chans.sum()) * (F // G)
+            out["gu"] += 2 * cu * D * 2 + act_gu
+            out["down"] += D * cu * 2 + act_down
             launches["gu"] += 1
             launches["down"] += 1
     return out, launches
@@ -486,7 +496,10 @@ def decode_bench(args):
         "step_hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "per_kernel": per_kernel,
         "roofline": {
-            "kernel": "gemv_kernel<EPI_SWIGLU> (gate/up row-vector products + SwiGLU, one row per sample)",
+            "kernel": ("gemv_kernel<EPI_SWIGLU> (gate/up row-vector products + SwiGLU, one row per "
+                       "sample)" if B == 1 else
+                       "gemv_mfma_shared_kernel<EPI_SWIGLU> (gate/up: each weight block once for "
+                       "every sample using it, MFMA over the samples' rows, + SwiGLU)"),
             "bound": "hbm", "achieved": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gu_bytes / (gu_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -27,7 +27,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC",
           # no packed-fp32 instructions anywhere in the device code
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-Wall", "-Wno-unused-result", f"-I{os.path.join(ROOT, 'include')}"]
+          # a function that can fall off its end without a value is an error
+          "-Wall", "-Wno-unused-result", "-Werror=return-type",
+          f"-I{os.path.join(ROOT, 'include')}"]
 
 
 def _compile(src: str) -> str:

@@ -205,9 +205,19 @@ struct Exec {
     a.partial = reinterpret_cast<float*>(ws + L.partial);
     const bool f16 = c.compute == SVL_COMPUTE_F16;
     if (decode) {
-      // one row per sample: row-vector products over the groups' blocks
+      // one row per sample: row-vector products over the groups' blocks, or
+      // over the shared segments (a batch: each weight block read once for
+      // all samples using it)
       a.ngroups = g.ngroups;
       a.nblocks = g.nblocks;
+      if (g.nsegs > 0) {
+        a.segs = at<DecSeg>(g.segs_off);
+        a.nsegs = g.nsegs;
+        a.uses = at<DecUse>(g.uses_off);
+        a.cmasks = at<int32_t>(g.cmasks_off);
+        a.max_uses = g.max_uses;
+        return timed(cls, st, [&] { return launch_gemv_shared(a, epi, f16, st); });
+      }
       return timed(cls, st, [&] { return launch_gemv(a, epi, f16, st); });
     }
     const bool paired = epi == EPI_QKV || epi == EPI_SWIGLU;

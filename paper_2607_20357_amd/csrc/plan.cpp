@@ -267,6 +267,62 @@ void push_chunks(std::vector<KChunk>& ch, int32_t a, int32_t b, int32_t bk) {
   for (int32_t k = a; k < b; k += bk) ch.push_back({k, std::min(bk, b - k)});
 }
 
+// Shared row-vector launch of one layer's GEMM (decode of a batch):
+// segments of weight blocks with the samples that use them.
+struct DecBuild {
+  std::vector<DecSeg> segs;
+  std::vector<DecUse> uses;
+  std::vector<int32_t> masks;
+  int32_t nblocks = 0, max_uses = 0;
+  // One segment per group of at most DEC_MAX_USES samples; `masks_of(c)`
+  // gives chunk c's use mask for the group's samples (empty: every use).
+  void add(int32_t nblk, int32_t wsel, int32_t wrow0, int32_t ocol0, int32_t rope,
+           const std::vector<int32_t>& samples, const std::vector<int32_t>& arow,
+           const std::vector<int32_t>& orow, const int32_t* pos, int32_t kc_off, int32_t kc_cnt,
+           int32_t kdense, const std::vector<int32_t>* per_sample_chunk_on = nullptr,
+           int32_t nchunks_all = 0, std::vector<KChunk>* chunks = nullptr) {
+    for (size_t s0 = 0; s0 < samples.size(); s0 += DEC_MAX_USES) {
+      const size_t s1 = std::min(samples.size(), s0 + DEC_MAX_USES);
+      DecSeg g{};
+      g.blk0 = nblocks; g.nblk = nblk; g.wsel = wsel; g.wrow0 = wrow0; g.ocol0 = ocol0;
+      g.rope = rope; g.nuse = (int32_t)(s1 - s0); g.use_off = (int32_t)uses.size();
+      g.kc_off = kc_off; g.kc_cnt = kc_cnt; g.kdense = kdense; g.mask_off = -1;
+      for (size_t i = s0; i < s1; ++i) {
+        const int32_t b = samples[i];
+        uses.push_back({arow[b], orow[b], pos ? pos[b] : 0, 0});
+      }
+      if (per_sample_chunk_on) {
+        // the union of the group's active chunks, each with its use mask
+        g.kc_off = (int32_t)chunks->size();
+        g.mask_off = (int32_t)masks.size();
+        g.kdense = -1;
+        for (int32_t c = 0; c < nchunks_all; ++c) {
+          int32_t mk = 0;
+          for (size_t i = s0; i < s1; ++i)
+            if ((*per_sample_chunk_on)[(size_t)samples[i] * nchunks_all + c]) mk |= 1 << (i - s0);
+          if (!mk) continue;
+          chunks->push_back({c * MFMA_BK, MFMA_BK});
+          masks.push_back(mk);
+        }
+        g.kc_cnt = (int32_t)chunks->size() - g.kc_off;
+        if (g.kc_cnt == 0) continue;
+      }
+      segs.push_back(g);
+      nblocks += nblk;
+      max_uses = std::max(max_uses, g.nuse);
+    }
+  }
+  void finish(ImageWriter& w, GemmLaunch& L) {
+    if (segs.empty()) return;
+    L.segs_off = w.append(segs);
+    L.uses_off = w.append(uses);
+    L.cmasks_off = w.append(masks);
+    L.nsegs = (int32_t)segs.size();
+    L.nblocks = nblocks;
+    L.max_uses = max_uses;
+  }
+};
+
 }  // namespace
 
 int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t R, int32_t nlayers) {
@@ -303,6 +359,15 @@ int64_t plan_bytes_bound(const svl_config& c, int32_t B, int32_t R, int32_t nlay
   int64_t chunks = (D + bk - 1) / bk + B * A * ((d + bk - 1) / bk) +
                    B * G * ((F / G + bk - 1) / bk);
   per_layer += chunks * (int64_t)sizeof(KChunk) + 16;
+  // shared row-vector segments (decode of a batch): at most one segment per
+  // (head, K/V head, FFN slice or projection) and group of DEC_MAX_USES
+  // samples, one use per sample in each, and the output / down projections'
+  // union chunk lists with their use masks
+  const int64_t ngrp = (B + DEC_MAX_USES - 1) / DEC_MAX_USES;
+  const int64_t nseg = (A + 2 * KV + G + 2) * ngrp;
+  const int64_t nuch = 2 * ngrp * ((A * d + F) / bk + 2);
+  per_layer += nseg * (int64_t)sizeof(DecSeg) + (A + 2 * KV + G + 2) * B * (int64_t)sizeof(DecUse) +
+               nuch * (int64_t)(sizeof(KChunk) + 4) + 64;
   return 64 + (int64_t)B * 4 + (int64_t)(B + 1) * 4 + 32 + B * (int64_t)sizeof(NormSeg) + 16 +
          per_layer * nlayers;
 }
@@ -519,6 +584,97 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     } else {
       LP.gu = gu.finish(w, BM, F32_SWIGLU_CH, F32_BN, 1);
       LP.down = down.finish(w, BM, F32_BN, F32_BN, 1);
+    }
+    if (mfma && rowvec && B > 1) {
+      // decode of a batch: each weight block once for every sample using it
+      DecBuild dq, dout, dgu, ddown;
+      std::vector<uint8_t> on_h((size_t)B * std::max(A, KV));
+      struct Sec { int32_t wsel, n, col0; bool kv; };
+      const Sec secs[3] = {{0, A, 0, false}, {1, KV, A * d, true}, {2, KV, (A + KV) * d, true}};
+      for (const Sec& sc : secs) {
+        for (int32_t b = 0; b < B; ++b) {
+          const uint8_t* hm = m.head_mask + b * m.head_stride;
+          for (int32_t h = 0; h < sc.n; ++h) {
+            uint8_t v = 0;
+            if (run_attn[b]) {
+              if (!sc.kv) v = hm[h];
+              else for (int32_t q = h * rep; q < (h + 1) * rep; ++q) v |= hm[q];
+            }
+            on_h[(size_t)b * sc.n + h] = v;
+          }
+        }
+        // runs of consecutive heads used by the same samples
+        int32_t h0 = 0;
+        while (h0 < sc.n) {
+          std::vector<int32_t> smp;
+          for (int32_t b = 0; b < B; ++b) if (on_h[(size_t)b * sc.n + h0]) smp.push_back(b);
+          int32_t h1 = h0 + 1;
+          while (h1 < sc.n) {
+            bool same = true;
+            for (int32_t b = 0; b < B && same; ++b)
+              same = on_h[(size_t)b * sc.n + h1] == on_h[(size_t)b * sc.n + h0];
+            if (!same) break;
+            ++h1;
+          }
+          if (!smp.empty())
+            dq.add((h1 - h0) * (d / 16), sc.wsel, h0 * d, sc.col0 + h0 * d, sc.wsel < 2 ? 1 : 0, smp,
+                   pcu, pcu, pos_base, 0, dense_cnt, 0);
+          h0 = h1;
+        }
+      }
+      // FFN slices
+      {
+        std::vector<uint8_t> on_j((size_t)B * G);
+        for (int32_t b = 0; b < B; ++b) {
+          const uint8_t* fm = m.ffn_mask ? m.ffn_mask + b * m.ffn_stride : nullptr;
+          for (int32_t j = 0; j < G; ++j) on_j[(size_t)b * G + j] = run_ffn[b] && (!fm || fm[j]);
+        }
+        int32_t j0 = 0;
+        while (j0 < G) {
+          std::vector<int32_t> smp;
+          for (int32_t b = 0; b < B; ++b) if (on_j[(size_t)b * G + j0]) smp.push_back(b);
+          int32_t j1 = j0 + 1;
+          while (j1 < G) {
+            bool same = true;
+            for (int32_t b = 0; b < B && same; ++b) same = on_j[(size_t)b * G + j1] == on_j[(size_t)b * G + j0];
+            if (!same) break;
+            ++j1;
+          }
+          if (!smp.empty())
+            dgu.add((j1 - j0) * slice / 8, 0, j0 * slice, j0 * slice, 0, smp, pcu, pcu, nullptr, 0,
+                    dense_cnt, 0);
+          j0 = j1;
+        }
+        // down projection: the union of the samples' active slices' chunks
+        const int32_t fc = F / bk;
+        std::vector<int32_t> chon((size_t)B * fc, 0);
+        std::vector<int32_t> smp;
+        for (int32_t b = 0; b < B; ++b) {
+          if (!run_ffn[b]) continue;
+          smp.push_back(b);
+          for (int32_t c = 0; c < fc; ++c) chon[(size_t)b * fc + c] = on_j[(size_t)b * G + (c * bk) / slice];
+        }
+        if (!smp.empty())
+          ddown.add(D / 16, 0, 0, 0, 0, smp, pcu, cu, nullptr, 0, 0, -1, &chon, fc, &chunks);
+      }
+      // output projection: the union of the samples' active heads' chunks
+      {
+        const int32_t oc = A * d / bk;
+        std::vector<int32_t> chon((size_t)B * oc, 0);
+        std::vector<int32_t> smp;
+        for (int32_t b = 0; b < B; ++b) {
+          if (!run_attn[b]) continue;
+          smp.push_back(b);
+          const uint8_t* hm = m.head_mask + b * m.head_stride;
+          for (int32_t c = 0; c < oc; ++c) chon[(size_t)b * oc + c] = hm[(c * bk) / d];
+        }
+        if (!smp.empty())
+          dout.add(D / 16, 0, 0, 0, 0, smp, pcu, cu, nullptr, 0, 0, -1, &chon, oc, &chunks);
+      }
+      dq.finish(w, LP.qkv);
+      dout.finish(w, LP.o);
+      dgu.finish(w, LP.gu);
+      ddown.finish(w, LP.down);
     }
     LP.chunks_off = w.append(chunks);
   }

@@ -23,7 +23,11 @@ struct GemmLaunch {
   int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
   int32_t nitems = 0;       // split QKV / gate-up launches: finish kernel work items
   int32_t nblocks = 0;      // 16-bit path: the groups' 16-column blocks (each group's
-                            // first block in MmGroup::pad0)
+                            // first block in MmGroup::pad0); shared row-vector
+                            // launches: the segments' blocks
+  // shared row-vector launch (decode of a batch), nsegs > 0
+  int64_t segs_off = 0, uses_off = 0, cmasks_off = 0;
+  int32_t nsegs = 0, max_uses = 0;
 };
 
 struct AttnLaunch {

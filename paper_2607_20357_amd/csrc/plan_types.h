@@ -96,6 +96,29 @@ struct MmTile {
 };
 static_assert(sizeof(MmTile) == 64, "one 64-byte record per workgroup");
 
+// Decode row-vector launches of a batch: a segment is a run of 16-column
+// weight blocks (same block layout as the groups: QKV blocks pair rotary
+// dims, gate/up blocks pair gate and up channels) together with the samples
+// (uses) whose masks include those blocks, so each weight block is streamed
+// once for all of them.  Output / down projection segments multiply the
+// union of their samples' active K chunks; a chunk's use mask says which
+// samples it belongs to.
+constexpr int DEC_MAX_USES = 8;
+struct DecUse {
+  int32_t arow;     // the sample's activation row
+  int32_t orow;     // its output row (activation row, or residual row for RESID)
+  int32_t pos;      // RoPE position of its new token
+  int32_t pad;
+};
+struct DecSeg {
+  int32_t blk0, nblk;          // launch blocks [blk0, blk0 + nblk)
+  int32_t wsel, wrow0, ocol0, rope;   // as in MmGroup
+  int32_t nuse, use_off;       // uses [use_off, use_off + nuse) of the use table
+  int32_t kc_off, kc_cnt;      // K chunks (the layer's chunk table)
+  int32_t kdense;              // >= 0: chunk c starts at kdense + 64 c
+  int32_t mask_off;            // >= 0: per-chunk use masks (bit u: use u); -1: every use
+};
+
 // One sample of an attention launch: one workgroup per (active head, q tile).
 // With a KV cache, the sample's rows are positions pos_base .. pos_base+S-1
 // of its cached sequence (prefill: pos_base = 0; decode: S = 1 new row).

@@ -63,6 +63,11 @@ struct MmArgs {
   int32_t pld;
   int32_t ngroups;       // row-vector launches (decode): groups, and the blocks
   int32_t nblocks;       // of all groups (a group's first block in its pad0)
+  const DecSeg* segs;    // shared row-vector launches (decode of a batch): segments,
+  int32_t nsegs;         // their uses and per-chunk use masks; nblocks counts
+  const DecUse* uses;    // the segments' blocks
+  const int32_t* cmasks;
+  int32_t max_uses;      // most uses of a segment
 };
 
 // Finish of a split QKV / gate-up launch: sums the split slices in order,
@@ -186,6 +191,7 @@ hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st
 hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st);
 hipError_t launch_finish(const FinishArgs& a, int32_t epi, bool f16, hipStream_t st);
 // Decode: one-row groups, one workgroup per 16-column block (QKV, SWIGLU, RESID).
+hipError_t launch_gemv_shared(const MmArgs& a, int32_t epi, bool f16, hipStream_t st);
 hipError_t launch_gemv(const MmArgs& a, int32_t epi, bool f16, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int32_t epi, hipStream_t st);
 hipError_t launch_attn_mfma(const AttnArgs& a, int32_t head_dim, bool f16, hipStream_t st);

@@ -94,6 +94,21 @@ def test_decode_gqa():
     assert max(errs) <= tol_for(w.shape), errs
 
 
+def test_decode_batch_past_eight_uses():
+    """A batch of 11 samples: the shared row-vector launches split each
+    weight block's samples into groups of at most 8 (8 + 3), with heads of
+    64 columns (one K chunk per head), grouped K/V heads and per-sample head
+    groups, FFN slices and skipped layers."""
+    import dataclasses
+    base = W.scaled(W.get_workload("llava7b_b8_ragged"), n_layers=3, d_model=512,
+                    d_ffn=1024, batch=11, n_vision=96, n_text=16, name="dec11")
+    w = dataclasses.replace(base, shape=dataclasses.replace(base.shape, n_heads=8, n_kv_heads=4,
+                                                            head_dim=64))
+    errs = _decode_case(w, 9, steps=2)
+    print(f"max rel err over rows: {max(errs):.2e}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+
+
 def test_decode_headline_full_size():
     """The headline shape (32 layers, d 4096, one sample, 144 + 64 tokens),
     two decode steps."""
