@@ -203,6 +203,7 @@ struct Exec {
     a.rope = reinterpret_cast<const float2*>(ws + L.rope);
     a.head_dim = c.head_dim;
     a.partial = reinterpret_cast<float*>(ws + L.partial);
+    a.rowpos = at<int32_t>(plan.rowpos_off);
     const bool f16 = c.compute == SVL_COMPUTE_F16;
     if (decode) {
       // one row per sample: row-vector products over the groups' blocks, or

@@ -14,6 +14,10 @@
 // gate/up: a run of active FFN slices; output / down projections: all
 // columns, with K restricted to the active heads' / slices' columns), so
 // weight rows and columns of inactive heads and FFN slices are never read.
+// In a batch, a QKV or gate/up group covers a run of consecutive samples
+// that all use its heads or slices (their padded rows are contiguous; the
+// padding rows between them compute values nobody reads), and its RoPE
+// positions come from a per-row table.
 // A tile is up to 256 rows of a group times nblk <= NB 16-column blocks
 // times a range of K chunks; the planner balances the block counts so a
 // launch has about one tile per CU (every tile streams the whole activation
@@ -372,7 +376,8 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int pos = tl.pos0 + min(rbase + 16 * i + r, mcnt - 1);
+            const int rr = min(rbase + 16 * i + r, mcnt - 1);
+            const int pos = tl.pos0 >= 0 ? tl.pos0 + rr : a.rowpos[tl.arow + rr];
 #pragma unroll
             for (int j = 0; j < NB; ++j) {
               const int gb = tl.b0 + min(j, nblk - 1);

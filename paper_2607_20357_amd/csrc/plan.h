@@ -64,6 +64,9 @@ struct Plan {
   std::vector<LayerPlan> layers;
   NormLaunch final_norm;          // adds the last layer's pending partials
   int64_t keep_off = 0, cu_off = 0;
+  // per activation row (padded space): its RoPE position inside its sample
+  // (padding rows: 0), read by QKV tiles that span several samples
+  int64_t rowpos_off = 0;
   int32_t max_seq = 0;            // most rows of one sample in this call
   int32_t max_pos = 0;            // positions the RoPE table covers: max of pos_base + rows
   int32_t padded_rows = 0;        // rows of the activation buffers

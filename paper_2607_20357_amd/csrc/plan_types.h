@@ -83,7 +83,8 @@ struct MmTile {
   int32_t arow;     // first packed row of A: group arow0 + m0 (multiple of 16)
   int32_t orow;     // first output row: group orow0 + m0
   int32_t mcnt;     // rows of the tile (1 .. 256)
-  int32_t pos0;     // position in the sample of the first row: m0 (RoPE)
+  int32_t pos0;     // position in the sample of the first row: m0 (RoPE); -1:
+                    // the rows span several samples (per-row position table)
   int32_t wsel, wrow0, ocol0, rope;   // as in the group
   int32_t chunk0;   // first entry of the tile's K chunks in the chunk table
   int32_t kcn;      // K chunks

@@ -68,6 +68,8 @@ struct MmArgs {
   const DecUse* uses;    // the segments' blocks
   const int32_t* cmasks;
   int32_t max_uses;      // most uses of a segment
+  const int32_t* rowpos; // per activation row: RoPE position in its sample (QKV
+                         // tiles spanning samples: pos0 < 0)
 };
 
 // Finish of a split QKV / gate-up launch: sums the split slices in order,
