@@ -447,8 +447,15 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
 
   // A residual / norm launch over the samples that are pending or run the
   // next sub-block (run[b] != 0).
-  auto norm_launch = [&](const std::vector<uint8_t>& run) {
+  // A sub-block that no sample runs launches nothing: split-K partials still
+  // pending (from the last output / down projection) stay in their slices,
+  // untouched until the next sub-block a sample runs, whose norm adds them
+  // (`final`: the closing add-only launch after the last layer).
+  auto norm_launch = [&](const std::vector<uint8_t>& run, bool final = false) {
     NormLaunch L;
+    bool any = final;
+    for (int32_t b = 0; b < B && !any; ++b) any = run[b] && seqlens[b] > 0;
+    if (!any) return L;
     std::vector<NormSeg> segs;
     int32_t prefix = 0, gprefix = 0;
     for (int32_t b = 0; b < B; ++b) {
@@ -759,7 +766,7 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     LP.chunks_off = w.append(chunks);
   }
   std::vector<uint8_t> none(B, 0);
-  plan->final_norm = norm_launch(none);
+  plan->final_norm = norm_launch(none, true);
   return true;
 }
 
