@@ -81,13 +81,19 @@ def parse():
 
 COPY_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_traffic.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2607_20357_amd", "csrc", "gemm_mfma.hip")
+# the gate/up kernel's source and the headers it includes
+GEMM_SOURCE = [os.path.join(ROOT, "paper_2607_20357_amd", "csrc", n)
+               for n in ("gemm_mfma.hip", "device_util.h", "svl_internal.h", "plan_types.h")]
+GEMM_SOURCE.append(os.path.join(ROOT, "include", "svl.h"))
 
 
-def source_hash(path):
+def source_hash(paths):
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def write_traffic(run_dir):

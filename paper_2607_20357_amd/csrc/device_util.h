@@ -80,7 +80,14 @@ __device__ __forceinline__ float act_bits_to_f32(uint32_t h) {
 
 template <bool F16>
 __device__ __forceinline__ uint32_t pack_act2(float lo, float hi) {
-  return (uint32_t)f32_to_act_bits<F16>(lo) | ((uint32_t)f32_to_act_bits<F16>(hi) << 16);
+  if constexpr (F16) {
+    // one packed conversion, rounding to nearest even as the scalar one does
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, f16x2_t));
+  } else {
+    return (uint32_t)f32_to_act_bits<false>(lo) | ((uint32_t)f32_to_act_bits<false>(hi) << 16);
+  }
 }
 
 // Two bf16 values (one 32-bit word) -> the same two values as fp16.  Exact
