@@ -232,7 +232,7 @@ struct Exec {
       a.pld = ldo;
       a.pslice = L.partial_slice;
     }
-    hipError_t e = timed(cls, st, [&] { return launch_gemm_mfma(a, epi, g.nb, f16, st); });
+    hipError_t e = timed(cls, st, [&] { return launch_gemm_mfma(a, epi, g.nb, g.waves, f16, st); });
     if (e != hipSuccess || !(paired && g.nsplit > 1)) return e;
     FinishArgs f{};
     f.groups = a.groups;

@@ -24,16 +24,18 @@
 // slice it multiplies, so a launch with fewer, wider tiles reads less).
 //
 // Workgroup: 512 threads = 8 waves, wave w owning tile rows 32w .. 32w+31
-// (two 16-row MFMA blocks) and all blocks of the tile.  K advances in
+// (two 16-row MFMA blocks) and all blocks of the tile; or, for launches
+// with more tiles than CUs (the output / down projections), 256 threads =
+// 4 waves of four 16-row blocks each, two workgroups per CU.  K advances in
 // chunks of 64.  Per chunk:
 //   * each wave loads its own A fragments straight from the packed layout
 //     into registers (two 1 KB contiguous loads per 16-row block);
 //   * the tile's weight rows are loaded cooperatively (16 bytes per thread
-//     and row segment) and staged through LDS, where all eight waves read
-//     them.
+//     and row segment) and staged through LDS, where all waves read them.
 // The weights are staged KS = 4 chunks at a time (one barrier per stage,
 // so the waves drift freely inside a stage), double-buffered in LDS with one
-// or two further stages in flight in registers; A runs KS chunks ahead.
+// or two further stages in flight in registers; A runs 4 (8 waves) or 2
+// (4 waves) chunks ahead.
 // Loads are buffer loads whose range ends at the last valid row, so rows
 // past the tile read as zero.
 //
@@ -55,7 +57,7 @@
 namespace svl {
 namespace {
 
-constexpr int BM = MFMA_BM, NWAVE = 8, NT = NWAVE * 64;
+constexpr int BM = MFMA_BM;
 #ifndef SVL_GEMM_KS
 #define SVL_GEMM_KS 4
 #endif
@@ -65,8 +67,7 @@ constexpr int MAX_CHUNKS = 1024;               // K chunks per tile (K <= 65536)
 #ifndef SVL_GEMM_NSA
 #define SVL_GEMM_NSA KS
 #endif
-constexpr int NSA = SVL_GEMM_NSA;              // A chunks in flight (register slot = chunk % NSA)
-static_assert(KS % NSA == 0, "a stage holds whole rounds of A slots");
+constexpr int NSA8 = SVL_GEMM_NSA;             // A chunks in flight, 8-wave tiles
 
 // Raw buffer resource over [p, p + bytes): loads past the end return zero.
 // The inputs are wave-uniform; readfirstlane keeps the descriptor in scalar
@@ -110,8 +111,15 @@ __device__ __forceinline__ uint4 weight_to_act(const uint4& v) {
 template <int P>
 using Phase = std::integral_constant<int, P>;
 
-template <int EPI, int NB, bool F16>
-__global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
+// NWAVE waves per workgroup, each RB 16-row blocks of the tile: 8 x 2 (two
+// waves per SIMD), or 4 x 4 (one wave per SIMD; each LDS operand feeds twice
+// the MFMAs, the accumulators sit in the AGPRs, and two workgroups share a
+// CU: the output / down projections of launches with more tiles than CUs).
+template <int EPI, int NB, bool F16, int NWAVE>
+__global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
+  constexpr int NT = NWAVE * 64;
+  constexpr int RB = BM / (16 * NWAVE);         // 16-row blocks per wave
+  static_assert(RB * 16 * NWAVE == BM, "waves cover the tile's rows");
   constexpr int BN = NB * 16;                   // weight rows per tile
   // gate/up: weight loads of the next stage issued before the stage barrier
   // (measured 2.8 us faster per headline launch; the other epilogues' shapes
@@ -120,8 +128,10 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 #ifdef SVL_GEMM_NWS
   constexpr int NWS = SVL_GEMM_NWS;
 #else
-  constexpr int NWS = NB <= 6 ? 2 : 1;          // weight register stages
+  constexpr int NWS = NB <= (NWAVE == 8 ? 6 : 3) ? 2 : 1;   // weight register stages
 #endif
+  constexpr int NSA = NWAVE == 8 ? NSA8 : 2;    // A chunks in flight (register slot = chunk % NSA)
+  static_assert(KS % NSA == 0, "a stage holds whole rounds of A slots");
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
   __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
 
@@ -140,28 +150,29 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
 
   const int d = a.head_dim, hb = d >> 4;        // QKV: blocks per head
 
-  // A: packed blocks of this tile's rows; wave w reads 16-row blocks 2w, 2w+1.
+  // A: packed blocks of this tile's rows; wave w reads 16-row blocks RB w .. RB w + RB-1.
   const uint32_t kblocks = (uint32_t)(a.lda / 64);
   const uint32_t blk_bytes = kblocks * 2048u;   // one 16-row block over all of K
   const int rb0 = (tl.arow) / 16;
   const __amdgpu_buffer_rsrc_t rsA =
       make_rsrc(static_cast<const uint16_t*>(a.A) + (size_t)rb0 * kblocks * 1024,
                 (uint32_t)((mcnt + 15) / 16) * blk_bytes);
-  uint32_t voA[2];
+  uint32_t voA[RB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) voA[i] = (uint32_t)(2 * wave + i) * blk_bytes + lane * 16u;
-  bool rowblk[2];   // this wave's 16-row blocks hold rows of the tile (wave-uniform)
+  for (int i = 0; i < RB; ++i) voA[i] = (uint32_t)(RB * wave + i) * blk_bytes + lane * 16u;
+  bool rowblk[RB];   // this wave's 16-row blocks hold rows of the tile (wave-uniform)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) rowblk[i] = 32 * wave + 16 * i < mcnt;
+  for (int i = 0; i < RB; ++i) rowblk[i] = 16 * (RB * wave + i) < mcnt;
 
-  // Weights, one stage = KS chunks: piece p = tid + NT*s (s < NB) is unit
+  // Weights, one stage = KS chunks: piece p = tid + NT*s (s < WLD) is unit
   // p % 32 (chunk u / 8 of the stage, 16-byte segment u % 8) of tile row
   // p / 32 (block j = row/16, column i = row%16 of the block).  Half a wave
   // loads 512 bytes of one weight row; a wave's two rows share one column
   // half of a block (i < 8 or i >= 8), so the matrix choice is wave-uniform.
   static_assert(KS == 4 || KS == 8, "stage rows are 512 or 1024 bytes");
   constexpr int RU = KS * 8;                    // 16-byte units per stage row
-  constexpr int WLD = NB * KS / 4;              // BN * RU pieces / NT threads
+  constexpr int WLD = BN * RU / NT;             // BN * RU pieces / NT threads
+  static_assert(BN * RU % NT == 0, "whole weight pieces per thread");
   __amdgpu_buffer_rsrc_t rsB[WLD];
   uint32_t voB[WLD];
   const int wu = tid & (RU - 1), wqc = wu >> 3;   // this thread's unit and chunk of the stage
@@ -192,14 +203,14 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   __syncthreads();   // s_k0 ready
 
   const int last = nk - 1;
-  uint4 sa[NSA][2][2], sw[NWS][WLD];
+  uint4 sa[NSA][RB][2], sw[NWS][WLD];
   // A loads and MFMAs of the wave's NRB row blocks that hold rows of the
   // tile (the pipeline is instantiated per NRB, so a wave past the tile's
-  // rows issues no loads for them and the waits stay exact).  NRB < 0: both
+  // rows issues no loads for them and the waits stay exact).  NRB < 0: all RB
   // blocks are loaded (out-of-range rows read zero) and the MFMAs branch on
   // rowblk, which keeps the widest tiles within the registers.
-  auto loadA = [&](auto nrb, int c, uint4 (&ra)[2][2]) __attribute__((always_inline)) {
-    constexpr int NRB = decltype(nrb)::value < 0 ? 2 : decltype(nrb)::value;
+  auto loadA = [&](auto nrb, int c, uint4 (&ra)[RB][2]) __attribute__((always_inline)) {
+    constexpr int NRB = decltype(nrb)::value < 0 ? RB : decltype(nrb)::value;
     const uint32_t soA = (uint32_t)__builtin_amdgcn_readfirstlane(s_k0[c]) * 32u;
 #pragma unroll
     for (int i = 0; i < NRB; ++i) {
@@ -224,9 +235,9 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     }
   };
 
-  floatx4 acc[2][NB];
+  floatx4 acc[RB][NB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < RB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
@@ -236,9 +247,9 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   // swizzle of rows j*16 + lane%16 depends on lane%16 only
   const int fl = (2 * (lane >> 4)) ^ swz(lane & 15);
   const uint16_t* Bl = Bs + (lane & 15) * LDS_STRIDE;
-  auto compute = [&](auto nrb, int buf, int q, const uint4 (&ra)[2][2]) __attribute__((always_inline)) {
+  auto compute = [&](auto nrb, int buf, int q, const uint4 (&ra)[RB][2]) __attribute__((always_inline)) {
     constexpr bool DYN = decltype(nrb)::value < 0;
-    constexpr int NRB = DYN ? 2 : decltype(nrb)::value;
+    constexpr int NRB = DYN ? RB : decltype(nrb)::value;
     const uint16_t* B = Bl + buf * (BN * LDS_STRIDE);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -316,7 +327,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   };
   // every instantiation runs the same barrier sequence
   if (nk > 0) {
-    if constexpr (NB >= 8) {
+    if constexpr (NB >= 8 || NWAVE != 8) {
       pipeline(std::integral_constant<int, -1>{});
     } else {
       if (rowblk[1]) pipeline(std::integral_constant<int, 2>{});
@@ -325,9 +336,9 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     }
   }
 
-  // Epilogue.  acc[i][j][r] is C[32 wave + 16 i + 4 (lane/16) + r][16 j + lane%16]
+  // Epilogue.  acc[i][j][r] is C[16 RB wave + 16 i + 4 (lane/16) + r][16 j + lane%16]
   // of the tile; tile row m is row m0 + m of the group.
-  const int rbase = wave * 32 + (lane >> 4) * 4;
+  const int rbase = wave * 16 * RB + (lane >> 4) * 4;
   const int ci = lane & 15;           // column inside the block
   if constexpr (EPI == EPI_QKV || EPI == EPI_SWIGLU) {
     if (a.split > 1) {
@@ -335,7 +346,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       // at the gate / up column (SWIGLU); the finish kernel does the rest
       float* out = a.partial + (size_t)tl.slice * a.pslice;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rbase + 16 * i + r;
@@ -363,17 +374,17 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     // (SWIGLU rows are padded to an odd number of 16-byte pieces, so the
     // row-strided piece reads below hit distinct banks)
     constexpr int RW = EPI == EPI_QKV ? NB * 16 : (NB | 1) * 8;
-    static_assert(NWAVE * 32 * RW <= 2 * BN * LDS_STRIDE, "staging tiles fit the weight buffers");
-    uint16_t* E = Bs + wave * (32 * RW);
+    static_assert(NWAVE * 16 * RB * RW <= 2 * BN * LDS_STRIDE, "staging tiles fit the weight buffers");
+    uint16_t* E = Bs + wave * (16 * RB * RW);
     const int lr0 = (lane >> 4) * 4;    // wave-local row of acc[i][j][0] is lr0 + 16 i
     uint16_t* out = static_cast<uint16_t*>(a.out);
     if constexpr (EPI == EPI_QKV) {
       const int half = d >> 1;
       // all table loads before the barrier and the stores
-      float2 cs[2][4][NB];
+      float2 cs[RB][4][NB];
       if (tl.rope) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < RB; ++i)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int rr = min(rbase + 16 * i + r, mcnt - 1);
@@ -388,7 +399,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       }
       __syncthreads();   // every wave is done with the weight buffers
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -405,10 +416,10 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
       __syncthreads();
       // piece q: wave-local row q / (2 NB), block (q / 2) % NB, half q % 2
 #pragma unroll
-      for (int it = 0; it < NB; ++it) {
+      for (int it = 0; it < RB * NB / 2; ++it) {
         const int q = it * 64 + lane;
         const int lr = q / (2 * NB), j = (q >> 1) % NB, h = q & 1;
-        const int row = wave * 32 + lr;
+        const int row = wave * 16 * RB + lr;
         const uint4 v = *reinterpret_cast<const uint4*>(&E[q * 8]);
         const int gb = tl.b0 + j;
         const int col = tl.ocol0 + (gb / hb) * d + (gb % hb) * 8 + h * half;
@@ -418,7 +429,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
     } else {
       __syncthreads();   // every wave is done with the weight buffers
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -431,13 +442,14 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
                   gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up);
           }
       __syncthreads();
-      // piece q < 32 NB: wave-local row q % 32, block q / 32 (16 lanes store
-      // the 256 contiguous bytes of one 8-channel group of 16 packed rows)
+      // piece q < 16 RB NB: wave-local row q % (16 RB), block q / (16 RB) (16
+      // lanes store the 256 contiguous bytes of one 8-channel group of 16
+      // packed rows)
 #pragma unroll
-      for (int it = 0; it < (NB + 1) / 2; ++it) {
+      for (int it = 0; it < (RB * NB + 3) / 4; ++it) {
         const int q = it * 64 + lane;
-        const int lr = q & 31, j = q >> 5;
-        const int row = wave * 32 + lr;
+        const int lr = q % (16 * RB), j = q / (16 * RB);
+        const int row = wave * 16 * RB + lr;
         if (j < NB) {
           const uint4 v = *reinterpret_cast<const uint4*>(&E[lr * RW + j * 8]);
           if (j < nblk && row < mcnt)
@@ -449,10 +461,10 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   } else {
     float* out = EPI == EPI_PARTIAL ? a.partial + (size_t)tl.slice * a.pslice
                                     : static_cast<float*>(a.out);
-    float old[2][4][NB];
+    float old[RB][4][NB];
     if constexpr (EPI == EPI_RESID) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float* orow =
@@ -463,7 +475,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
         }
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RB; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rbase + 16 * i + r;
@@ -478,10 +490,10 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(MmArgs a) {
   }
 }
 
-template <int EPI, int NB, bool F16>
+template <int EPI, int NB, bool F16, int NWAVE = 8>
 hipError_t launch(const MmArgs& a, hipStream_t st) {
   const unsigned grid = (unsigned)((a.ntiles + 7) / 8 * 8);
-  gemm_mfma_kernel<EPI, NB, F16><<<grid, NT, 0, st>>>(a);
+  gemm_mfma_kernel<EPI, NB, F16, NWAVE><<<grid, NWAVE * 64, 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -499,7 +511,13 @@ hipError_t by_nb(const MmArgs& a, int32_t nb, hipStream_t st) {
 }
 
 template <bool F16>
-hipError_t dispatch(const MmArgs& a, int32_t epi, int32_t nb, hipStream_t st) {
+hipError_t dispatch(const MmArgs& a, int32_t epi, int32_t nb, int32_t waves, hipStream_t st) {
+  if (waves == 4) {
+    // 4-wave tiles: the residual-add output / down projections of 4 blocks
+    if (epi == EPI_RESID && nb == 4) return launch<EPI_RESID, 4, F16, 4>(a, st);
+    return hipErrorInvalidValue;
+  }
+  if (waves != 8) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_QKV: return by_nb<EPI_QKV, F16>(a, nb, st);
     case EPI_SWIGLU: return by_nb<EPI_SWIGLU, F16>(a, nb, st);
@@ -511,9 +529,10 @@ hipError_t dispatch(const MmArgs& a, int32_t epi, int32_t nb, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st) {
+hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, int32_t waves, bool f16,
+                            hipStream_t st) {
   if (a.ntiles <= 0) return hipSuccess;
-  return f16 ? dispatch<true>(a, epi, nb, st) : dispatch<false>(a, epi, nb, st);
+  return f16 ? dispatch<true>(a, epi, nb, waves, st) : dispatch<false>(a, epi, nb, waves, st);
 }
 
 }  // namespace svl

@@ -20,6 +20,8 @@ struct GemmLaunch {
   int32_t ngroups = 0;
   int32_t ntiles = 0;
   int32_t nb = 0;           // 16-bit MFMA path: kernel block count (tiles hold <= nb)
+  int32_t waves = 8;        // 16-bit MFMA path: waves per workgroup (8, or 4 for wide
+                            // residual-add launches)
   int32_t nsplit = 1;       // > 1: split-K pieces written as float32 partial slices
   int32_t nitems = 0;       // split QKV / gate-up launches: finish kernel work items
   int32_t nblocks = 0;      // 16-bit path: the groups' 16-column blocks (each group's

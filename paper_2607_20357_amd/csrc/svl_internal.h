@@ -190,7 +190,9 @@ hipError_t launch_gather(const int32_t* kept_idx, const int32_t* keep_dev, const
                          hipStream_t st);
 // out_kind: 0 float32 row-major, 1 bf16 packed, 2 fp16 packed
 hipError_t launch_resid_norm(const NormArgs& a, int32_t out_kind, hipStream_t st);
-hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, bool f16, hipStream_t st);
+// waves: 8 (any epilogue and block count) or 4 (EPI_RESID with 4 blocks)
+hipError_t launch_gemm_mfma(const MmArgs& a, int32_t epi, int32_t nb, int32_t waves, bool f16,
+                            hipStream_t st);
 hipError_t launch_finish(const FinishArgs& a, int32_t epi, bool f16, hipStream_t st);
 // Decode: one-row groups, one workgroup per 16-column block (QKV, SWIGLU, RESID).
 hipError_t launch_gemv_shared(const MmArgs& a, int32_t epi, bool f16, hipStream_t st);

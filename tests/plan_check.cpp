@@ -68,6 +68,8 @@ static int block_row(int kind, int wrow0, int gb, int d) {
   return wrow0 + gb * 16;
 }
 
+static int g_waves4 = 0;   // launches planned with 4-wave tiles
+
 static void check_prefill(const Case& c) {
   const svl_config& cfg = c.cfg;
   const int B = c.B, L = cfg.n_layers, A = cfg.n_heads, KV = cfg.n_kv_heads, d = cfg.head_dim;
@@ -120,6 +122,7 @@ static void check_prefill(const Case& c) {
         const MmGroup& g = gr[x.group];
         CHECK(x.arow % 16 == 0 && x.mcnt >= 1 && x.mcnt <= MFMA_BM, "qkv tile rows");
         CHECK(x.b0 >= 0 && x.b0 + x.nblk <= g.nblocks && x.nblk <= LP.qkv.nb, "qkv tile blocks");
+        CHECK(LP.qkv.waves == 8 && LP.gu.waves == 8, "paired launches take 8-wave tiles");
         int s0 = -2;
         bool single = true;
         for (int r = 0; r < x.mcnt; ++r) {
@@ -193,6 +196,12 @@ static void check_prefill(const Case& c) {
     for (int which = 0; which < 2; ++which) {
       const GemmLaunch& GL = which == 0 ? LP.o : LP.down;
       const int K = which == 0 ? A * d : F;
+      g_waves4 += GL.waves == 4;
+      // 4-wave tiles only for unsplit 4-block launches with more tiles than CUs
+      CHECK(GL.waves == 8 || (GL.waves == 4 && GL.nsplit == 1 && GL.nb == 4 &&
+                              GL.ntiles > kTargetTiles),
+            "plain launch waves %d (nsplit %d, nb %d, tiles %d)", GL.waves, GL.nsplit, GL.nb,
+            GL.ntiles);
       std::map<std::tuple<int, int, int>, int> co;
       const MmGroup* gr = at<MmGroup>(plan, GL.groups_off);
       const MmTile* tl = at<MmTile>(plan, GL.tiles_off);
@@ -392,6 +401,35 @@ int main() {
     std::fprintf(stderr, "plan_check: %d failures\n", g_fail);
     return 1;
   }
-  std::printf("plan_check ok (%d cases)\n", cases);
+  {
+    // a batch whose output / down projections have more tiles than CUs
+    // (16 samples x 3 M tiles x 8 N tiles)
+    Case c{};
+    c.cfg = svl_config{};
+    c.cfg.n_layers = 1;
+    c.cfg.d_model = 512;
+    c.cfg.n_heads = 8;
+    c.cfg.n_kv_heads = 8;
+    c.cfg.head_dim = 64;
+    c.cfg.d_ffn = 256;
+    c.cfg.n_groups = 4;
+    c.cfg.rms_eps = 1e-6f;
+    c.cfg.rope_theta = 10000.f;
+    c.cfg.dtype = SVL_BF16;
+    c.cfg.compute = SVL_COMPUTE_F16;
+    c.B = 16;
+    c.seq.assign(c.B, 520);
+    c.lon.assign(c.B, 1);
+    c.hm.assign((size_t)c.B * 8, 1);
+    c.fm.assign((size_t)c.B * 4, 1);
+    c.ffn_gated = true;
+    check_prefill(c);
+    ++cases;
+  }
+  if (g_waves4 == 0) {
+    std::fprintf(stderr, "plan_check: no case planned 4-wave tiles\n");
+    return 1;
+  }
+  std::printf("plan_check ok (%d cases, %d launches with 4-wave tiles)\n", cases, g_waves4);
   return 0;
 }

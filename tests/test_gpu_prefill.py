@@ -125,11 +125,14 @@ def test_layer_masks_and_edges(dtype, compute):
 
 
 @pytest.mark.parametrize("name,compute", [("llava7b_b1_keep25", "f16"), ("llava7b_b1_keep25", "bf16"),
-                                          ("llava7b_b8_ragged", "f16"), ("gqa7b_hires_b2", "f16"),
+                                          ("llava7b_b8_ragged", "f16"), ("llava7b_b8_ragged", "bf16"),
+                                          ("gqa7b_hires_b2", "f16"),
                                           ("llava13b_video_b4", "f16")])
 def test_layer_full_size(name, compute):
     """One decoder layer at each workload's real width, sequence lengths and
-    masks (first non-prefix layer of the seed-0 draw)."""
+    masks (first non-prefix layer of the seed-0 draw).  The batched workloads'
+    output / down projections have more tiles than CUs and run as 4-wave
+    tiles."""
     w = W.get_workload(name)
     keep, lm, hm, fm = W.draw_masks(w, 0)
     l = w.shape.prefix
