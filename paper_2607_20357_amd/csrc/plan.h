@@ -90,9 +90,10 @@ constexpr int32_t kSkinnyRows = MFMA_BM;
 constexpr int32_t kTargetTiles = 256;
 // Norm launches of at least this many rows (16-bit output) use the 8-row
 // group kernel (whole packed lines per store) instead of one row per
-// workgroup (more workgroups for short launches; measured faster from a few
-// hundred rows: 18.7 -> 12.3 us per launch on a ragged batch of 8).
-constexpr int32_t kNormRows8 = 256;
+// workgroup (more workgroups for short launches: at 208 rows the 8-row
+// kernel's 26 workgroups take 29.5 us against 11.1; from 1024 rows it is
+// faster, 18.7 -> 12.6 us per launch on a ragged batch of 8).
+constexpr int32_t kNormRows8 = 1024;
 
 // Builds the plan for `nlayers` layers.  seqlens/keep host [B]; masks[l]
 // gives layer l's masks.  Returns false with a message on inconsistency.

@@ -198,7 +198,7 @@ def test_layer_forced_paired_split(split, monkeypatch):
 
 
 def test_norm_row_groups(monkeypatch):
-    """The 8-row-group residual norm (taken by launches of 256+ rows), forced
+    """The 8-row-group residual norm (taken by launches of 1024+ rows), forced
     onto small launches: ragged segments whose lengths are not multiples of 8,
     split-K partial slices to add (the output and down projections split at
     these row counts), a final add-only launch, and row widths in registers of
