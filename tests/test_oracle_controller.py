@@ -232,3 +232,49 @@ def test_controlled_prefill_rows_before_the_first_drop_are_unaffected():
         # and the sequence still ends with the text and budget rows
         assert res.cu_seqlens[b + 1] - res.cu_seqlens[b] == res.keep[b] + w.n_text + 1
     assert checked > 0
+
+
+def test_controlled_prefill_identity_prefix_equals_plain_prefill_of_projected_keep():
+    """0 < P < L with token drops and prefix layers that are the identity on the
+    residual stream (their output and down projections zeroed): the sequence
+    that enters layer P must be [projected kept vision ; text ; budget row]
+    exactly as the plain prefill of the projected keep builds it, so every row
+    of the result (kept, text and budget rows alike) equals that prefill under
+    the final masks.  This fixes which rows survive the projection at the
+    prefix boundary and where the text and budget rows are taken from."""
+    P = 2
+    w = SHAPE_W
+    seed = 11
+    inp = W.draw_inputs(w, seed)
+    layers = [host_layer(W.draw_layer_weights(w, l, seed)) for l in range(w.shape.n_layers)]
+    for l in range(P):
+        layers[l] = dict(layers[l])
+        layers[l]["wo"] = np.zeros_like(layers[l]["wo"])
+        layers[l]["w_down"] = np.zeros_like(layers[l]["w_down"])
+    draw = W.draw_controller(w, seed, prefix=P, units=4, pe_dim=16, hidden=32)
+    ctrl = host_controller(draw)
+    rng = np.random.default_rng(seed)
+    z = (rng.standard_normal((w.batch, w.n_vision)) + 0.3).astype(np.float32)
+    vis, txt = W.as_f32(inp.vision), W.as_f32(inp.text)
+    budget = 0.35
+    res = oc.prefill_controlled(w.shape, lambda l: layers[l], ctrl, z, vis, txt, budget)
+    counts = np.array([ob.threshold_count(z[b]) for b in range(w.batch)])
+    assert np.all(res.keep < counts), "the case must exercise token drops"
+    assert np.all(res.keep > 0), "the case must keep visual tokens on both sides of a drop"
+    # the first discarded token is not the last threshold-kept one, so rows
+    # after it (kept vision, then text and budget) change position
+    for b in range(w.batch):
+        first = oracle.select_topk(z[b], int(counts[b]))
+        final = res.kept_idx[b, :res.keep[b]]
+        assert not np.array_equal(first[:final.size], final), "a drop ahead of a kept token"
+    ref = oracle.prefill(w.shape, lambda l: layers[l], z, res.keep, vis,
+                         _text_with_budget_row(txt, ctrl, budget), res.layer_mask,
+                         res.head_mask, res.ffn_mask)
+    np.testing.assert_array_equal(res.kept_idx, ref.kept_idx)
+    np.testing.assert_array_equal(res.cu_seqlens, ref.cu_seqlens)
+    np.testing.assert_allclose(res.resid, ref.resid, rtol=0, atol=1e-12)
+    # the budget row of each sample is its last row and came through unchanged
+    # by the prefix (identity) into the gated layers
+    for b in range(w.batch):
+        np.testing.assert_allclose(res.prefix_resid[b][-1], oc.budget_token(ctrl, budget),
+                                   rtol=0, atol=0)
