@@ -170,7 +170,123 @@ def _dev(t: Optional[torch.Tensor], name: str) -> int:
         raise ValueError(f"{name} must be a GPU tensor (no CPU path exists)")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} is on {t.device}, the library launches on "
+                         f"cuda:{torch.cuda.current_device()}")
     return t.data_ptr()
+
+
+# ------------------------------------------------------------------ tensor checks
+# The C ABI takes plain pointers, so it cannot see a tensor's size or type:
+# a short buffer or a wrong element type would make a kernel read or write
+# past the allocation.  Every entry point below therefore checks each
+# tensor's dtype and element count against the configuration and the batch
+# before anything is passed to the library (and before the device check, so
+# the host tests can exercise these checks without a GPU).
+def storage_dtype(cfg: svl_config) -> torch.dtype:
+    """Torch dtype of weights and hidden inputs for a configuration."""
+    return torch.bfloat16 if cfg.dtype == SVL_BF16 else torch.float32
+
+
+def _expect(t: Optional[torch.Tensor], name: str, dtype: torch.dtype, numel: int,
+            shape: Optional[tuple] = None) -> None:
+    """t must have `dtype` and at least `numel` elements (exactly `shape` if given)."""
+    if t is None:
+        if numel > 0:
+            raise ValueError(f"{name} is required")
+        return
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs at least {numel}")
+
+
+def _weight_shapes(cfg: svl_config) -> Dict[str, tuple]:
+    D, A, KV, d, F = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ffn
+    return {"attn_norm": (D,), "wq": (A * d, D), "wk": (KV * d, D), "wv": (KV * d, D),
+            "wo": (D, A * d), "ffn_norm": (D,), "w_gate": (F, D), "w_up": (F, D),
+            "w_down": (D, F)}
+
+
+def check_layer_weights(cfg: svl_config, w: Dict[str, torch.Tensor], what: str = "layer") -> None:
+    """Every weight tensor has the configuration's storage dtype and its exact shape."""
+    dt = storage_dtype(cfg)
+    for n, shp in _weight_shapes(cfg).items():
+        if n not in w:
+            raise ValueError(f"{what}: weight {n} is missing")
+        _expect(w[n], f"{what}.{n}", dt, int(np.prod(shp)), shp)
+
+
+def _check_hidden(cfg: svl_config, B: int, N: int, T: int, scores, vision, text,
+                  kept_idx, score_name: str = "scores") -> None:
+    D = cfg.d_model
+    dt = storage_dtype(cfg)
+    _expect(scores, score_name, torch.float32, B * N, (B, N))
+    _expect(vision, "vision", dt, B * N * D, (B, N, D))
+    _expect(text, "text", dt, B * T * D, (B, T, D))
+    _expect(kept_idx, "kept_idx", torch.int32, B * N)
+
+
+def _check_table(cfg: svl_config, table: "LayerTable") -> None:
+    if len(table.layers) != cfg.n_layers:
+        raise ValueError(f"{len(table.layers)} layers given, the configuration has {cfg.n_layers}")
+    if table.cfg_checked is not None and table.cfg_checked == _cfg_key(cfg):
+        return
+    for l, w in enumerate(table.layers):
+        check_layer_weights(cfg, w, f"layer {l}")
+    table.cfg_checked = _cfg_key(cfg)
+
+
+def _table(cfg: svl_config, layers) -> "LayerTable":
+    """A checked LayerTable from a LayerTable or a list of per-layer weight dicts
+    (the dicts are checked before any device pointer is taken)."""
+    if not isinstance(layers, LayerTable):
+        layers = list(layers)
+        if len(layers) != cfg.n_layers:
+            raise ValueError(f"{len(layers)} layers given, the configuration has {cfg.n_layers}")
+        for l, w in enumerate(layers):
+            check_layer_weights(cfg, w, f"layer {l}")
+        table = LayerTable(layers)
+        table.cfg_checked = _cfg_key(cfg)
+        return table
+    _check_table(cfg, layers)
+    return layers
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def _cfg_key(cfg: svl_config) -> tuple:
+    return tuple(getattr(cfg, n) for n, _ in cfg._fields_)
+
+
+def _batch_dims(scores: torch.Tensor, text: torch.Tensor, score_name: str = "scores"):
+    """(B, N, T) from scores [B][N] and text [B][T][D]."""
+    if not isinstance(scores, torch.Tensor) or scores.dim() != 2:
+        raise ValueError(f"{score_name} must be a [B][N] tensor")
+    if not isinstance(text, torch.Tensor) or text.dim() != 3:
+        raise ValueError("text must be a [B][T][D] tensor")
+    return int(scores.shape[0]), int(scores.shape[1]), int(text.shape[1])
+
+
+def _check_keep(kp: np.ndarray, B: int, N: int) -> int:
+    if kp.shape != (B,):
+        raise ValueError(f"keep has shape {kp.shape}, expected ({B},)")
+    if np.any(kp < 0) or np.any(kp > N):
+        raise ValueError(f"keep values must lie in [0, {N}]")
+    return int(kp.sum())
+
+
+def _host_mask(a, name: str, shape: tuple):
+    arr, ptr = _host_u8(a, name)
+    if arr.shape != tuple(shape):
+        raise ValueError(f"{name} has shape {arr.shape}, expected {tuple(shape)}")
+    return arr, ptr
 
 
 def _host_u8(a, name: str):
@@ -225,11 +341,14 @@ def svl_count_flops(cfg: svl_config, seqlens, layer_mask, head_mask, ffn_mask=No
 
 def svl_count_positive(logits: torch.Tensor, ws: torch.Tensor, stream=None) -> np.ndarray:
     """Threshold counts (logits > 0 per sample), host int32 [B]; synchronises the stream."""
+    if not isinstance(logits, torch.Tensor) or logits.dim() != 2:
+        raise ValueError("logits must be a [B][N] tensor")
     B, N = logits.shape
+    _expect(logits, "logits", torch.float32, B * N)
     counts = np.zeros(B, dtype=np.int32)
     _check(load_library().svl_count_positive(int(B), int(N), _dev(logits, "logits"),
                                              counts.ctypes.data_as(ctypes.c_void_p),
-                                             _dev(ws, "ws"), ws.numel(), _stream(stream)))
+                                             _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
     return counts
 
 
@@ -258,13 +377,16 @@ def svl_select_tokens(cfg: svl_config, keep, scores: torch.Tensor, vision: torch
                       ws: torch.Tensor, stream=None) -> np.ndarray:
     """Top-k selection and packing; returns cu_seqlens (host int32 [B+1])."""
     kp, kpp = _host_i32(keep)
-    B, N = scores.shape
-    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
+    B, N, T = _batch_dims(scores, text)
+    R = _check_keep(kp, B, N) + B * T
+    _check_hidden(cfg, B, N, T, scores, vision, text, kept_idx)
+    _expect(resid, "resid", torch.float32, R * cfg.d_model)
+    batch = svl_batch(int(B), int(N), int(T), kpp)
     cu = np.zeros(B + 1, dtype=np.int32)
     _check(load_library().svl_select_tokens(
         ctypes.byref(cfg), ctypes.byref(batch), _dev(scores, "scores"), _dev(vision, "vision"),
         _dev(text, "text"), _dev(kept_idx, "kept_idx"), _dev(resid, "resid"),
-        cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), _dev(ws, "ws"), ws.numel(),
+        cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), _dev(ws, "ws"), _nbytes(ws),
         _stream(stream)))
     return cu
 
@@ -273,20 +395,31 @@ def svl_layer_forward(cfg: svl_config, layer: int, weights: Dict[str, torch.Tens
                       layer_on, head_mask, ffn_mask, resid: torch.Tensor, ws: torch.Tensor,
                       stream=None) -> None:
     cu, cup = _host_i32(cu_seqlens)
-    lo, lop = _host_u8(layer_on, "layer_on")
-    hm, hmp = _host_u8(head_mask, "head_mask")
-    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    if cu.ndim != 1 or cu.shape[0] < 2:
+        raise ValueError("cu_seqlens must be a host array of batch + 1 entries")
+    B = int(cu.shape[0] - 1)
+    lo, lop = _host_mask(layer_on, "layer_on", (B,))
+    hm, hmp = _host_mask(head_mask, "head_mask", (B, cfg.n_heads))
+    fm, fmp = (None, None) if ffn_mask is None else _host_mask(ffn_mask, "ffn_mask",
+                                                                (B, cfg.n_groups))
+    check_layer_weights(cfg, weights)
+    _expect(resid, "resid", torch.float32, int(cu[-1]) * cfg.d_model)
     w = layer_weights(weights)
     _check(load_library().svl_layer_forward(
         ctypes.byref(cfg), int(layer), ctypes.byref(w), int(cu.shape[0] - 1), cup, lop, hmp, fmp,
-        _dev(resid, "resid"), _dev(ws, "ws"), ws.numel(), _stream(stream)))
+        _dev(resid, "resid"), _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
 
 
 class LayerTable:
-    """Host array of svl_layer_weights for svl_prefill (built once, reused)."""
+    """Host array of svl_layer_weights for svl_prefill (built once, reused).
+
+    The weights' shapes and dtypes are checked against the configuration of
+    the first call that uses the table (and again if the configuration
+    changes)."""
 
     def __init__(self, layers: Sequence[Dict[str, torch.Tensor]]):
         self.layers = list(layers)         # keeps the tensors alive
+        self.cfg_checked = None
         self.array = (svl_layer_weights * len(self.layers))(*[layer_weights(w) for w in self.layers])
 
 
@@ -296,20 +429,24 @@ def svl_prefill(cfg: svl_config, layers, keep, scores: torch.Tensor, vision: tor
     """The whole budget-adapted prefill; returns (cu_seqlens, flops dict or None).
 
     `layers` is a LayerTable or a list of per-layer weight dicts."""
-    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
     kp, kpp = _host_i32(keep)
-    B, N = scores.shape
-    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
-    lm, lmp = _host_u8(layer_mask, "layer_mask")
-    hm, hmp = _host_u8(head_mask, "head_mask")
-    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    B, N, T = _batch_dims(scores, text)
+    R = _check_keep(kp, B, N) + B * T
+    L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    _check_hidden(cfg, B, N, T, scores, vision, text, kept_idx)
+    _expect(resid, "resid", torch.float32, R * cfg.d_model)
+    batch = svl_batch(int(B), int(N), int(T), kpp)
+    lm, lmp = _host_mask(layer_mask, "layer_mask", (B, L))
+    hm, hmp = _host_mask(head_mask, "head_mask", (B, L, A))
+    fm, fmp = (None, None) if ffn_mask is None else _host_mask(ffn_mask, "ffn_mask", (B, L, G))
     cu = np.zeros(B + 1, dtype=np.int32)
     fl = svl_flops()
+    table = _table(cfg, layers)
     _check(load_library().svl_prefill(
         ctypes.byref(cfg), table.array, ctypes.byref(batch), _dev(scores, "scores"),
         _dev(vision, "vision"), _dev(text, "text"), lmp, hmp, fmp, _dev(kept_idx, "kept_idx"),
         _dev(resid, "resid"), cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
+        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
     return cu, (fl.as_dict() if want_flops else None)
 
 
@@ -337,19 +474,24 @@ def svl_prefill_cache(cfg: svl_config, layers, keep, scores: torch.Tensor, visio
                       resid: torch.Tensor, kv_cache: torch.Tensor, max_len: int, ws: torch.Tensor,
                       stream=None) -> np.ndarray:
     """The prefill that also fills the KV cache; returns cu_seqlens."""
-    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
     kp, kpp = _host_i32(keep)
-    B, N = scores.shape
-    batch = svl_batch(int(B), int(N), int(text.shape[1]), kpp)
-    lm, lmp = _host_u8(layer_mask, "layer_mask")
-    hm, hmp = _host_u8(head_mask, "head_mask")
-    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    B, N, T = _batch_dims(scores, text)
+    R = _check_keep(kp, B, N) + B * T
+    L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    _check_hidden(cfg, B, N, T, scores, vision, text, kept_idx)
+    _expect(resid, "resid", torch.float32, R * cfg.d_model)
+    _expect(kv_cache, "kv_cache", torch.uint8, svl_kv_cache_bytes(cfg, B, max_len))
+    batch = svl_batch(int(B), int(N), int(T), kpp)
+    lm, lmp = _host_mask(layer_mask, "layer_mask", (B, L))
+    hm, hmp = _host_mask(head_mask, "head_mask", (B, L, A))
+    fm, fmp = (None, None) if ffn_mask is None else _host_mask(ffn_mask, "ffn_mask", (B, L, G))
     cu = np.zeros(B + 1, dtype=np.int32)
+    table = _table(cfg, layers)
     _check(load_library().svl_prefill_cache(
         ctypes.byref(cfg), table.array, ctypes.byref(batch), _dev(scores, "scores"),
         _dev(vision, "vision"), _dev(text, "text"), lmp, hmp, fmp, _dev(kept_idx, "kept_idx"),
         _dev(resid, "resid"), cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-        _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), ws.numel(), _stream(stream)))
+        _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
     return cu
 
 
@@ -357,14 +499,22 @@ def svl_decode_step(cfg: svl_config, layers, x: torch.Tensor, cache_len, layer_m
                     ffn_mask, kv_cache: torch.Tensor, max_len: int, ws: torch.Tensor,
                     stream=None) -> None:
     """One decode step, x [B][D] float32 updated in place; the caller advances cache_len."""
-    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x must be a [B][D] tensor")
+    B = int(x.shape[0])
+    L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    _expect(x, "x", torch.float32, B * cfg.d_model, (B, cfg.d_model))
+    _expect(kv_cache, "kv_cache", torch.uint8, svl_kv_cache_bytes(cfg, B, max_len))
     cl, clp = _host_i32(cache_len)
-    lm, lmp = _host_u8(layer_mask, "layer_mask")
-    hm, hmp = _host_u8(head_mask, "head_mask")
-    fm, fmp = (None, None) if ffn_mask is None else _host_u8(ffn_mask, "ffn_mask")
+    if cl.shape != (B,):
+        raise ValueError(f"cache_len has shape {cl.shape}, expected ({B},)")
+    lm, lmp = _host_mask(layer_mask, "layer_mask", (B, L))
+    hm, hmp = _host_mask(head_mask, "head_mask", (B, L, A))
+    fm, fmp = (None, None) if ffn_mask is None else _host_mask(ffn_mask, "ffn_mask", (B, L, G))
+    table = _table(cfg, layers)
     _check(load_library().svl_decode_step(
         ctypes.byref(cfg), table.array, int(x.shape[0]), _dev(x, "x"),
-        clp, lmp, hmp, fmp, _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), ws.numel(),
+        clp, lmp, hmp, fmp, _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), _nbytes(ws),
         _stream(stream)))
 
 
@@ -392,6 +542,17 @@ class Controller:
                                      float(pe_scale), float(pe_base),
                                      *[_dev(self.tensors[n], n) for n in CONTROLLER_FIELDS])
 
+    def check(self, cfg: svl_config) -> None:
+        """The parameters' dtypes and shapes against the configuration."""
+        E, H, D = self.struct.pe_dim, self.struct.hidden, cfg.d_model
+        n = (cfg.n_layers - self.struct.prefix) * self.struct.units
+        shapes = {"llm_w1": (H, E), "llm_b1": (H,), "llm_w2": (D, H), "llm_b2": (D,),
+                  "kap_w1": (H, E), "kap_b1": (H,), "kap_w2": (D, H), "kap_b2": (D,),
+                  "gate_w": (max(n, 0), D), "gate_b": (max(n, 0),)}
+        dt = storage_dtype(cfg)
+        for name, shp in shapes.items():
+            _expect(self.tensors.get(name), f"controller.{name}", dt, int(np.prod(shp)), shp)
+
 
 def svl_controlled_workspace_bytes(cfg: svl_config, ctrl: Controller, batch: int, n_vision: int,
                                    n_text: int) -> int:
@@ -415,10 +576,11 @@ def svl_prefill_controlled(cfg: svl_config, layers, ctrl: Controller, logits: to
     """The controlled prefill (synchronises the stream twice).  resid needs room
     for B (N + T + 1) rows.  Returns the host outputs: cu_seqlens, keep,
     layer_mask, head_mask, ffn_mask, gate_logits and flops."""
-    table = layers if isinstance(layers, LayerTable) else LayerTable(layers)
-    B, N = logits.shape
-    T = int(text.shape[1])
+    B, N, T = _batch_dims(logits, text, "logits")
     L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    _check_hidden(cfg, B, N, T, logits, vision, text, kept_idx, "logits")
+    _expect(resid, "resid", torch.float32, B * (N + T + 1) * cfg.d_model)
+    ctrl.check(cfg)
     nl = (L - ctrl.struct.prefix) * ctrl.struct.units
     out = {"cu_seqlens": np.zeros(B + 1, np.int32), "keep": np.zeros(B, np.int32),
            "layer_mask": np.zeros((B, L), np.uint8), "head_mask": np.zeros((B, L, A), np.uint8),
@@ -426,13 +588,14 @@ def svl_prefill_controlled(cfg: svl_config, layers, ctrl: Controller, logits: to
            "gate_logits": np.zeros((B, max(nl, 0)), np.float32)}
     vp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
     fl = svl_flops()
+    table = _table(cfg, layers)
     _check(load_library().svl_prefill_controlled(
         ctypes.byref(cfg), table.array, ctypes.byref(ctrl.struct), int(B), int(N), T,
         ctypes.c_float(budget), ctypes.c_int64(int(vocab)), _dev(logits, "logits"),
         _dev(vision, "vision"), _dev(text, "text"), _dev(kept_idx, "kept_idx"),
         _dev(resid, "resid"), vp(out["cu_seqlens"]), vp(out["keep"]), vp(out["layer_mask"]),
         vp(out["head_mask"]), vp(out["ffn_mask"]), vp(out["gate_logits"]),
-        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), ws.numel(), _stream(stream)))
+        ctypes.byref(fl) if want_flops else None, _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
     out["flops"] = fl.as_dict() if want_flops else None
     return out
 
@@ -442,8 +605,18 @@ def svl_budget_loss(cfg: svl_config, params: svl_budget_loss_params, logits: tor
                     stream=None) -> Dict[str, torch.Tensor]:
     """Training-time budget term on the GPU; returns device tensors token_mask,
     unit_mask, ratio, loss, grad_logits, grad_gate (enqueued on the stream)."""
+    if not isinstance(logits, torch.Tensor) or logits.dim() != 2:
+        raise ValueError("logits must be a [B][N] tensor")
+    if not isinstance(gate_logits, torch.Tensor) or gate_logits.dim() != 2:
+        raise ValueError("gate_logits must be a [B][units] tensor")
     B, N = logits.shape
     nl = gate_logits.shape[1]
+    _expect(logits, "logits", torch.float32, B * N)
+    _expect(gate_logits, "gate_logits", torch.float32, B * nl, (B, nl))
+    if token_noise is not None:
+        _expect(token_noise, "token_noise", torch.float32, B * N, (B, N))
+    if gate_noise is not None:
+        _expect(gate_noise, "gate_noise", torch.float32, B * nl, (B, nl))
     dev = logits.device
     out = {"token_mask": torch.empty((B, N), dtype=torch.uint8, device=dev),
            "unit_mask": torch.empty((B, nl), dtype=torch.uint8, device=dev),

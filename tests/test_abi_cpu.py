@@ -292,3 +292,113 @@ def test_budget_loss_rejects_bad_arguments():
         assert call(**kw) == want, kw
     assert lib.svl_budget_loss(ctypes.byref(cfg), None, 1, 1, 1, dev, None, dev, None, dev, dev,
                                dev, dev, dev, dev, None) == 1
+
+
+# ============================================================================ binding checks
+# The binding checks every tensor's dtype and size against the configuration
+# and the batch before a pointer reaches the library: a short buffer or a
+# wrong element type would otherwise let a kernel read or write past the
+# allocation.  These run on CPU tensors: every case must fail on its shape or
+# dtype check, which comes before the device check, and a correct set of
+# tensors gets as far as the device check ("must be a GPU tensor").
+import torch  # noqa: E402
+
+_BSHAPE = ModelShape(n_layers=2, d_model=64, n_heads=4, n_kv_heads=2, head_dim=64, d_ffn=256,
+                     n_groups=4, dtype="bf16")
+
+
+def _bind_case(dtype=torch.bfloat16):
+    cfg = svl.make_config(_BSHAPE)
+    B, N, T, D = 2, 12, 3, _BSHAPE.d_model
+    keep = np.array([5, 12], np.int32)
+    R = int(keep.sum()) + B * T
+    layers = []
+    for _ in range(_BSHAPE.n_layers):
+        w = {n: torch.zeros(shp, dtype=dtype) for n, shp in binding._weight_shapes(cfg).items()}
+        layers.append(w)
+    L, A, G = _BSHAPE.n_layers, _BSHAPE.n_heads, _BSHAPE.n_groups
+    args = dict(cfg=cfg, layers=layers, keep=keep,
+                scores=torch.zeros((B, N), dtype=torch.float32),
+                vision=torch.zeros((B, N, D), dtype=dtype), text=torch.zeros((B, T, D), dtype=dtype),
+                layer_mask=np.ones((B, L), np.uint8), head_mask=np.ones((B, L, A), np.uint8),
+                ffn_mask=np.ones((B, L, G), np.uint8),
+                kept_idx=torch.zeros((B, N), dtype=torch.int32),
+                resid=torch.zeros((R, D), dtype=torch.float32),
+                ws=torch.zeros(64, dtype=torch.uint8))
+    return args
+
+
+def _prefill(**a):
+    return svl.svl_prefill(a["cfg"], a["layers"], a["keep"], a["scores"], a["vision"], a["text"],
+                           a["layer_mask"], a["head_mask"], a["ffn_mask"], a["kept_idx"],
+                           a["resid"], a["ws"])
+
+
+def test_binding_prefill_accepts_consistent_tensors_up_to_the_device_check():
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        _prefill(**_bind_case())
+
+
+@pytest.mark.parametrize("change, match", [
+    (lambda a: a.update(resid=a["resid"][:-1]), "resid holds"),
+    (lambda a: a.update(resid=a["resid"].to(torch.float64)), "resid has dtype"),
+    (lambda a: a.update(vision=a["vision"][:, :-1]), "vision has shape"),
+    (lambda a: a.update(text=a["text"].float()), "text has dtype"),
+    (lambda a: a.update(scores=a["scores"].double()), "scores has dtype"),
+    (lambda a: a.update(kept_idx=a["kept_idx"].long()), "kept_idx has dtype"),
+    (lambda a: a.update(kept_idx=a["kept_idx"][:1]), "kept_idx holds"),
+    (lambda a: a["layers"][1].update(w_down=a["layers"][1]["w_down"].t()), "layer 1.w_down has shape"),
+    (lambda a: a["layers"][0].update(wq=a["layers"][0]["wq"].float()), "layer 0.wq has dtype"),
+    (lambda a: a["layers"][0].update(wk=a["layers"][0]["wq"]), "layer 0.wk has shape"),
+    (lambda a: a["layers"][0].pop("ffn_norm"), "ffn_norm is missing"),
+    (lambda a: a.update(layers=a["layers"][:1]), "1 layers given"),
+    (lambda a: a.update(head_mask=a["head_mask"][:, :, :2]), "head_mask has shape"),
+    (lambda a: a.update(layer_mask=a["layer_mask"][:1]), "layer_mask has shape"),
+    (lambda a: a.update(ffn_mask=a["ffn_mask"][..., :3]), "ffn_mask has shape"),
+    (lambda a: a.update(keep=np.array([5, 13], np.int32)), "keep values"),
+    (lambda a: a.update(keep=np.array([5], np.int32)), "keep has shape"),
+])
+def test_binding_prefill_rejects_mismatched_tensors(change, match):
+    a = _bind_case()
+    change(a)
+    with pytest.raises(ValueError, match=match):
+        _prefill(**a)
+
+
+def test_binding_select_layer_decode_reject_mismatched_tensors():
+    a = _bind_case()
+    cfg, D = a["cfg"], _BSHAPE.d_model
+    # selection: resid one row short
+    with pytest.raises(ValueError, match="resid holds"):
+        svl.svl_select_tokens(cfg, a["keep"], a["scores"], a["vision"], a["text"], a["kept_idx"],
+                              a["resid"][:-1], a["ws"])
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        svl.svl_select_tokens(cfg, a["keep"], a["scores"], a["vision"], a["text"], a["kept_idx"],
+                              a["resid"], a["ws"])
+    # one layer: resid shorter than cu_seqlens[-1] rows, wrong weight dtype, mask shapes
+    cu = np.array([0, 8, 23], np.int32)
+    ok = dict(cfg=cfg, layer=0, weights=a["layers"][0], cu_seqlens=cu,
+              layer_on=np.ones(2, np.uint8), head_mask=np.ones((2, 4), np.uint8),
+              ffn_mask=np.ones((2, 4), np.uint8), resid=torch.zeros((23, D)), ws=a["ws"])
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        svl.svl_layer_forward(**ok)
+    for bad, match in ((dict(resid=torch.zeros((22, D))), "resid holds"),
+                       (dict(head_mask=np.ones((2, 3), np.uint8)), "head_mask has shape"),
+                       (dict(layer_on=np.ones(3, np.uint8)), "layer_on has shape"),
+                       (dict(weights={**a["layers"][0], "wo": a["layers"][0]["wo"].float()}),
+                        "wo has dtype")):
+        with pytest.raises(ValueError, match=match):
+            svl.svl_layer_forward(**{**ok, **bad})
+    # decode: x not [B][D] float32, cache_len of the wrong length
+    x = torch.zeros((2, D))
+    dec = dict(cfg=cfg, layers=a["layers"], x=x, cache_len=np.array([3, 4], np.int32),
+               layer_mask=a["layer_mask"], head_mask=a["head_mask"], ffn_mask=a["ffn_mask"],
+               kv_cache=torch.zeros(svl.svl_kv_cache_bytes(cfg, 2, 16), dtype=torch.uint8),
+               max_len=16, ws=a["ws"])
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        svl.svl_decode_step(**dec)
+    for bad, match in ((dict(x=torch.zeros((2, D), dtype=torch.float64)), "x has dtype"),
+                       (dict(cache_len=np.array([3], np.int32)), "cache_len has shape"),
+                       (dict(kv_cache=torch.zeros(100, dtype=torch.uint8)), "kv_cache holds")):
+        with pytest.raises(ValueError, match=match):
+            svl.svl_decode_step(**{**dec, **bad})
