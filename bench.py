@@ -41,9 +41,14 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default=None)
     p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--compute", choices=("f16", "bf16"), default="f16",
+                   help="activation / matrix-input type of the 16-bit path (fp16 or bf16 MFMA)")
+    p.add_argument("--no-bf16-line", action="store_true",
+                   help="skip the extra timing of the headline with bf16 activations")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=3,
-                   help="executed layers the CPU-baseline sample runs")
+    p.add_argument("--cpu-layers", type=int, default=0,
+                   help="executed layers the CPU-baseline sample runs (0: all of them, no "
+                        "extrapolation; the headline's 24 take about 20 s on 16 host threads)")
     p.add_argument("--traffic-from", default=None,
                    help="directory holding fetch/ and write/ rocprofv3 --pmc FETCH_SIZE / "
                         "WRITE_SIZE runs of `bench.py --copy-calibration`: write the gate/up "
@@ -205,7 +210,7 @@ def gemm_bytes(shape, seqlens, layer_mask, head_mask, ffn_mask):
 
 
 def cpu_baseline(w, inp, layers, n_exec_layers):
-    """The CPU oracle on the first `n_exec_layers` executed layers of the same
+    """The CPU oracle on the first `n_exec_layers` executed layers (0: all) of the same
     inputs (selection and packing included); the rate is scaled to the whole
     prefill by the executed-layer count."""
     import oracle
@@ -215,9 +220,22 @@ def cpu_baseline(w, inp, layers, n_exec_layers):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count()
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        nproc = os.cpu_count()
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
     B = w.batch
     executed = [l for l in range(w.shape.n_layers) if inp.layer_mask[:, l].any()]
-    sample = executed[:n_exec_layers]
+    sample = executed[:n_exec_layers] if n_exec_layers > 0 else executed
     host = {}
     for l in sample:
         host[l] = {k: W.as_f32(v) for k, v in layers[l].items()}
@@ -229,9 +247,31 @@ def cpu_baseline(w, inp, layers, n_exec_layers):
     est = dt * len(executed) / max(1, len(sample))
     tokens = B * (w.n_vision + w.n_text)
     return {"value": tokens / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "nproc": int(nproc), "os_cpu_count": os.cpu_count(), "blas_threads": int(threads),
+            "cpu_model": model,
+            "layers_timed": len(sample), "layers_executed": len(executed),
+            "seconds_timed": round(dt, 2),
             "sample": f"{len(sample)} of {len(executed)} executed layers (float64 numpy oracle, "
-                      f"selection and packing included), {dt:.1f} s, rate scaled by "
+                      f"selection and packing included), {dt:.1f} s on {threads} BLAS threads "
+                      f"({nproc} usable cores, {model}), rate scaled by "
                       f"{len(executed)}/{len(sample)}"}
+
+
+def eq8_flops(shape, seqlens, layer_mask, head_mask, n_vision, n_text):
+    """The paper's estimator, Eq. (8), with V = 0 (no LM head): per sample,
+    sum_l alpha_l [(8 D^2 + 6 D F) S + 4 D S^2], alpha_l = active query heads
+    / A (0 for a skipped layer), S the sample's executed sequence length; and
+    the same at full capacity (every alpha_l = 1, S = N + T).  Reported next
+    to the executed (causal) count for comparison with the paper's figures."""
+    D, F, A, L = shape.d_model, shape.d_ffn, shape.n_heads, shape.n_layers
+    per_s = lambda S: (8 * D * D + 6 * D * F) * S + 4 * D * S * S
+    pruned = 0.0
+    for b, S in enumerate(seqlens):
+        for l in range(L):
+            if layer_mask[b][l]:
+                pruned += float(np.sum(head_mask[b][l])) / A * per_s(int(S))
+    full = len(seqlens) * L * per_s(n_vision + n_text)
+    return int(round(pruned)), int(full)
 
 
 def memory_sweep(args):
@@ -551,7 +591,7 @@ def main():
     inp = W.draw_inputs(w, args.seed, device=dev)
     layers = [W.draw_layer_weights(w, l, args.seed, device=dev) for l in range(shape.n_layers)]
     table = svl.LayerTable(layers)
-    cfg = svl.make_config(shape)
+    cfg = svl.make_config(shape, compute=args.compute)
     B, N = inp.scores.shape
     seqlens = (inp.keep + w.n_text).astype(np.int64)
     R = int(seqlens.sum())
@@ -632,6 +672,28 @@ def main():
     print(f"# timed {args.steps} steps: {ms:.4f} ms/step (wall {1e3 * t_wall / args.steps:.4f})",
           file=sys.stderr, flush=True)
 
+    bf16_line = None
+    if (not args.no_bf16_line and args.compute == "f16" and shape.dtype == "bf16"
+            and args.threshold_budget is None and args.controller is None):
+        # the same step with bf16 activations and bf16 MFMA products
+        cfg16 = cfg
+        cfg = svl.make_config(shape, compute="bf16")
+        for _ in range(max(1, args.warmup)):
+            step()
+        torch.cuda.synchronize()
+        eb0, eb1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        eb0.record(stream)
+        for _ in range(args.steps):
+            step()
+        eb1.record(stream)
+        torch.cuda.synchronize()
+        ms_b = eb0.elapsed_time(eb1) / args.steps
+        tok = B * (w.n_vision + w.n_text)
+        bf16_line = {"compute": "bf16 activations, bf16 MFMA", "ms_per_step": round(ms_b, 4),
+                     "value": round(tok / (ms_b * 1e-3), 1), "unit": "tokens/s"}
+        cfg = cfg16
+        print(f"# bf16 compute: {ms_b:.4f} ms/step", file=sys.stderr, flush=True)
+
     # second pass, same steps, every launch bracketed by HIP events on `stream`
     svl.svl_timing_enable(True)
     for _ in range(args.steps):
@@ -663,6 +725,7 @@ def main():
         flops = svl.svl_count_flops(cfg, seqlens, lm_run, hm_run, fm_run)
         bytes_, launches = gemm_bytes(shape, seqlens, lm_run, hm_run, fm_run)
     gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
+    eq8 = eq8_flops(shape, seqlens, lm_run, hm_run, w.n_vision, w.n_text)
     gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / args.steps
     attn_ms = ktime["attention"][0] / args.steps
     tokens = B * (w.n_vision + w.n_text)
@@ -701,7 +764,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16" if shape.dtype == "bf16" else "f32",
+        "dtype": ("f16" if args.compute == "f16" else "bf16") if shape.dtype == "bf16" else "f32",
         "storage_dtype": shape.dtype,
         "data": "synthetic",
         "config": {"workload": workload,
@@ -714,6 +777,10 @@ def main():
         "kept_tokens_per_s": round(R / (ms * 1e-3), 1),
         "executed_tflops": round(flops["total"] / (ms * 1e-3) / 1e12, 2),
         "executed_flops_per_step": flops["total"],
+        "eq8_flops_per_step": eq8[0],
+        "eq8_flops_full_capacity": eq8[1],
+        "eq8_note": "the paper's estimator, Eq. (8), V = 0: non-causal 4 D S^2 and alpha on "
+                    "every projection (the executed count is the causal closed form)",
         "mfma_util_gemm_pct": round(100 * gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2),
         "mfma_util_attn_pct": round(100 * flops["attn"] / (attn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 3)
         if attn_ms > 0 else None,
@@ -746,6 +813,8 @@ def main():
             "layers_skipped": int((lm_run == 0).sum()),
             "step": "stats kernel + sync + prefix layers + controller head + sync + projection "
                     "+ row compaction + remaining layers"}
+    if bf16_line is not None:
+        result["bf16_compute"] = bf16_line
     if not args.no_cpu_baseline and default_mode:
         result["cpu_baseline"] = cpu_baseline(w, inp, layers, args.cpu_layers)
     print(json.dumps(result))
