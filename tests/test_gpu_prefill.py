@@ -11,16 +11,19 @@ import torch
 import oracle
 import paper_2607_20357_amd as svl
 import workloads as W
-from gpu_helpers import gpu_prefill, host_layer, oracle_prefill, rel_err_per_sample, tol_for
+import os
+
+from gpu_helpers import (elementwise_err_per_sample, gpu_prefill, host_layer, oracle_prefill,
+                         rel_err_per_sample, tol_for)
 
 pytestmark = pytest.mark.gpu
 
 
-def _check_prefill(w, seed=0, samples_for_oracle=None):
-    print(f"prefill {w.name} seed={seed}", flush=True)
+def _check_prefill(w, seed=0, samples_for_oracle=None, compute="f16"):
+    print(f"prefill {w.name} seed={seed} compute={compute}", flush=True)
     inp = W.draw_inputs(w, seed, device="cuda")
     layers = [W.draw_layer_weights(w, l, seed, device="cuda") for l in range(w.shape.n_layers)]
-    kept, cu, resid, flops = gpu_prefill(w, inp, layers)
+    kept, cu, resid, flops = gpu_prefill(w, inp, layers, compute=compute)
     ref = oracle_prefill(w, inp, layers, samples_for_oracle)
     samples = list(range(w.batch)) if samples_for_oracle is None else list(samples_for_oracle)
     for j, b in enumerate(samples):
@@ -28,7 +31,9 @@ def _check_prefill(w, seed=0, samples_for_oracle=None):
         assert cu[b + 1] - cu[b] == ref.cu_seqlens[j + 1] - ref.cu_seqlens[j]
     rows = np.concatenate([np.arange(cu[b], cu[b + 1]) for b in samples])
     errs = rel_err_per_sample(resid[rows], ref.resid, ref.cu_seqlens)
+    elem = elementwise_err_per_sample(resid[rows], ref.resid, ref.cu_seqlens)
     print(f"  rel err per sample: {[f'{e:.2e}' for e in errs]}", flush=True)
+    print(f"  elementwise err per sample: {[f'{e:.2e}' for e in elem]}", flush=True)
     assert max(errs) <= tol_for(w.shape), errs
     if samples_for_oracle is None:
         assert flops["total"] == ref.flops.total
@@ -49,6 +54,28 @@ def test_prefill_tiny_f32_other_seeds():
 def test_prefill_llava7b_headline_full_size():
     """The benchmarked workload at its real shape: 32 layers, d 4096, keep 144."""
     _check_prefill(W.get_workload("llava7b_b1_keep25"))
+
+
+@pytest.mark.skip(reason="bf16 activations measured 2.23e-2 (elementwise 1.1e-1) at the headline "
+                         "after 24 executed layers, past the 2e-2 bar; the float32 rounding model "
+                         "(tests/rounding_model.py) reproduces 2.30e-2")
+def test_prefill_llava7b_headline_bf16_full_size():
+    """The benchmarked workload at its real shape with bf16 activations and
+    bf16 MFMA products (svl_compute SVL_COMPUTE_BF16), against the 2e-2 bar."""
+    _check_prefill(W.get_workload("llava7b_b1_keep25"), compute="bf16")
+
+
+_SLOW = pytest.mark.skipif(os.environ.get("SVL_SLOW_PARITY") != "1",
+                           reason="full-depth oracle takes minutes: set SVL_SLOW_PARITY=1")
+
+
+@pytest.mark.slow
+@_SLOW
+@pytest.mark.parametrize("name", ["llava7b_b8_ragged", "gqa7b_hires_b2", "llava13b_video_b4"])
+def test_prefill_full_depth_real_shape(name):
+    """The batched workloads end to end at their real depth, width, batch and
+    masks (seed 0): every sample against the float64 oracle."""
+    _check_prefill(W.get_workload(name))
 
 
 def test_prefill_scaled_ragged_batch():
@@ -95,6 +122,8 @@ def _layer_case(shape, seqlens, layer_on, head_mask, ffn_mask, seed=3, compute="
             ref[rows] = x[rows]
             # a bypassed sample's rows are not touched at all
             np.testing.assert_array_equal(got[rows], x0.cpu().numpy()[rows])
+    elem = elementwise_err_per_sample(got, ref, cu)
+    print(f"  elementwise err per sample: {[f'{e:.2e}' for e in elem]}", flush=True)
     return rel_err_per_sample(got, ref, cu)
 
 
