@@ -405,6 +405,30 @@ svl_status svl_decode_step(const svl_config *cfg, const svl_layer_weights *layer
                            const uint8_t *ffn_mask, void *kv_cache, int32_t max_len,
                            void *ws, size_t ws_bytes, void *stream);
 
+/* Allocation-free decode step, for callers that cannot allocate device
+ * memory between steps (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same computation, kernels and
+ * results as svl_decode_step, with its workspace taken from a device array
+ * of SVL_NOALLOC_SCRATCH_BYTES inside the library instead of a caller
+ * buffer.  Arguments as svl_decode_step without ws / ws_bytes.
+ *   - Calls no hipMalloc, hipFree or other allocating routine; the step's
+ *     plan is copied from host memory with an ordinary stream copy.
+ *   - The array exists once per GPU the library runs on and is held until
+ *     the process ends.  Its device address on the current GPU is looked up
+ *     on the first call there.
+ *   - Every call on one GPU uses that GPU's array and leaves the last call's
+ *     contents in it (nothing in it needs to start at zero): calls that
+ *     overlap on one GPU (several host threads or streams) race and must be
+ *     serialised by the caller.
+ *   - A shape whose decode workspace (svl_decode_workspace_bytes) exceeds
+ *     the array returns SVL_E_WORKSPACE before anything is enqueued. */
+#define SVL_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+svl_status svl_decode_step_noalloc(const svl_config *cfg, const svl_layer_weights *layers,
+                                   int32_t batch, float *x, const int32_t *cache_len,
+                                   const uint8_t *layer_mask, const uint8_t *head_mask,
+                                   const uint8_t *ffn_mask, void *kv_cache, int32_t max_len,
+                                   void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *svl_last_error(void);
 

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libsvl.so")
 
 SVL_F32, SVL_BF16 = 0, 1
 SVL_COMPUTE_F16, SVL_COMPUTE_BF16 = 0, 1
+SVL_NOALLOC_SCRATCH_BYTES = 64 << 20   # include/svl.h
 KCLASS = {"select": 0, "gather": 1, "rmsnorm": 2, "gemm_qkv": 3, "attention": 4, "gemm_o": 5,
           "gemm_gate_up": 6, "gemm_down": 7, "rope_table": 8, "finish": 9, "kv_append": 10,
           "controller": 11}
@@ -102,6 +103,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                       P, P, P, P, P, P, P, P, ctypes.POINTER(i32), P, i32, P, sz, P]
     lib.svl_decode_step.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), i32, P, P, P, P, P, P,
                                     i32, P, sz, P]
+    lib.svl_decode_step_noalloc.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights), i32, P, P, P,
+                                            P, P, P, i32, P]
     lib.svl_kv_cache_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_kv_cache_bytes.restype = sz
     lib.svl_decode_workspace_bytes.argtypes = [cfgp, i32, i32]
@@ -128,7 +131,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(ctypes.c_int64)]
     for f in ("svl_select_tokens", "svl_layer_forward", "svl_prefill", "svl_count_flops",
               "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
-              "svl_prefill_cache", "svl_decode_step", "svl_prefill_controlled",
+              "svl_prefill_cache", "svl_decode_step", "svl_decode_step_noalloc",
+              "svl_prefill_controlled",
               "svl_budget_loss"):
         getattr(lib, f).restype = i32
     _lib = lib
@@ -516,6 +520,30 @@ def svl_decode_step(cfg: svl_config, layers, x: torch.Tensor, cache_len, layer_m
         ctypes.byref(cfg), table.array, int(x.shape[0]), _dev(x, "x"),
         clp, lmp, hmp, fmp, _dev(kv_cache, "kv_cache"), int(max_len), _dev(ws, "ws"), _nbytes(ws),
         _stream(stream)))
+
+
+def svl_decode_step_noalloc(cfg: svl_config, layers, x: torch.Tensor, cache_len, layer_mask,
+                            head_mask, ffn_mask, kv_cache: torch.Tensor, max_len: int,
+                            stream=None) -> None:
+    """svl_decode_step on the library's own device scratch (no workspace
+    argument; the library allocates nothing).  Calls on one GPU share that
+    scratch, so overlapping calls must be serialised by the caller."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x must be a [B][D] tensor")
+    B = int(x.shape[0])
+    L, A, G = cfg.n_layers, cfg.n_heads, cfg.n_groups
+    _expect(x, "x", torch.float32, B * cfg.d_model, (B, cfg.d_model))
+    _expect(kv_cache, "kv_cache", torch.uint8, svl_kv_cache_bytes(cfg, B, max_len))
+    cl, clp = _host_i32(cache_len)
+    if cl.shape != (B,):
+        raise ValueError(f"cache_len has shape {cl.shape}, expected ({B},)")
+    lm, lmp = _host_mask(layer_mask, "layer_mask", (B, L))
+    hm, hmp = _host_mask(head_mask, "head_mask", (B, L, A))
+    fm, fmp = (None, None) if ffn_mask is None else _host_mask(ffn_mask, "ffn_mask", (B, L, G))
+    table = _table(cfg, layers)
+    _check(load_library().svl_decode_step_noalloc(
+        ctypes.byref(cfg), table.array, B, _dev(x, "x"), clp, lmp, hmp, fmp,
+        _dev(kv_cache, "kv_cache"), int(max_len), _stream(stream)))
 
 
 def svl_timing_enable(on: bool) -> None:

@@ -125,6 +125,7 @@ struct WsLayout {
 // Activation buffers use the padded row space (16-row blocks per sample on
 // the 16-bit MFMA path); the partial region holds the float32 split-K slices.
 // pos_rows: RoPE table rows (positions) when they exceed R (decode: max_len).
+// Decode (pos_rows > 0) never splits K, so its layout has no partial region.
 WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows = 0) {
   const int64_t es = c.dtype == SVL_BF16 ? 2 : 4;
   const int64_t prow = std::max<int64_t>(padded_rows_bound(c, B, R), 16);
@@ -137,7 +138,7 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows =
   };
   L.plan = take(plan_bytes_bound(c, B, R, c.n_layers));
   L.rope = take(std::max<int64_t>(std::max(R, pos_rows), 1) * (c.head_dim / 2) * 8);
-  L.partial = take(partial_floats_bound(c, B, R) * 4);
+  L.partial = take(pos_rows > 0 ? 0 : partial_floats_bound(c, B, R) * 4);
   L.partial_slice = (int64_t)R * c.d_model;
   L.prows = prow;
   L.xn = take(prow * c.d_model * es);
@@ -421,11 +422,17 @@ hipError_t upload_plan(uint8_t* dst, const uint8_t* src, size_t n, hipStream_t s
   return hipSuccess;
 }
 
-// Copies the plan image and builds the RoPE table.
-svl_status stage(const Exec& ex, bool need_layers) {
+// Copies the plan image and builds the RoPE table.  pageable: copy straight
+// from the plan's host memory (the allocation-free entry point; a copy from
+// pageable memory has consumed its source when the call returns) instead of
+// through the pinned buffers, which are allocated on first use.
+svl_status stage(const Exec& ex, bool need_layers, bool pageable = false) {
   if ((int64_t)ex.plan.image.size() > ex.L.rope - ex.L.plan)
     return fail(SVL_E_SHAPE, "internal: plan image exceeds its workspace region");
-  hipError_t e = upload_plan(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(), ex.st);
+  hipError_t e =
+      pageable ? hipMemcpyAsync(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(),
+                                hipMemcpyHostToDevice, ex.st)
+               : upload_plan(ex.ws + ex.L.plan, ex.plan.image.data(), ex.plan.image.size(), ex.st);
   if (e != hipSuccess) return hip_fail(e, "plan upload");
   if (need_layers) {
     e = timed(K_ROPE, ex.st, [&] {
@@ -729,17 +736,53 @@ size_t svl_decode_workspace_bytes(const svl_config* cfg, int32_t batch, int32_t 
   return (size_t)ws_layout(*cfg, batch, batch, max_len).total;
 }
 
-svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layers, int32_t batch,
-                           float* x, const int32_t* cache_len, const uint8_t* layer_mask,
-                           const uint8_t* head_mask, const uint8_t* ffn_mask, void* kv_cache,
-                           int32_t max_len, void* ws, size_t ws_bytes, void* stream) {
+// Device scratch of svl_decode_step_noalloc: one copy per GPU, held until
+// the process ends.  In host code `noalloc_scratch` names a host-side stand-in,
+// not device memory: every host use goes through the device address that
+// hipGetSymbolAddress returns on each GPU (scratch_address below).
+static __device__ __align__(256) uint8_t noalloc_scratch[SVL_NOALLOC_SCRATCH_BYTES];
+
+namespace svl {
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the scratch array on the current GPU, looked up once per
+// device (with that device current) and kept.
+svl_status scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SVL_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SVL_E_HIP, "device index %d unsupported", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch));
+    if (e != hipSuccess || !p)
+      return fail(SVL_E_HIP, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SVL_OK;
+}
+}  // namespace
+}  // namespace svl
+
+// ws == nullptr: the allocation-free variant (the library's scratch array,
+// the plan copied from pageable host memory).
+static svl_status decode_impl(const svl_config* cfg, const svl_layer_weights* layers, int32_t batch,
+                              float* x, const int32_t* cache_len, const uint8_t* layer_mask,
+                              const uint8_t* head_mask, const uint8_t* ffn_mask, void* kv_cache,
+                              int32_t max_len, void* ws, size_t ws_bytes, void* stream,
+                              bool noalloc) {
   svl_status s = check_config(cfg);
   if (s != SVL_OK) return s;
   if (cfg->dtype != SVL_BF16) return fail(SVL_E_DTYPE, "decode runs on the 16-bit path only");
   if (batch <= 0) return fail(SVL_E_SHAPE, "batch must be positive");
-  if (!x || !cache_len || !layer_mask || !head_mask || !kv_cache || !ws)
+  if (!x || !cache_len || !layer_mask || !head_mask || !kv_cache || (!noalloc && !ws))
     return fail(SVL_E_NULL, "NULL argument");
-  if (!aligned16(x) || !aligned16(kv_cache) || !aligned16(ws))
+  if (!aligned16(x) || !aligned16(kv_cache) || (!noalloc && !aligned16(ws)))
     return fail(SVL_E_ALIGN, "device pointers must be 16-byte aligned");
   if (max_len <= 0 || max_len > 32768) return fail(SVL_E_SHAPE, "max_len outside [1, 32768]");
   for (int32_t b = 0; b < batch; ++b)
@@ -751,6 +794,15 @@ svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layer
   if ((s = check_mask(head_mask, (int64_t)batch * L * A, "head_mask")) != SVL_OK) return s;
   if (ffn_mask && (s = check_mask(ffn_mask, (int64_t)batch * L * G, "ffn_mask")) != SVL_OK) return s;
   const WsLayout WL = ws_layout(*cfg, batch, batch, max_len);
+  if (noalloc) {
+    if (WL.total > (int64_t)SVL_NOALLOC_SCRATCH_BYTES)
+      return fail(SVL_E_WORKSPACE,
+                  "decode of %d samples with max_len %d needs %lld workspace bytes, the "
+                  "allocation-free scratch holds %zu",
+                  batch, max_len, (long long)WL.total, (size_t)SVL_NOALLOC_SCRATCH_BYTES);
+    if ((s = scratch_address(&ws)) != SVL_OK) return s;
+    ws_bytes = SVL_NOALLOC_SCRATCH_BYTES;
+  }
   if ((int64_t)ws_bytes < WL.total)
     return fail(SVL_E_WORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)WL.total);
   std::vector<int32_t> seq(batch, 1);
@@ -765,7 +817,7 @@ svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layer
   ex.max_len = max_len;
   ex.batch = batch;
   ex.decode = true;
-  if ((s = stage(ex, true)) != SVL_OK) return s;
+  if ((s = stage(ex, true, noalloc)) != SVL_OK) return s;
   for (int32_t l = 0; l < L; ++l) {
     hipError_t e = ex.layer(t_plan.layers[l], layers[l], l);
     if (e != hipSuccess) return hip_fail(e, "layer launch");
@@ -773,6 +825,23 @@ svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layer
   hipError_t e = ex.norm(t_plan.final_norm, nullptr);
   if (e != hipSuccess) return hip_fail(e, "final residual launch");
   return SVL_OK;
+}
+
+svl_status svl_decode_step(const svl_config* cfg, const svl_layer_weights* layers, int32_t batch,
+                           float* x, const int32_t* cache_len, const uint8_t* layer_mask,
+                           const uint8_t* head_mask, const uint8_t* ffn_mask, void* kv_cache,
+                           int32_t max_len, void* ws, size_t ws_bytes, void* stream) {
+  return decode_impl(cfg, layers, batch, x, cache_len, layer_mask, head_mask, ffn_mask, kv_cache,
+                     max_len, ws, ws_bytes, stream, false);
+}
+
+svl_status svl_decode_step_noalloc(const svl_config* cfg, const svl_layer_weights* layers,
+                                   int32_t batch, float* x, const int32_t* cache_len,
+                                   const uint8_t* layer_mask, const uint8_t* head_mask,
+                                   const uint8_t* ffn_mask, void* kv_cache, int32_t max_len,
+                                   void* stream) {
+  return decode_impl(cfg, layers, batch, x, cache_len, layer_mask, head_mask, ffn_mask, kv_cache,
+                     max_len, nullptr, 0, stream, true);
 }
 
 svl_status svl_count_positive(int32_t batch, int32_t n_vision, const float* logits,

@@ -416,7 +416,8 @@ bool build_plan(const svl_config& cfg, int32_t B, const int32_t* keep, const int
     *err = "a sample's Q/K/V rows span 2 GiB or more (attention addresses them with 32-bit offsets)";
     return false;
   }
-  const int64_t cap = partial_floats_bound(cfg, B, R);
+  // split-K partial slices the workspace holds (decode: none, it never splits)
+  const int64_t cap = rowvec ? 0 : partial_floats_bound(cfg, B, R);
   int32_t force_split = 1;
   if (const char* e = std::getenv("SVL_PAIRED_SPLIT")) force_split = std::max(1, std::min(4, std::atoi(e)));
   // 8-row-group norm kernel: 16-bit output, d_model % 256 == 0 and <= 8192

@@ -402,3 +402,31 @@ def test_binding_select_layer_decode_reject_mismatched_tensors():
                        (dict(kv_cache=torch.zeros(100, dtype=torch.uint8)), "kv_cache holds")):
         with pytest.raises(ValueError, match=match):
             svl.svl_decode_step(**{**dec, **bad})
+
+
+def test_noalloc_decode_rejects_shapes_past_its_scratch_on_the_host():
+    """svl_decode_step_noalloc checks its decode workspace against the
+    library's scratch size before anything else touches the GPU (fake,
+    never dereferenced device pointers)."""
+    lib = svl.load_library()
+    cfg = svl.make_config(n_layers=2, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128,
+                          d_ffn=11008, n_groups=4, dtype="bf16")
+    P = ctypes.c_void_p
+    ptr = 16 * 4096
+    fake = binding.svl_layer_weights(*([ptr] * 9))
+    table = (binding.svl_layer_weights * 2)(fake, fake)
+    for B, max_len, fits in ((64, 64, False), (1, 40000, None)):
+        need = lib.svl_decode_workspace_bytes(ctypes.byref(cfg), B, max_len)
+        if fits is False:
+            assert need > binding.SVL_NOALLOC_SCRATCH_BYTES
+        cl = np.zeros(B, np.int32)
+        lm = np.ones((B, 2), np.uint8)
+        hm = np.ones((B, 2, 32), np.uint8)
+        st = lib.svl_decode_step_noalloc(ctypes.byref(cfg), table, B, P(ptr), cl.ctypes.data_as(P),
+                                         lm.ctypes.data_as(P), hm.ctypes.data_as(P), None, P(ptr),
+                                         max_len, None)
+        msg = lib.svl_last_error().decode()
+        if fits is False:
+            assert st == 4 and "allocation-free scratch" in msg, msg
+        else:
+            assert st == 2 and "max_len" in msg, msg      # max_len past 32768
