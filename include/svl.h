@@ -353,6 +353,68 @@ svl_status svl_budget_loss(const svl_config *cfg, const svl_budget_loss_params *
                            uint8_t *token_mask, uint8_t *unit_mask, float *ratio, float *loss,
                            float *grad_logits, float *grad_gate, void *stream);
 
+/* ---- training-time masked decoder ----------------------------------------
+ * The prediction side of a training step (Sec. 3.1 Eq. (6); Sec. 3.2).  The
+ * sequences keep their length: sample b is S = N + T rows, its N vision
+ * embeddings each multiplied by the forward value of its straight-through
+ * token mask m_i = 1[z_i + xi_i > 0] (a dropped token becomes a zero row),
+ * then its T text embeddings, at positions 0..S-1.  Every decoder layer
+ * computes every head and every FFN channel; in the controlled layers
+ * l >= P, unit u's mask M_lu = 1[g_lu + xi_lu > 0] multiplies the attention
+ * output of the heads of group u (heads [u A/U, (u+1) A/U)) before the output
+ * projection and the SwiGLU output of FFN slice u (channels [u F/U,
+ * (u+1) F/U)) before the down projection.  U = n_groups is the layer-head
+ * controller; U = 1 is the layer controller (M_l = 0 makes layer l the
+ * identity).  Layers 0..P-1 run with every mask at 1.
+ *
+ * Given an upstream gradient G of the final hidden states (the prediction
+ * loss, outside the library, as dL/dX_L), the call runs the backward of that
+ * decoder, with the masks treated as numbers, and applies the straight-
+ * through estimator:
+ *   dL/dz_i  = (sum_d dL/dX0[i][d] v_i[d]) y_i (1 - y_i) / tau_tok,
+ *   dL/dg_lu = dL/dM_lu y_lu (1 - y_lu) / tau_comp,
+ * with y = sigma((logit + xi) / tau).  The budget term's gradient
+ * (svl_budget_loss) is separate; the total gradient is the sum.
+ *
+ * Arithmetic: float32 throughout (weights and embeddings widened exactly
+ * from the storage dtype; svl_config.compute is ignored); the forward of each
+ * layer is recomputed from its stored input during the backward.
+ * Requirements beyond the config's: head_dim in {32, 64, 128}; d_model and
+ * d_ffn multiples of 16; n_heads and d_ffn divisible by units, d_ffn / units
+ * a multiple of 4 (SVL_E_SHAPE otherwise). */
+typedef struct {
+  float tau_tok;     /* token temperature, finite and > 0 */
+  float tau_comp;    /* compute temperature, finite and > 0 */
+  int32_t prefix;    /* P, 0 <= P <= n_layers */
+  int32_t units;     /* U >= 1 */
+} svl_train_params;
+
+/* Workspace bytes of svl_train_step for `batch` samples of n_vision + n_text
+ * rows (0 on bad arguments): the input of every layer, one layer's forward
+ * intermediates and its gradients, all float32. */
+size_t svl_train_workspace_bytes(const svl_config *cfg, const svl_train_params *params,
+                                 int32_t batch, int32_t n_vision, int32_t n_text);
+
+/* One training step of the masked decoder (all pointers dev, row-major):
+ *   logits       float [B][N] token logits z;  token_noise float [B][N] or NULL
+ *   gate_logits  float [B][(L-P) U] (layer-major);  gate_noise same or NULL
+ *   vision       dtype [B][N][D];  text dtype [B][T][D]
+ *   grad_hidden  float [B][S][D]: dL/dX_L, or NULL for the forward only
+ *   hidden       float [B][S][D] (out): X_L
+ *   token_mask   uint8 [B][N] (out);  unit_mask uint8 [B][(L-P) U] (out)
+ *   grad_logits  float [B][N] (out, when grad_hidden is given)
+ *   grad_gate    float [B][(L-P) U] (out, when grad_hidden is given)
+ *   ws/ws_bytes: at least svl_train_workspace_bytes(...).
+ * Arrays with no elements (N = 0, or (L-P) U = 0) may be NULL.  Enqueued on
+ * `stream`; nothing is synchronised. */
+svl_status svl_train_step(const svl_config *cfg, const svl_layer_weights *layers,
+                          const svl_train_params *params, int32_t batch, int32_t n_vision,
+                          int32_t n_text, const float *logits, const float *token_noise,
+                          const float *gate_logits, const float *gate_noise, const void *vision,
+                          const void *text, const float *grad_hidden, float *hidden,
+                          uint8_t *token_mask, uint8_t *unit_mask, float *grad_logits,
+                          float *grad_gate, void *ws, size_t ws_bytes, void *stream);
+
 /* ---- decode on the pruned and gated KV cache ----------------------------
  * After the prefill, tokens are generated one at a time; the paper leaves
  * this stage to future work (Sec. 5).  The cache holds only what the prefill

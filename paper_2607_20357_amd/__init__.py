@@ -11,5 +11,6 @@ from .binding import (  # noqa: F401
     svl_budget_loss, svl_budget_loss_params, svl_budget_project, svl_controlled_workspace_bytes, svl_count_flops, svl_count_positive,
     svl_decode_step, svl_decode_step_noalloc, svl_kv_cache_bytes, svl_layer_forward, svl_prefill, svl_prefill_cache,
     svl_prefill_controlled, svl_select_tokens, svl_timing_enable, svl_timing_read,
-    svl_workspace_bytes,
+    svl_workspace_bytes, alloc_train_workspace, svl_train_params, svl_train_step,
+    svl_train_workspace_bytes,
 )

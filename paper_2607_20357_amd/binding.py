@@ -70,6 +70,11 @@ class svl_budget_loss_params(ctypes.Structure):
                 ("units", ctypes.c_int32), ("vocab", ctypes.c_int64)]
 
 
+class svl_train_params(ctypes.Structure):
+    _fields_ = [("tau_tok", ctypes.c_float), ("tau_comp", ctypes.c_float),
+                ("prefix", ctypes.c_int32), ("units", ctypes.c_int32)]
+
+
 class svl_flops(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in ("q", "kv", "o", "attn", "ffn", "total")]
 
@@ -120,6 +125,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                            P, P, P, P, ctypes.POINTER(svl_flops), P, sz, P]
     lib.svl_budget_loss.argtypes = [cfgp, ctypes.POINTER(svl_budget_loss_params), i32, i32, i32,
                                     P, P, P, P, P, P, P, P, P, P, P]
+    lib.svl_train_workspace_bytes.argtypes = [cfgp, ctypes.POINTER(svl_train_params), i32, i32, i32]
+    lib.svl_train_workspace_bytes.restype = sz
+    lib.svl_train_step.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights),
+                                   ctypes.POINTER(svl_train_params), i32, i32, i32, P, P, P, P, P,
+                                   P, P, P, P, P, P, P, P, sz, P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_workspace_bytes.restype = sz
     lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
@@ -133,7 +143,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
               "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
               "svl_prefill_cache", "svl_decode_step", "svl_decode_step_noalloc",
               "svl_prefill_controlled",
-              "svl_budget_loss"):
+              "svl_budget_loss", "svl_train_step"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -660,4 +670,67 @@ def svl_budget_loss(cfg: svl_config, params: svl_budget_loss_params, logits: tor
         _dev(out["unit_mask"], "unit_mask"), _dev(out["ratio"], "ratio"), _dev(out["loss"], "loss"),
         _dev(out["grad_logits"], "grad_logits"), _dev(out["grad_gate"], "grad_gate"),
         _stream(stream)))
+    return out
+
+
+def svl_train_workspace_bytes(cfg: svl_config, params: svl_train_params, batch: int,
+                              n_vision: int, n_text: int) -> int:
+    n = load_library().svl_train_workspace_bytes(ctypes.byref(cfg), ctypes.byref(params),
+                                                 int(batch), int(n_vision), int(n_text))
+    if n == 0:
+        raise SvlError(2, "svl_train_workspace_bytes: " + load_library().svl_last_error().decode())
+    return int(n)
+
+
+def alloc_train_workspace(cfg: svl_config, params: svl_train_params, batch: int, n_vision: int,
+                          n_text: int, device="cuda") -> torch.Tensor:
+    n = svl_train_workspace_bytes(cfg, params, batch, n_vision, n_text)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def svl_train_step(cfg: svl_config, layers, params: svl_train_params, logits: torch.Tensor,
+                   gate_logits: Optional[torch.Tensor], vision: torch.Tensor, text: torch.Tensor,
+                   grad_hidden: Optional[torch.Tensor], ws: torch.Tensor, token_noise=None,
+                   gate_noise=None, stream=None) -> Dict[str, torch.Tensor]:
+    """Training step of the masked decoder (svl_train_step in svl.h).  Returns
+    device tensors hidden [B][S][D], token_mask, unit_mask and, with
+    grad_hidden, grad_logits [B][N] and grad_gate [B][(L-P) U]."""
+    if not isinstance(logits, torch.Tensor) or logits.dim() != 2:
+        raise ValueError("logits must be a [B][N] tensor")
+    if not isinstance(text, torch.Tensor) or text.dim() != 3:
+        raise ValueError("text must be a [B][T][D] tensor")
+    B, N = logits.shape
+    T = text.shape[1]
+    S, D = N + T, cfg.d_model
+    nl = (cfg.n_layers - params.prefix) * params.units
+    dt = storage_dtype(cfg)
+    _expect(logits, "logits", torch.float32, B * N, (B, N))
+    _expect(vision, "vision", dt, B * N * D, (B, N, D))
+    _expect(text, "text", dt, B * T * D, (B, T, D))
+    if token_noise is not None:
+        _expect(token_noise, "token_noise", torch.float32, B * N, (B, N))
+    if nl > 0:
+        _expect(gate_logits, "gate_logits", torch.float32, B * nl, (B, nl))
+        if gate_noise is not None:
+            _expect(gate_noise, "gate_noise", torch.float32, B * nl, (B, nl))
+    if grad_hidden is not None:
+        _expect(grad_hidden, "grad_hidden", torch.float32, B * S * D, (B, S, D))
+    table = _table(cfg, layers)
+    dev = logits.device
+    out = {"hidden": torch.empty((B, S, D), dtype=torch.float32, device=dev),
+           "token_mask": torch.empty((B, N), dtype=torch.uint8, device=dev),
+           "unit_mask": torch.empty((B, nl), dtype=torch.uint8, device=dev)}
+    if grad_hidden is not None:
+        out["grad_logits"] = torch.empty((B, N), dtype=torch.float32, device=dev)
+        out["grad_gate"] = torch.empty((B, nl), dtype=torch.float32, device=dev)
+    opt = lambda t, n: None if t is None or t.numel() == 0 else _dev(t, n)
+    _check(load_library().svl_train_step(
+        ctypes.byref(cfg), table.array, ctypes.byref(params), int(B), int(N), int(T),
+        opt(logits, "logits"), opt(token_noise, "token_noise"),
+        None if nl == 0 else _dev(gate_logits, "gate_logits"),
+        None if nl == 0 else opt(gate_noise, "gate_noise"), opt(vision, "vision"),
+        opt(text, "text"), opt(grad_hidden, "grad_hidden"), _dev(out["hidden"], "hidden"),
+        opt(out["token_mask"], "token_mask"), opt(out["unit_mask"], "unit_mask"),
+        opt(out.get("grad_logits"), "grad_logits"), opt(out.get("grad_gate"), "grad_gate"),
+        _dev(ws, "ws"), _nbytes(ws), _stream(stream)))
     return out

@@ -21,7 +21,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["abi.cpp", "plan.cpp", "select_gather.hip", "norm_misc.hip", "gemm_mfma.hip",
            "attn_mfma.hip", "fp32_path.hip", "finish.hip", "budget.cpp", "attn_decode.hip",
-           "controller.hip", "budget_loss.hip", "gemv_decode.hip"]
+           "controller.hip", "budget_loss.hip", "gemv_decode.hip", "train_abi.cpp",
+           "train.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC",

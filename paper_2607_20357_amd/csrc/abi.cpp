@@ -517,6 +517,14 @@ void closed_form(const svl_config& c, int64_t S, const uint8_t* hm, const uint8_
 }
 
 }  // namespace
+
+// Error reporting and the config check, shared with the other C-ABI sources.
+svl_status set_error(svl_status st, const char* msg) {
+  g_err = msg;
+  return st;
+}
+svl_status validate_config(const svl_config* c) { return check_config(c); }
+
 }  // namespace svl
 
 using namespace svl;

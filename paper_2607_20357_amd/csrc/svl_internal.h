@@ -217,4 +217,9 @@ hipError_t launch_compact_rows(const CompactArgs& a, int32_t rows, hipStream_t s
 hipError_t launch_budget_loss(const BudgetLossArgs& a, int32_t B, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t st);
 
+// Shared by the C-ABI sources: sets the per-thread message of svl_last_error
+// and returns st; validates a config as every entry point does.
+svl_status set_error(svl_status st, const char* msg);
+svl_status validate_config(const svl_config* c);
+
 }  // namespace svl

@@ -1,0 +1,705 @@
+// Training-time masked decoder (Sec. 3.1 Eq. (6) with dropped tokens zeroed;
+// Sec. 3.2 unit masks over head groups and FFN slices, or whole layers):
+// float32 kernels for the static-shape forward and for its backward down to
+// the token and gate logits.
+//
+// Rows: a batch of B samples of S = N + T rows each, row m = b S + i, RoPE
+// position i.  Every head and FFN channel is computed; unit u of a layer
+// scales the attention output of its heads and the SwiGLU output of its FFN
+// slice (the matrix products read the scale with their A operand).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_util.h"
+#include "train_internal.h"
+
+namespace svl {
+namespace {
+
+constexpr int TNT = 256;
+
+// ------------------------------------------------------------------ loads
+template <class T>
+__device__ __forceinline__ float4 ld4(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float4 ld4<float>(const float* p, int64_t i) {
+  return *reinterpret_cast<const float4*>(p + i);
+}
+template <>
+__device__ __forceinline__ float4 ld4<uint16_t>(const uint16_t* p, int64_t i) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p + i);
+  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                     __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+}
+
+__device__ __forceinline__ float4 f4scale(float4 v, float s) {
+  return make_float4(v.x * s, v.y * s, v.z * s, v.w * s);
+}
+
+// Sum over the 256 threads of a workgroup, the same order on every call.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = warp_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// y (1 - y) / tau for y = sigma(v / tau), without cancellation on either side.
+__device__ __forceinline__ float ste_factor(float v, float tau) {
+  const float a = expf(-fabsf(v / tau));
+  return a / ((1.0f + a) * (1.0f + a)) / tau;
+}
+
+// ------------------------------------------------------------------ masks
+__global__ void train_masks_kernel(TrainMaskArgs a) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nt = (int64_t)a.B * a.N;
+  const int64_t per = (int64_t)(a.L - a.P) * a.U;
+  const int64_t ng = (int64_t)a.B * per;
+  const int64_t np = (int64_t)a.B * a.P * a.U;
+  if (i < nt) {
+    const float v = a.z[i] + (a.zn ? a.zn[i] : 0.0f);
+    const bool on = v > 0.0f;
+    a.tmask[i] = on ? 1 : 0;
+    a.mtok[i] = on ? 1.0f : 0.0f;
+    a.stet[i] = ste_factor(v, a.tau_tok);
+    return;
+  }
+  i -= nt;
+  if (i < ng) {
+    const float v = a.g[i] + (a.gn ? a.gn[i] : 0.0f);
+    const bool on = v > 0.0f;
+    const int64_t b = i / per, r = i % per;
+    a.umask[i] = on ? 1 : 0;
+    a.mfull[b * a.L * a.U + (int64_t)a.P * a.U + r] = on ? 1.0f : 0.0f;
+    a.steg[i] = ste_factor(v, a.tau_comp);
+    return;
+  }
+  i -= ng;
+  if (i < np) {
+    const int64_t pp = (int64_t)a.P * a.U;
+    a.mfull[(i / pp) * a.L * a.U + i % pp] = 1.0f;
+  }
+}
+
+// X0 = [m_i v_i ; text] (Sec. 3.1, training: the sequence keeps its length).
+template <class T>
+__global__ void train_embed_kernel(const T* vision, const T* text, const float* mtok, int32_t B,
+                                   int32_t N, int32_t Tn, int32_t D, float* X) {
+  const int64_t D4 = D / 4, S = (int64_t)N + Tn;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)B * S * D4) return;
+  const int64_t m = q / D4, c = (q % D4) * 4, b = m / S, i = m % S;
+  float4 v;
+  if (i < N) {
+    v = f4scale(ld4(vision, (b * N + i) * D + c), mtok[b * N + i]);
+  } else {
+    v = ld4(text, (b * Tn + (i - N)) * D + c);
+  }
+  *reinterpret_cast<float4*>(X + m * D + c) = v;
+}
+
+// ------------------------------------------------------------------ RMSNorm
+template <class T>
+__global__ __launch_bounds__(TNT) void train_norm_kernel(const float* X, const T* gain, float eps,
+                                                         int32_t D, float* U, float* r) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  const float* x = X + m * D;
+  float ss = 0.0f;
+  for (int c = threadIdx.x * 4; c < D; c += TNT * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum(ss, red);
+  const float rr = 1.0f / sqrtf(ss / (float)D + eps);
+  if (threadIdx.x == 0) r[m] = rr;
+  for (int c = threadIdx.x * 4; c < D; c += TNT * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float4 g = ld4(gain, c);
+    *reinterpret_cast<float4*>(U + m * D + c) =
+        make_float4(v.x * rr * g.x, v.y * rr * g.y, v.z * rr * g.z, v.w * rr * g.w);
+  }
+}
+
+// dX = dRes + r g dY - x r^3 (sum_k g_k dY_k x_k) / D  (dX may be dRes).
+template <class T>
+__global__ __launch_bounds__(TNT) void train_norm_bwd_kernel(const float* X, const T* gain,
+                                                             const float* r, const float* dY,
+                                                             const float* dRes, int32_t D,
+                                                             float* dX) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  const float* x = X + m * D;
+  const float* dy = dY + m * D;
+  float dot = 0.0f;
+  for (int c = threadIdx.x * 4; c < D; c += TNT * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float4 e = *reinterpret_cast<const float4*>(dy + c);
+    const float4 g = ld4(gain, c);
+    dot += g.x * e.x * v.x + g.y * e.y * v.y + g.z * e.z * v.z + g.w * e.w * v.w;
+  }
+  dot = block_sum(dot, red);
+  const float rr = r[m];
+  const float coef = rr * rr * rr * dot / (float)D;
+  for (int c = threadIdx.x * 4; c < D; c += TNT * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float4 e = *reinterpret_cast<const float4*>(dy + c);
+    const float4 g = ld4(gain, c);
+    const float4 d0 = *reinterpret_cast<const float4*>(dRes + m * D + c);
+    *reinterpret_cast<float4*>(dX + m * D + c) =
+        make_float4(d0.x + rr * g.x * e.x - v.x * coef, d0.y + rr * g.y * e.y - v.y * coef,
+                    d0.z + rr * g.z * e.z - v.z * coef, d0.w + rr * g.w * e.w - v.w * coef);
+  }
+}
+
+// ------------------------------------------------------------------ matrix products
+// C[M][N] = R + (s . A)[M][K] op(B): BL = 0 reads B as [N][K] (x W^T with
+// W = [out][in]), BL = 1 as [K][N] (dY W).  64 x 64 output tiles, K in steps
+// of 16 staged through LDS, 4 x 4 outputs per thread.  With ASC, A[m][k] is
+// scaled by ascale[(m / S) astride + k / kg] (the unit masks).
+constexpr int GBM = 64, GBN = 64, GBK = 16, GPAD = 4;
+
+template <int BL, class TB, bool ASC>
+__global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
+  __shared__ __attribute__((aligned(16))) float As[GBK][GBM + GPAD];
+  __shared__ __attribute__((aligned(16))) float Bs[GBK][GBN + GPAD];
+  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int64_t m0 = (int64_t)blockIdx.y * GBM, n0 = (int64_t)blockIdx.x * GBN;
+  const TB* B = static_cast<const TB*>(a.B);
+
+  const int ar = t >> 2, ak = (t & 3) * 4;
+  const int64_t arow = m0 + ar;
+  const bool aok = arow < a.M;
+  int bn, bk;
+  if constexpr (BL == 0) { bn = t >> 2; bk = (t & 3) * 4; }
+  else { bk = t >> 4; bn = (t & 15) * 4; }
+  const bool bok = n0 + bn < a.N;
+
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int64_t k0 = 0; k0 < a.K; k0 += GBK) {
+    float4 av = zero;
+    if (aok) {
+      av = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + ak);
+      if constexpr (ASC) av = f4scale(av, a.ascale[(arow / a.S) * a.astride + (k0 + ak) / a.kg]);
+    }
+    float4 bv = zero;
+    if (bok) {
+      if constexpr (BL == 0) bv = ld4(B, (n0 + bn) * a.ldb + k0 + bk);
+      else bv = ld4(B, (k0 + bk) * a.ldb + n0 + bn);
+    }
+    __syncthreads();
+    As[ak + 0][ar] = av.x;
+    As[ak + 1][ar] = av.y;
+    As[ak + 2][ar] = av.z;
+    As[ak + 3][ar] = av.w;
+    if constexpr (BL == 0) {
+      Bs[bk + 0][bn] = bv.x;
+      Bs[bk + 1][bn] = bv.y;
+      Bs[bk + 2][bn] = bv.z;
+      Bs[bk + 3][bn] = bv.w;
+    } else {
+      *reinterpret_cast<float4*>(&Bs[bk][bn]) = bv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < GBK; ++k) {
+      const float4 x = *reinterpret_cast<const float4*>(&As[k][ty * 4]);
+      const float4 y = *reinterpret_cast<const float4*>(&Bs[k][tx * 4]);
+      const float xa[4] = {x.x, x.y, x.z, x.w};
+      const float ya[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += xa[i] * ya[j];
+    }
+  }
+
+  const int64_t col = n0 + tx * 4;
+  if (col >= a.N) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t row = m0 + ty * 4 + i;
+    if (row >= a.M) break;
+    float4 o = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+    if (a.R) {
+      const float4 rv = *reinterpret_cast<const float4*>(a.R + row * a.ldr + col);
+      o = make_float4(rv.x + o.x, rv.y + o.y, rv.z + o.z, rv.w + o.w);
+    }
+    *reinterpret_cast<float4*>(a.C + row * a.ldc + col) = o;
+  }
+}
+
+// ------------------------------------------------------------------ RoPE
+// Rotates pairs (r, r + d/2) of nheads heads of X [M][ld] in place by the
+// angle of the row's position (sgn = +1) or back (sgn = -1, the transpose).
+__global__ void train_rope_kernel(float* X, int64_t ld, int32_t nheads, int32_t d, int32_t S,
+                                  int64_t M, const float2* tab, float sgn) {
+  const int half = d / 2;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= M * nheads * half) return;
+  const int64_t m = q / ((int64_t)nheads * half);
+  const int rem = (int)(q % ((int64_t)nheads * half));
+  const int h = rem / half, r = rem % half;
+  const float2 cs = tab[(m % S) * half + r];
+  const float s = sgn * cs.y;
+  float* p = X + m * ld + (int64_t)h * d;
+  const float a1 = p[r], a2 = p[r + half];
+  p[r] = a1 * cs.x - a2 * s;
+  p[r + half] = a2 * cs.x + a1 * s;
+}
+
+// ------------------------------------------------------------------ attention
+// One workgroup: 64 rows (queries, or keys for the K/V gradient) of one head
+// of one sample; four threads per row, each holding a quarter of the head's
+// dimensions; the other operand's rows stream through LDS 64 at a time.
+template <int HD>
+struct AttnTile {
+  float a[64][HD];
+  float b[64][HD];
+  float s0[64], s1[64];
+};
+
+template <int HD>
+__device__ __forceinline__ void load_rows(float (*dst)[HD], const float* src, int64_t row0,
+                                          int64_t ld, int64_t col0, int64_t rows_left) {
+  constexpr int C4 = HD / 4;
+  for (int q = threadIdx.x; q < 64 * C4; q += TNT) {
+    const int r = q / C4, c = (q % C4) * 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < rows_left) v = *reinterpret_cast<const float4*>(src + (row0 + r) * ld + col0 + c);
+    *reinterpret_cast<float4*>(&dst[r][c]) = v;
+  }
+}
+
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  return v;
+}
+
+template <int HD>
+__global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
+  constexpr int PD = HD / 4;
+  __shared__ AttnTile<HD> sm;
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int rep = a.A / a.KV, g = h / rep;
+  const int qr = threadIdx.x >> 2, part = threadIdx.x & 3;
+  const int64_t i = (int64_t)qt * 64 + qr;
+  const bool valid = i < a.S;
+  const int64_t base = (int64_t)b * a.S;
+  const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
+  float q[PD], acc[PD];
+#pragma unroll
+  for (int x = 0; x < PD; ++x) {
+    q[x] = valid ? a.Q[(base + i) * ldq + (int64_t)h * HD + part * PD + x] * a.scale : 0.0f;
+    acc[x] = 0.0f;
+  }
+  float mx = -INFINITY, l = 0.0f;
+  for (int kt = 0; kt <= qt; ++kt) {
+    __syncthreads();
+    load_rows<HD>(sm.a, a.K, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
+    load_rows<HD>(sm.b, a.V, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
+    __syncthreads();
+    if (!valid) continue;
+    int jn = (int)min((int64_t)64, a.S - (int64_t)kt * 64);
+    if (kt == qt) jn = min(jn, qr + 1);
+    for (int j = 0; j < jn; ++j) {
+      float s = 0.0f;
+#pragma unroll
+      for (int x = 0; x < PD; ++x) s += q[x] * sm.a[j][part * PD + x];
+      s = quad_sum(s);
+      const float mn = fmaxf(mx, s);
+      const float corr = expf(mx - mn), p = expf(s - mn);
+      l = l * corr + p;
+#pragma unroll
+      for (int x = 0; x < PD; ++x) acc[x] = acc[x] * corr + p * sm.b[j][part * PD + x];
+      mx = mn;
+    }
+  }
+  if (!valid) return;
+  const float inv = 1.0f / l;
+#pragma unroll
+  for (int x = 0; x < PD; ++x) a.out[(base + i) * ldq + (int64_t)h * HD + part * PD + x] = acc[x] * inv;
+  if (part == 0) a.lse[(base + i) * a.A + h] = mx + logf(l);
+}
+
+// dQ_i = scale sum_j P_ij (dP_ij - D_i) k_j, dP_ij = dO_i . v_j,
+// D_i = dO_i . O_i (also stored for the K / V gradient).
+template <int HD>
+__global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
+  constexpr int PD = HD / 4;
+  __shared__ AttnTile<HD> sm;
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int rep = a.A / a.KV, g = h / rep;
+  const int qr = threadIdx.x >> 2, part = threadIdx.x & 3;
+  const int64_t i = (int64_t)qt * 64 + qr;
+  const bool valid = i < a.S;
+  const int64_t base = (int64_t)b * a.S;
+  const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
+  const int64_t off = (base + (valid ? i : 0)) * ldq + (int64_t)h * HD + part * PD;
+  float q[PD], dout[PD], dq[PD];
+  float Di = 0.0f;
+#pragma unroll
+  for (int x = 0; x < PD; ++x) {
+    q[x] = valid ? a.Q[off + x] * a.scale : 0.0f;
+    dout[x] = valid ? a.dO[off + x] : 0.0f;
+    Di += valid ? dout[x] * a.O[off + x] : 0.0f;
+    dq[x] = 0.0f;
+  }
+  Di = quad_sum(Di);
+  const float lse = valid ? a.lse[(base + i) * a.A + h] : 0.0f;
+  if (valid && part == 0) a.Dv[(base + i) * a.A + h] = Di;
+  for (int kt = 0; kt <= qt; ++kt) {
+    __syncthreads();
+    load_rows<HD>(sm.a, a.K, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
+    load_rows<HD>(sm.b, a.V, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
+    __syncthreads();
+    if (!valid) continue;
+    int jn = (int)min((int64_t)64, a.S - (int64_t)kt * 64);
+    if (kt == qt) jn = min(jn, qr + 1);
+    for (int j = 0; j < jn; ++j) {
+      float s = 0.0f, dp = 0.0f;
+#pragma unroll
+      for (int x = 0; x < PD; ++x) {
+        s += q[x] * sm.a[j][part * PD + x];
+        dp += dout[x] * sm.b[j][part * PD + x];
+      }
+      s = quad_sum(s);
+      dp = quad_sum(dp);
+      const float ds = expf(s - lse) * (dp - Di);
+#pragma unroll
+      for (int x = 0; x < PD; ++x) dq[x] += ds * sm.a[j][part * PD + x];
+    }
+  }
+  if (!valid) return;
+#pragma unroll
+  for (int x = 0; x < PD; ++x) a.out[off + x] = dq[x] * a.scale;
+}
+
+// dV_j = sum_{h of the group} sum_{i >= j} P_ij dO_i,
+// dK_j = scale sum_h sum_{i >= j} P_ij (dP_ij - D_i) q_i.
+template <int HD>
+__global__ __launch_bounds__(TNT) void train_attn_dkv_kernel(TAttnArgs a) {
+  constexpr int PD = HD / 4;
+  __shared__ AttnTile<HD> sm;
+  const int kt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int rep = a.A / a.KV;
+  const int kr = threadIdx.x >> 2, part = threadIdx.x & 3;
+  const int64_t j = (int64_t)kt * 64 + kr;
+  const bool valid = j < a.S;
+  const int64_t base = (int64_t)b * a.S;
+  const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
+  const int64_t koff = (base + (valid ? j : 0)) * ldk + (int64_t)g * HD + part * PD;
+  float k[PD], v[PD], dk[PD], dv[PD];
+#pragma unroll
+  for (int x = 0; x < PD; ++x) {
+    k[x] = valid ? a.K[koff + x] : 0.0f;
+    v[x] = valid ? a.V[koff + x] : 0.0f;
+    dk[x] = 0.0f;
+    dv[x] = 0.0f;
+  }
+  const int nqt = (int)((a.S + 63) / 64);
+  for (int h = g * rep; h < (g + 1) * rep; ++h) {
+    for (int qt = kt; qt < nqt; ++qt) {
+      const int64_t rows_left = a.S - (int64_t)qt * 64;
+      __syncthreads();
+      load_rows<HD>(sm.a, a.Q, base + (int64_t)qt * 64, ldq, (int64_t)h * HD, rows_left);
+      load_rows<HD>(sm.b, a.dO, base + (int64_t)qt * 64, ldq, (int64_t)h * HD, rows_left);
+      if (threadIdx.x < 64) {
+        const bool in = threadIdx.x < rows_left;
+        const int64_t r = base + (int64_t)qt * 64 + threadIdx.x;
+        sm.s0[threadIdx.x] = in ? a.lse[r * a.A + h] : 0.0f;
+        sm.s1[threadIdx.x] = in ? a.Dv[r * a.A + h] : 0.0f;
+      }
+      __syncthreads();
+      if (!valid) continue;
+      const int i0 = qt == kt ? kr : 0;
+      const int in = (int)min((int64_t)64, rows_left);
+      for (int ii = i0; ii < in; ++ii) {
+        float s = 0.0f, dp = 0.0f;
+#pragma unroll
+        for (int x = 0; x < PD; ++x) {
+          s += sm.a[ii][part * PD + x] * k[x];
+          dp += sm.b[ii][part * PD + x] * v[x];
+        }
+        s = quad_sum(s) * a.scale;
+        dp = quad_sum(dp);
+        const float p = expf(s - sm.s0[ii]);
+        const float ds = p * (dp - sm.s1[ii]);
+#pragma unroll
+        for (int x = 0; x < PD; ++x) {
+          dv[x] += p * sm.b[ii][part * PD + x];
+          dk[x] += ds * sm.a[ii][part * PD + x];
+        }
+      }
+    }
+  }
+  if (!valid) return;
+#pragma unroll
+  for (int x = 0; x < PD; ++x) {
+    a.dK[koff + x] = dk[x] * a.scale;
+    a.dV[koff + x] = dv[x];
+  }
+}
+
+// ------------------------------------------------------------------ SwiGLU
+__global__ void train_swiglu_kernel(const float* AG, const float* AE, int64_t n, float* H) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= n) return;
+  const float x = AG[q];
+  H[q] = x / (1.0f + expf(-x)) * AE[q];
+}
+
+// Per row: part[m][u] = sum over unit u's channels of dHm . H; then, with the
+// unit's mask s, dH = s dHm and the gate / up gradients replace AG and AE.
+__global__ __launch_bounds__(TNT) void train_swiglu_bwd_kernel(const float* dHm, float* AG,
+                                                               float* AE, const float* H,
+                                                               const float* mrow, int64_t mstride,
+                                                               int32_t S, int32_t F, int32_t U,
+                                                               float* part) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  const int64_t b = m / S;
+  const int w = F / U;
+  for (int u = 0; u < U; ++u) {
+    const float s = mrow[b * mstride + u];
+    float dot = 0.0f;
+    for (int c = u * w + threadIdx.x; c < (u + 1) * w; c += TNT) {
+      const int64_t q = m * F + c;
+      const float dh = dHm[q];
+      dot += dh * H[q];
+      const float x = AG[q], e = AE[q];
+      const float sg = 1.0f / (1.0f + expf(-x));
+      const float dm = dh * s;
+      AG[q] = dm * e * sg * (1.0f + x * (1.0f - sg));
+      AE[q] = dm * x * sg;
+    }
+    dot = block_sum(dot, red);
+    if (threadIdx.x == 0) part[m * U + u] = dot;
+  }
+}
+
+// Per row: part[m][u] = sum over unit u's head columns of dOm . O; dOm *= s.
+__global__ __launch_bounds__(TNT) void train_attn_mask_bwd_kernel(float* dOm, const float* O,
+                                                                  const float* mrow,
+                                                                  int64_t mstride, int32_t S,
+                                                                  int32_t W, int32_t U,
+                                                                  float* part) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  const int64_t b = m / S;
+  const int w = W / U;
+  for (int u = 0; u < U; ++u) {
+    const float s = mrow[b * mstride + u];
+    float dot = 0.0f;
+    for (int c = u * w + threadIdx.x; c < (u + 1) * w; c += TNT) {
+      const int64_t q = m * W + c;
+      const float d = dOm[q];
+      dot += d * O[q];
+      dOm[q] = d * s;
+    }
+    dot = block_sum(dot, red);
+    if (threadIdx.x == 0) part[m * U + u] = dot;
+  }
+}
+
+// dM[b][l][u] = sum over the sample's rows of both partial sums (float64, row order).
+__global__ void train_mask_reduce_kernel(const float* pa, const float* pf, int32_t B, int32_t S,
+                                         int32_t U, int32_t L, int32_t l, float* dM) {
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= B * U) return;
+  const int b = q / U, u = q % U;
+  double s = 0.0;
+  for (int64_t i = 0; i < S; ++i) {
+    const int64_t r = ((int64_t)b * S + i) * U + u;
+    s += (double)pa[r] + (double)pf[r];
+  }
+  dM[((int64_t)b * L + l) * U + u] = (float)s;
+}
+
+// dL/dz_i = (dX0_i . v_i) y (1 - y) / tau_tok, one workgroup per vision token.
+template <class T>
+__global__ __launch_bounds__(TNT) void train_token_grad_kernel(const float* dX0, const T* vision,
+                                                               const float* stet, int32_t N,
+                                                               int32_t S, int32_t D,
+                                                               float* grad) {
+  __shared__ float red[4];
+  const int64_t t = blockIdx.x;   // b N + i
+  const int64_t b = t / N, i = t % N;
+  const float* dx = dX0 + (b * S + i) * D;
+  float dot = 0.0f;
+  for (int c = threadIdx.x * 4; c < D; c += TNT * 4) {
+    const float4 e = *reinterpret_cast<const float4*>(dx + c);
+    const float4 v = ld4(vision, t * D + c);
+    dot += e.x * v.x + e.y * v.y + e.z * v.z + e.w * v.w;
+  }
+  dot = block_sum(dot, red);
+  if (threadIdx.x == 0) grad[t] = dot * stet[t];
+}
+
+__global__ void train_gate_grad_kernel(const float* dM, const float* steg, int32_t B, int32_t L,
+                                       int32_t P, int32_t U, float* grad) {
+  const int64_t per = (int64_t)(L - P) * U;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= B * per) return;
+  const int64_t b = q / per, r = q % per;
+  grad[q] = dM[b * L * U + (int64_t)P * U + r] * steg[q];
+}
+
+unsigned blocks(int64_t n) { return (unsigned)((n + TNT - 1) / TNT); }
+
+}  // namespace
+
+hipError_t launch_train_masks(const TrainMaskArgs& a, hipStream_t st) {
+  const int64_t n = (int64_t)a.B * a.N + (int64_t)a.B * (a.L - a.P) * a.U + (int64_t)a.B * a.P * a.U;
+  if (n <= 0) return hipSuccess;
+  train_masks_kernel<<<blocks(n), TNT, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_embed(const void* vision, const void* text, const float* mtok, int32_t B,
+                              int32_t N, int32_t T, int32_t D, bool bf16, float* X,
+                              hipStream_t st) {
+  const int64_t n = (int64_t)B * (N + T) * (D / 4);
+  if (n <= 0) return hipSuccess;
+  if (bf16)
+    train_embed_kernel<uint16_t><<<blocks(n), TNT, 0, st>>>(
+        static_cast<const uint16_t*>(vision), static_cast<const uint16_t*>(text), mtok, B, N, T, D, X);
+  else
+    train_embed_kernel<float><<<blocks(n), TNT, 0, st>>>(static_cast<const float*>(vision),
+                                                         static_cast<const float*>(text), mtok, B,
+                                                         N, T, D, X);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_norm(const float* X, const void* gain, float eps, int64_t M, int32_t D,
+                             bool bf16, float* U, float* r, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (bf16)
+    train_norm_kernel<uint16_t><<<(unsigned)M, TNT, 0, st>>>(X, static_cast<const uint16_t*>(gain),
+                                                             eps, D, U, r);
+  else
+    train_norm_kernel<float><<<(unsigned)M, TNT, 0, st>>>(X, static_cast<const float*>(gain), eps,
+                                                          D, U, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_norm_bwd(const float* X, const void* gain, const float* r, const float* dY,
+                                 const float* dRes, int64_t M, int32_t D, bool bf16, float* dX,
+                                 hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (bf16)
+    train_norm_bwd_kernel<uint16_t><<<(unsigned)M, TNT, 0, st>>>(
+        X, static_cast<const uint16_t*>(gain), r, dY, dRes, D, dX);
+  else
+    train_norm_bwd_kernel<float><<<(unsigned)M, TNT, 0, st>>>(X, static_cast<const float*>(gain),
+                                                              r, dY, dRes, D, dX);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_gemm(const TGemmArgs& a, int32_t bl, bool bf16, hipStream_t st) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.N + GBN - 1) / GBN), (unsigned)((a.M + GBM - 1) / GBM));
+  const bool asc = a.ascale != nullptr;
+#define SVL_TGEMM(BLV, TB, ASCV) train_gemm_kernel<BLV, TB, ASCV><<<grid, TNT, 0, st>>>(a)
+  if (bl == 0) {
+    if (bf16) { if (asc) SVL_TGEMM(0, uint16_t, true); else SVL_TGEMM(0, uint16_t, false); }
+    else { if (asc) SVL_TGEMM(0, float, true); else SVL_TGEMM(0, float, false); }
+  } else {
+    if (bf16) SVL_TGEMM(1, uint16_t, false);
+    else SVL_TGEMM(1, float, false);
+  }
+#undef SVL_TGEMM
+  return hipGetLastError();
+}
+
+hipError_t launch_train_rope(float* X, int64_t ld, int32_t nheads, int32_t d, int32_t S, int64_t M,
+                             const float2* tab, float sgn, hipStream_t st) {
+  const int64_t n = M * nheads * (d / 2);
+  if (n <= 0) return hipSuccess;
+  train_rope_kernel<<<blocks(n), TNT, 0, st>>>(X, ld, nheads, d, S, M, tab, sgn);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_attn(const TAttnArgs& a, int32_t head_dim, int32_t B, int32_t which,
+                             hipStream_t st) {
+  const unsigned tiles = (unsigned)((a.S + 63) / 64);
+  if (tiles == 0 || B <= 0) return hipSuccess;
+  const dim3 grid(tiles, (unsigned)(which == 2 ? a.KV : a.A), (unsigned)B);
+#define SVL_TATTN(HD)                                                      \
+  do {                                                                     \
+    if (which == 0) train_attn_fwd_kernel<HD><<<grid, TNT, 0, st>>>(a);    \
+    else if (which == 1) train_attn_dq_kernel<HD><<<grid, TNT, 0, st>>>(a); \
+    else train_attn_dkv_kernel<HD><<<grid, TNT, 0, st>>>(a);               \
+  } while (0)
+  switch (head_dim) {
+    case 32: SVL_TATTN(32); break;
+    case 64: SVL_TATTN(64); break;
+    case 128: SVL_TATTN(128); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef SVL_TATTN
+  return hipGetLastError();
+}
+
+hipError_t launch_train_swiglu(const float* AG, const float* AE, int64_t n, float* H,
+                               hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  train_swiglu_kernel<<<blocks(n), TNT, 0, st>>>(AG, AE, n, H);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_swiglu_bwd(const float* dHm, float* AG, float* AE, const float* H,
+                                   const float* mrow, int64_t mstride, int32_t S, int64_t M,
+                                   int32_t F, int32_t U, float* part, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  train_swiglu_bwd_kernel<<<(unsigned)M, TNT, 0, st>>>(dHm, AG, AE, H, mrow, mstride, S, F, U, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_attn_mask_bwd(float* dOm, const float* O, const float* mrow,
+                                      int64_t mstride, int32_t S, int64_t M, int32_t W, int32_t U,
+                                      float* part, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  train_attn_mask_bwd_kernel<<<(unsigned)M, TNT, 0, st>>>(dOm, O, mrow, mstride, S, W, U, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_mask_reduce(const float* pa, const float* pf, int32_t B, int32_t S,
+                                    int32_t U, int32_t L, int32_t l, float* dM, hipStream_t st) {
+  if (B * U <= 0) return hipSuccess;
+  train_mask_reduce_kernel<<<blocks((int64_t)B * U), TNT, 0, st>>>(pa, pf, B, S, U, L, l, dM);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_token_grad(const float* dX0, const void* vision, const float* stet,
+                                   int32_t B, int32_t N, int32_t S, int32_t D, bool bf16,
+                                   float* grad, hipStream_t st) {
+  const int64_t n = (int64_t)B * N;
+  if (n <= 0) return hipSuccess;
+  if (bf16)
+    train_token_grad_kernel<uint16_t><<<(unsigned)n, TNT, 0, st>>>(
+        dX0, static_cast<const uint16_t*>(vision), stet, N, S, D, grad);
+  else
+    train_token_grad_kernel<float><<<(unsigned)n, TNT, 0, st>>>(
+        dX0, static_cast<const float*>(vision), stet, N, S, D, grad);
+  return hipGetLastError();
+}
+
+hipError_t launch_train_gate_grad(const float* dM, const float* steg, int32_t B, int32_t L,
+                                  int32_t P, int32_t U, float* grad, hipStream_t st) {
+  const int64_t n = (int64_t)B * (L - P) * U;
+  if (n <= 0) return hipSuccess;
+  train_gate_grad_kernel<<<blocks(n), TNT, 0, st>>>(dM, steg, B, L, P, U, grad);
+  return hipGetLastError();
+}
+
+}  // namespace svl

@@ -430,3 +430,52 @@ def test_noalloc_decode_rejects_shapes_past_its_scratch_on_the_host():
             assert st == 4 and "allocation-free scratch" in msg, msg
         else:
             assert st == 2 and "max_len" in msg, msg      # max_len past 32768
+
+
+def test_train_step_rejects_bad_arguments():
+    """Host-side checks of svl_train_step and svl_train_workspace_bytes (every
+    case is rejected before a launch)."""
+    cfg = svl.make_config(WORKLOADS["tiny_f32"].shape)
+    lib = svl.load_library()
+    dev = 16 * 4096 * 100
+    L = cfg.n_layers
+    table = (binding.svl_layer_weights * L)(*[binding.svl_layer_weights(*([dev] * 9))] * L)
+
+    def prm(**kw):
+        base = dict(tau_tok=0.7, tau_comp=1.3, prefix=1, units=4)
+        base.update(kw)
+        return binding.svl_train_params(*base.values())
+
+    def call(p=None, B=2, N=8, T=3, ws_bytes=None, **ptr):
+        p = p or prm()
+        n = lib.svl_train_workspace_bytes(ctypes.byref(cfg), ctypes.byref(p), B, N, T)
+        args = dict(logits=dev, tnoise=None, glog=dev, gnoise=None, vision=dev, text=dev,
+                    grad=dev, hidden=dev, tmask=dev, umask=dev, gl=dev, gg=dev, ws=dev)
+        args.update(ptr)
+        return lib.svl_train_step(ctypes.byref(cfg), table, ctypes.byref(p), B, N, T,
+                                  args["logits"], args["tnoise"], args["glog"], args["gnoise"],
+                                  args["vision"], args["text"], args["grad"], args["hidden"],
+                                  args["tmask"], args["umask"], args["gl"], args["gg"], args["ws"],
+                                  (n - 1) if ws_bytes is None else ws_bytes, None)
+
+    # the workspace one byte short is the last check: every other case fails earlier
+    assert call() == 4
+    for p, want in ((prm(tau_tok=0.0), 3), (prm(tau_comp=float("nan")), 3), (prm(prefix=-1), 3),
+                    (prm(prefix=L + 1), 3), (prm(units=0), 3), (prm(units=3), 2)):
+        assert call(p) == want
+        assert lib.svl_train_workspace_bytes(ctypes.byref(cfg), ctypes.byref(p), 2, 8, 3) == 0
+    assert call(B=0) == 2 and call(N=0, T=0) == 2 and call(B=70000) == 2
+    assert call(hidden=None) == 1 and call(logits=None) == 1 and call(text=None) == 1
+    assert call(glog=None) == 1 and call(gl=None) == 1 and call(gg=None) == 1
+    assert call(ws=None) == 1 and call(vision=dev + 4) == 7 and call(ws=dev + 8) == 7
+    # without grad_hidden the gradient outputs are not needed; N = 0 needs no token arrays;
+    # P = L controls no layer and needs no gate arrays (the workspace check still fails last)
+    assert call(grad=None, gl=None, gg=None) == 4
+    assert call(N=0, logits=None, vision=None, tmask=None, gl=None) == 4
+    assert call(prm(prefix=L), glog=None, umask=None, gg=None) == 4
+    bad = svl.make_config(WORKLOADS["tiny_f32"].shape)
+    bad.head_dim = 16
+    assert lib.svl_train_workspace_bytes(ctypes.byref(bad), ctypes.byref(prm()), 2, 8, 3) == 0
+    sizes = [lib.svl_train_workspace_bytes(ctypes.byref(cfg), ctypes.byref(prm()), b, 8, 3)
+             for b in (1, 2, 4)]
+    assert sizes[0] < sizes[1] < sizes[2]
