@@ -4,16 +4,15 @@ oracle/training.py's masked_train_step, through the C ABI.
 Per sample: token and unit masks exact (the decisions compare float32
 z + xi with 0 on both sides, and rounding keeps the sign of a sum); the final
 hidden states within 1e-4 normwise relative error (the float32 bar); the
-token-logit and gate-logit gradients within TOL_GRAD normwise, taken
-separately over kept tokens, dropped tokens and the token at position 0 (a
-dropped token's gradient passes through the RMSNorm of a zero row, which
-scales it by eps^(-1/2), so the groups differ in magnitude by orders), and
-over the unit gradients.
+gate-logit gradients within TOL_GRAD normwise; each token-logit gradient
+within TOL_GRAD of its condition scale: dL/dz_i is the dot product
+(dL/dX_0[i] . v_i) y_i (1 - y_i) / tau, whose rounding error is bounded by
+the error of dL/dX_0 times sum_d |dL/dX_0[i][d] v_i[d]| y_i (1 - y_i) / tau,
+so that scale (from the oracle) divides the difference.  (Gradients of
+dropped tokens pass through the RMSNorm of a zero row, which scales them by
+eps^(-1/2): they differ from the kept tokens' by orders, and a normwise
+measure over all tokens would see only them.)
 
-TOL_GRAD: the backward is float32 like the forward but twice as deep (each
-layer's backward walks its forward again in reverse) and takes differences
-of nearly equal terms (dP - D in the softmax, the RMSNorm's projection), so
-its normwise error is allowed ten times the forward's bar.
 """
 import numpy as np
 import pytest
@@ -65,7 +64,7 @@ def _run(w, seed, prefix, units, tau_tok=0.7, tau_comp=1.3, drop_first=False, no
 
     hl = [host_layer(l) for l in layers]
     vis, txt = W.as_f32(vision), W.as_f32(text)
-    errs = {"hidden": 0.0, "kept": 0.0, "dropped": 0.0, "first": 0.0, "gate": 0.0}
+    errs = {"hidden": 0.0, "token": 0.0, "gate": 0.0}
     for b in range(B):
         ref = ot.masked_train_step(s, lambda l: hl[l], vis[b], txt[b], z[b].astype(np.float64),
                                    g[b].astype(np.float64), G[b], prefix, units, tau_tok, tau_comp,
@@ -74,17 +73,15 @@ def _run(w, seed, prefix, units, tau_tok=0.7, tau_comp=1.3, drop_first=False, no
         np.testing.assert_array_equal(got["token_mask"][b], ref.token_mask)
         np.testing.assert_array_equal(got["unit_mask"][b], ref.unit_mask)
         errs["hidden"] = max(errs["hidden"], _normwise(got["hidden"][b], ref.hidden))
-        on = ref.token_mask.astype(bool)
-        rest = np.arange(N) > 0
-        errs["kept"] = max(errs["kept"], _normwise(got["grad_logits"][b][on & rest],
-                                                   ref.grad_z[on & rest]))
-        errs["dropped"] = max(errs["dropped"], _normwise(got["grad_logits"][b][~on & rest],
-                                                         ref.grad_z[~on & rest]))
-        errs["first"] = max(errs["first"], _normwise(got["grad_logits"][b][:1], ref.grad_z[:1]))
+        v = z[b].astype(np.float64) + (0.0 if xi is None else xi[b].astype(np.float64))
+        y = 1.0 / (1.0 + np.exp(-v / tau_tok))
+        cond = np.sum(np.abs(ref.grad_x0[:N] * vis[b]), axis=1) * y * (1.0 - y) / tau_tok
+        diff = np.abs(got["grad_logits"][b].astype(np.float64) - ref.grad_z)
+        errs["token"] = max(errs["token"], float(np.max(diff / cond, initial=0.0)))
         errs["gate"] = max(errs["gate"], _normwise(got["grad_gate"][b], ref.grad_gate))
     print("  " + ", ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
     assert errs["hidden"] <= TOL_HIDDEN, errs
-    for k in ("kept", "dropped", "first", "gate"):
+    for k in ("token", "gate"):
         assert errs[k] <= TOL_GRAD, (k, errs)
     return got
 
