@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector, published
 
 
 def parse():
@@ -46,6 +47,11 @@ def parse():
     p.add_argument("--no-bf16-line", action="store_true",
                    help="skip the extra timing of the headline with bf16 activations")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-train-line", action="store_true",
+                   help="skip the training-step timing (svl_train_step) of the default run")
+    p.add_argument("--train", action="store_true",
+                   help="time only the training step of the masked decoder at the workload's "
+                        "shape (one JSON line)")
     p.add_argument("--cpu-layers", type=int, default=0,
                    help="executed layers the CPU-baseline sample runs (0: all of them, no "
                         "extrapolation; the headline's 24 take about 20 s on 16 host threads)")
@@ -556,8 +562,82 @@ def decode_bench(args):
     print(json.dumps(result))
 
 
+def train_flops(shape, B, S):
+    """FLOPs the training step executes (2 per multiply-add): the forward, the
+    forward again during the backward (without the down projection), the
+    data-gradient products and the attention backward (seven S x S x d
+    products per head against the forward's two)."""
+    D, A, KV, d, F, L = (shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+                         shape.d_ffn, shape.n_layers)
+    M = B * S
+    gemm = 2 * M * (D * (A + 2 * KV) * d + A * d * D + 3 * D * F)
+    attn = 2 * A * d * S * (S + 1) * B
+    per_layer = 3 * gemm - 2 * M * D * F + 2 * attn + 3.5 * attn
+    return int(L * per_layer)
+
+
+def train_line(w, seed, dev, steps=2, warmup=1):
+    """Times svl_train_step (forward + backward to the token and gate logits)
+    at the workload's shape: prefix L/2, one unit per head group."""
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+    shape = w.shape
+    B, N, T = w.batch, w.n_vision, w.n_text
+    S = N + T
+    P, U = shape.n_layers // 2, shape.n_groups
+    cfg = svl.make_config(shape)
+    vision, text = W.draw_hidden(w, seed, device=dev)
+    table = svl.LayerTable([W.draw_layer_weights(w, l, seed, device=dev)
+                            for l in range(shape.n_layers)])
+    rng = np.random.default_rng([seed, 11])
+    z = torch.from_numpy(rng.normal(-0.7, 1.5, (B, N)).astype(np.float32)).to(dev)
+    g = torch.from_numpy(rng.normal(0.6, 1.5, (B, (shape.n_layers - P) * U)).astype(np.float32)).to(dev)
+    xi = torch.from_numpy(rng.logistic(0, 1, (B, N)).astype(np.float32)).to(dev)
+    xg = torch.from_numpy(rng.logistic(0, 1, tuple(g.shape)).astype(np.float32)).to(dev)
+    G = torch.from_numpy(rng.standard_normal((B, S, shape.d_model)).astype(np.float32)).to(dev)
+    prm = svl.svl_train_params(0.7, 1.3, P, U)
+    ws = svl.alloc_train_workspace(cfg, prm, B, N, T, dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        svl.svl_train_step(cfg, table, prm, z, g, vision, text, G, ws, token_noise=xi,
+                           gate_noise=xg, stream=stream)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    fl = train_flops(shape, B, S)
+    tf = fl / (ms * 1e-3) / 1e12
+    print(f"# training step: {ms:.2f} ms", file=sys.stderr, flush=True)
+    return {"what": "svl_train_step: static-shape forward under straight-through masks + "
+                    "backward to the token and gate logits, float32",
+            "workload": w.name, "batch": B, "seq_len": S, "prefix": P, "units": U,
+            "steps": steps, "warmup": warmup, "ms_per_step": round(ms, 3),
+            "tokens_per_s": round(B * S / (ms * 1e-3), 1),
+            "executed_flops_per_step": fl, "executed_tflops": round(tf, 2),
+            "fp32_peak_tflops": FP32_PEAK_TFLOPS, "frac_fp32_peak": round(tf / FP32_PEAK_TFLOPS, 4)}
+
+
 def main():
     args = parse()
+    if args.train:
+        import torch
+
+        import workloads as W
+        if args.gpus != 1 or not torch.cuda.is_available():
+            raise SystemExit("bench.py --train runs on one GPU")
+        w = W.get_workload(args.workload or W.HEADLINE)
+        print(json.dumps(train_line(w, args.seed, torch.device("cuda:0"), steps=args.steps,
+                                    warmup=args.warmup)))
+        return
     if args.traffic_from:
         write_traffic(args.traffic_from)
         return
@@ -815,6 +895,8 @@ def main():
                     "+ row compaction + remaining layers"}
     if bf16_line is not None:
         result["bf16_compute"] = bf16_line
+    if not args.no_train_line and default_mode and w.name == W.HEADLINE:
+        result["train_step"] = train_line(w, args.seed, dev)
     if not args.no_cpu_baseline and default_mode:
         result["cpu_baseline"] = cpu_baseline(w, inp, layers, args.cpu_layers)
     print(json.dumps(result))
