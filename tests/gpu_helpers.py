@@ -71,7 +71,13 @@ def gpu_prefill(w, inp, layers, dev="cuda", table=None, compute="f16"):
 def oracle_prefill(w, inp, layers, samples=None):
     sel = slice(None) if samples is None else list(samples)
     lm = inp.layer_mask[sel]
-    return oracle.prefill(w.shape, lambda l: host_layer(layers[l]), inp.scores[sel],
+    deep = w.shape.n_layers >= 16
+
+    def layer(l):
+        if deep:
+            print(f"  oracle layer {l}", flush=True)   # progress of a long reference run
+        return host_layer(layers[l])
+    return oracle.prefill(w.shape, layer, inp.scores[sel],
                           np.asarray(inp.keep)[sel], W.as_f32(inp.vision[sel]),
                           W.as_f32(inp.text[sel]), lm, inp.head_mask[sel],
                           None if inp.ffn_mask is None else inp.ffn_mask[sel])
