@@ -690,9 +690,13 @@ def main():
         scores = torch.from_numpy(logits_np).to(dev)
         count_ws = torch.empty(max(256, 4 * B), dtype=torch.uint8, device=dev)
         prefix = shape.n_layers // 2
+        # the count kernel runs on a stream of its own (default priority): its
+        # sync waits for the count alone, so the host projects and plans the
+        # next step while the previous step's prefill still runs on `stream`
+        count_stream = torch.cuda.Stream(device=dev)
 
         def project():
-            counts = svl.svl_count_positive(scores, count_ws, stream=stream)
+            counts = svl.svl_count_positive(scores, count_ws, stream=count_stream)
             return counts, svl.svl_budget_project(cfg, counts, N, w.n_text, args.threshold_budget,
                                                   0, prefix, inp.layer_mask, inp.head_mask,
                                                   inp.ffn_mask)
@@ -883,7 +887,9 @@ def main():
                                "groups_dropped_by_projection":
                                    int(np.sum(np.asarray(inp.head_mask) != np.asarray(hm_run)) //
                                        (shape.n_heads // shape.n_groups)),
-                               "step": "count kernel + host sync + projection + prefill"}
+                               "step": "count kernel (own stream) + host sync + projection + "
+                                       "prefill; the next step's count, projection and "
+                                       "planning overlap this step's prefill"}
     if args.controller is not None:
         result["controller"] = {
             "positive_logits": [int(c) for c in counts0], "budget": args.controller,

@@ -174,14 +174,26 @@ __global__ __launch_bounds__(NT) void gather_kernel(const int32_t* kept_idx, con
   float* dst = resid + (size_t)r * D;
   if constexpr (BF16) {
     const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(src) + src_row * D);
-    for (int c = threadIdx.x; c < D / 8; c += NT) {
-      const uint4 v = p[c];
-      float4 f0 = make_float4(bf16_bits_to_f32(v.x & 0xffffu), bf16_bits_to_f32(v.x >> 16),
-                              bf16_bits_to_f32(v.y & 0xffffu), bf16_bits_to_f32(v.y >> 16));
-      float4 f1 = make_float4(bf16_bits_to_f32(v.z & 0xffffu), bf16_bits_to_f32(v.z >> 16),
-                              bf16_bits_to_f32(v.w & 0xffffu), bf16_bits_to_f32(v.w >> 16));
-      reinterpret_cast<float4*>(dst)[2 * c] = f0;
-      reinterpret_cast<float4*>(dst)[2 * c + 1] = f1;
+    const int n8 = D / 8;
+    constexpr int PER = 4;   // every load of a batch in flight before the first store
+    for (int c0 = threadIdx.x; c0 < n8; c0 += PER * NT) {
+      uint4 v[PER];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const int c = c0 + j * NT;
+        v[j] = c < n8 ? p[c] : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const int c = c0 + j * NT;
+        if (c >= n8) break;
+        const float4 f0 = make_float4(bf16_bits_to_f32(v[j].x & 0xffffu), bf16_bits_to_f32(v[j].x >> 16),
+                                      bf16_bits_to_f32(v[j].y & 0xffffu), bf16_bits_to_f32(v[j].y >> 16));
+        const float4 f1 = make_float4(bf16_bits_to_f32(v[j].z & 0xffffu), bf16_bits_to_f32(v[j].z >> 16),
+                                      bf16_bits_to_f32(v[j].w & 0xffffu), bf16_bits_to_f32(v[j].w >> 16));
+        reinterpret_cast<float4*>(dst)[2 * c] = f0;
+        reinterpret_cast<float4*>(dst)[2 * c + 1] = f1;
+      }
     }
   } else {
     const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(src) + src_row * D);
