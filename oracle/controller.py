@@ -188,10 +188,9 @@ def prefill_controlled(shape, layer_weights: Callable[[int], Dict[str, np.ndarra
 
     counts = np.array([threshold_count(z[b]) for b in range(B)], dtype=np.int32)
     kaps = np.array([kappa(z[b]) for b in range(B)])
-    seqs, kept_first = [], []
+    seqs = []
     for b in range(B):
         kept = select_topk(z[b], int(counts[b]))
-        kept_first.append(kept)
         seqs.append(np.concatenate([np.asarray(vision[b], np.float64)[kept],
                                     np.asarray(text[b], np.float64), e_b[None, :]], axis=0))
 
@@ -208,24 +207,52 @@ def prefill_controlled(shape, layer_weights: Callable[[int], Dict[str, np.ndarra
     hm = np.zeros((B, L, A), np.uint8)
     fm = np.zeros((B, L, G), np.uint8)
     keep = np.zeros(B, np.int32)
-    kept_idx = np.full((B, N), -1, dtype=np.int32)
     for b in range(B):
         logits[b] = gate_logits(ctrl, seqs[b][-1], kaps[b])
-        lo, ho, fo = masks_from_logits(shape, logits[b], P, U)
-        conf = np.zeros((L, U))
-        conf[P:] = logits[b].reshape(L - P, U)
-        k, lo, ho, fo = project_sample(shape, z[b], T, budget, vocab, P, lo, ho, fo, conf,
-                                       units=U)
-        keep[b], lm[b], hm[b], fm[b] = k, lo, ho, fo
-        final = select_topk(z[b], int(k))
+        keep[b], lm[b], hm[b], fm[b] = decide_sample(shape, z[b], logits[b], T, budget, vocab, P, U)
+    kept_idx, cu, resid = finish_controlled(shape, layer_weights, prefix_resid, z, counts, keep,
+                                            lm, hm, fm, P, T, counter)
+    return ControlledResult(kept_idx, cu, resid.reshape(-1, D), keep, counts, kaps, logits,
+                            lm, hm, fm, prefix_resid, counter)
+
+
+def decide_sample(shape, z, logits, n_text: int, budget: float, vocab: int, prefix: int,
+                  units: int):
+    """One sample's decisions from its gate logits: a unit runs iff its logit
+    is > 0 (Eq. (7)'s sigma > 0.5), then the budget projection (Sec. 3.3
+    "Inference") with the logits as the units' confidences.  Returns
+    (keep, layer_on [L], head_on [L][A], ffn_on [L][G])."""
+    L = shape.n_layers
+    lo, ho, fo = masks_from_logits(shape, logits, prefix, units)
+    conf = np.zeros((L, units))
+    conf[prefix:] = np.asarray(logits, np.float64).reshape(L - prefix, units)
+    return project_sample(shape, z, n_text, budget, vocab, prefix, lo, ho, fo, conf, units=units)
+
+
+def finish_controlled(shape, layer_weights, prefix_resid, z, counts, keep, lm, hm, fm,
+                      prefix: int, n_text: int, counter: Optional[FlopCounter] = None):
+    """The controlled prefill after the decisions: each sample's sequence
+    after the prefix layers ([threshold-kept vision ; text ; budget token])
+    loses the visual tokens the projection discarded (the survivors keep their
+    order), then layers P..L-1 run under the masks.  Returns (kept_idx,
+    cu_seqlens, resid)."""
+    z = np.asarray(z)
+    B, N = z.shape
+    L, D = shape.n_layers, shape.d_model
+    T = n_text
+    seqs = [np.array(s, dtype=np.float64, copy=True) for s in prefix_resid]
+    kept_idx = np.full((B, N), -1, dtype=np.int32)
+    for b in range(B):
+        k = int(keep[b])
+        first = select_topk(z[b], int(counts[b]))
+        final = select_topk(z[b], k)
         kept_idx[b, :k] = final
         if k < counts[b]:
             # the discarded visual tokens leave the sequence at the prefix boundary
-            rows = np.concatenate([np.searchsorted(kept_first[b], final),
+            rows = np.concatenate([np.searchsorted(first, final),
                                    counts[b] + np.arange(T + 1)])
             seqs[b] = seqs[b][rows]
-
-    for l in range(P, L):
+    for l in range(prefix, L):
         if not lm[:, l].any():
             continue
         W = layer_weights(l)
@@ -236,5 +263,4 @@ def prefill_controlled(shape, layer_weights: Callable[[int], Dict[str, np.ndarra
     for b in range(B):
         cu[b + 1] = cu[b] + seqs[b].shape[0]
     resid = np.concatenate(seqs, axis=0) if seqs else np.zeros((0, D))
-    return ControlledResult(kept_idx, cu, resid.reshape(-1, D), keep, counts, kaps, logits,
-                            lm, hm, fm, prefix_resid, counter)
+    return kept_idx, cu, resid

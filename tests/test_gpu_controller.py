@@ -134,3 +134,60 @@ def test_controlled_headline_full_size():
     out, ref = _run(w, 0, prefix=16, units=4, budget=0.25, shift=-0.6745, pe_dim=256,
                     hidden=4096)
     assert ref.keep[0] < ref.counts[0]
+
+
+def test_controlled_near_zero_gate_logits_are_self_consistent():
+    """Sample 0's gate logits placed within float32 rounding of zero, where the
+    library's float32 decisions and the oracle's float64 ones may disagree.
+    Whatever the library decides must follow from its own reported float32
+    logits by the rule (a unit runs iff its logit > 0, then the budget
+    projection with the logits as confidences), and its hidden states must
+    equal the oracle's layers run under those decisions (same bar as the
+    other cases); the other samples keep ordinary logits and full parity."""
+    w = TINY4
+    seed, prefix, units, budget = 6, 1, 4, 0.6
+    print(f"controlled near-zero gates {w.name} seed={seed}", flush=True)
+    shape = w.shape
+    cfg = svl.make_config(shape)
+    inp = W.draw_inputs(w, seed, device="cuda")
+    layers = [W.draw_layer_weights(w, l, seed, device="cuda") for l in range(shape.n_layers)]
+    draw = W.draw_controller(w, seed, device="cuda", prefix=prefix, units=units)
+    rng = np.random.default_rng(seed + 17)
+    B, N, T, D = w.batch, w.n_vision, w.n_text, shape.d_model
+    z = (rng.standard_normal((B, N)) + 0.2).astype(np.float32)
+    hl = [host_layer(l) for l in layers]
+    vis, txt = W.as_f32(inp.vision), W.as_f32(inp.text)
+    ref = oc.prefill_controlled(shape, lambda l: hl[l], host_controller(draw), z, vis, txt, budget, 0)
+    # new biases: sample 0's float64 logits become 1e-9 of either sign
+    bias = W.as_f32(draw.tensors["gate_b"]).astype(np.float64)
+    sign = np.where(np.arange(bias.size) % 2 == 0, 1.0, -1.0)
+    nb = (bias - ref.logits[0] + 1e-9 * sign).astype(np.float32)
+    tensors = dict(draw.tensors)
+    tensors["gate_b"] = torch.from_numpy(nb).to(draw.tensors["gate_b"].device).to(
+        draw.tensors["gate_b"].dtype)
+    ctrl = svl.Controller(draw.prefix, draw.units, draw.pe_dim, draw.hidden, draw.pe_scale,
+                          draw.pe_base, tensors)
+    logits = torch.from_numpy(z).cuda()
+    kept = torch.full((B, N), -7, dtype=torch.int32, device="cuda")
+    resid = torch.full((B * (N + T + 1), D), float("nan"), dtype=torch.float32, device="cuda")
+    ws = svl.alloc_controlled_workspace(cfg, ctrl, B, N, T, "cuda")
+    out = svl.svl_prefill_controlled(cfg, svl.LayerTable(layers), ctrl, logits, inp.vision,
+                                     inp.text, budget, 0, kept, resid, ws)
+    torch.cuda.synchronize()
+    g = out["gate_logits"].astype(np.float64)
+    assert np.abs(g[0]).max() < 1e-4, "sample 0's logits should sit at zero"
+    for b in range(B):
+        k, lo, ho, fo = oc.decide_sample(shape, z[b], g[b], T, budget, 0, prefix, units)
+        assert int(out["keep"][b]) == k, b
+        np.testing.assert_array_equal(out["layer_mask"][b], lo)
+        np.testing.assert_array_equal(out["head_mask"][b], ho)
+        np.testing.assert_array_equal(out["ffn_mask"][b], fo)
+    kidx, cu, res = oc.finish_controlled(shape, lambda l: hl[l], ref.prefix_resid, z, ref.counts,
+                                         out["keep"], out["layer_mask"], out["head_mask"],
+                                         out["ffn_mask"], prefix, T)
+    np.testing.assert_array_equal(out["cu_seqlens"], cu)
+    np.testing.assert_array_equal(kept.cpu().numpy(), kidx)
+    errs = rel_err_per_sample(resid[:int(cu[-1])].cpu().numpy(), res, cu)
+    print(f"  sample 0 units on: {int(out['head_mask'][0].sum())}; rel err per sample: "
+          f"{[f'{e:.2e}' for e in errs]}", flush=True)
+    assert max(errs) <= tol_for(shape), errs
