@@ -114,10 +114,12 @@ def write_traffic(run_dir):
     import collections
     import csv
 
-    def per_dispatch(path):
+    def per_dispatch(path, counter):
         vals, names = collections.defaultdict(float), {}
         with open(path) as f:
             for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
                 d = int(r["Dispatch_Id"])
                 vals[d] += float(r["Counter_Value"])
                 names[d] = r["Kernel_Name"]
@@ -125,8 +127,8 @@ def write_traffic(run_dir):
 
     out = {"gemm_source_sha256": source_hash(GEMM_SOURCE), "copy_bytes": COPY_BYTES}
     for kind, sub in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
-        path = os.path.join(run_dir, kind, "t_counter_collection.csv")
-        vals, names = per_dispatch(path)
+        path = os.path.join(run_dir, kind, "p_counter_collection.csv")
+        vals, names = per_dispatch(path, sub)
         copies = [d for d, n in names.items() if "elementwise" in n or "copy" in n.lower()]
         if kind == "write":
             cal = max(copies, key=lambda d: vals[d])
@@ -142,9 +144,10 @@ def write_traffic(run_dir):
         out[f"{kind}_bytes_per_launch"] = sum(gu) / len(gu) * 1024.0 * factor
         out[f"{kind}_dispatches"] = len(gu)
         out[f"{kind}_counter"] = sub
-    out["command"] = ("rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE -d <dir>/fetch|write -o t "
-                      "--output-format csv -- python3 -u bench.py --steps 3 --warmup 1 "
-                      "--no-cpu-baseline --copy-calibration")
+    out["command"] = ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE TCP_TCC_READ_REQ_sum) "
+                      "-d <dir> -o p --output-format csv -- python3 -u bench.py --workload "
+                      "llava7b_b1_keep25 --steps 2 --warmup 1 --no-cpu-baseline --no-bf16-line "
+                      "--no-train-line --copy-calibration")
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out))
