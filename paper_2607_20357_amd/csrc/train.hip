@@ -285,50 +285,143 @@ __device__ __forceinline__ float quad_sum(float v) {
   return v;
 }
 
+// Forward: one workgroup = 64 query rows of one head.  The 64 x 64 score
+// block of each key tile is a register-tiled product (4 x 4 scores per
+// thread) of Q^T and K^T held in LDS; the probabilities go through LDS
+// (transposed) into the P V product (4 rows x HD/16 columns per thread).
+// The online softmax keeps each row's running max and sum in the 16
+// threads that share the row.
+template <int HD>
+struct FwdSmem {
+  float qt[HD][68];     // Q^T of the query tile, scaled by 1/sqrt(d)
+  float kt[HD][68];     // K^T of the key tile
+  float v[64][HD + 4];  // V rows of the key tile
+  float pt[64][68];     // P^T: pt[key][query]
+};
+
 template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
-  constexpr int PD = HD / 4;
-  __shared__ AttnTile<HD> sm;
+  constexpr int CPT = HD / 16;   // output columns per thread
+  constexpr int C4 = HD / 4;
+  __shared__ __attribute__((aligned(16))) FwdSmem<HD> sm;
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int rep = a.A / a.KV, g = h / rep;
-  const int qr = threadIdx.x >> 2, part = threadIdx.x & 3;
-  const int64_t i = (int64_t)qt * 64 + qr;
-  const bool valid = i < a.S;
+  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
   const int64_t base = (int64_t)b * a.S;
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
-  float q[PD], acc[PD];
-#pragma unroll
-  for (int x = 0; x < PD; ++x) {
-    q[x] = valid ? a.Q[(base + i) * ldq + (int64_t)h * HD + part * PD + x] * a.scale : 0.0f;
-    acc[x] = 0.0f;
+  const int64_t q0 = (int64_t)qt * 64;
+
+  for (int idx = t; idx < 64 * C4; idx += TNT) {
+    const int r = idx / C4, c = (idx % C4) * 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (q0 + r < a.S) v = f4scale(*reinterpret_cast<const float4*>(a.Q + (base + q0 + r) * ldq + (int64_t)h * HD + c), a.scale);
+    sm.qt[c + 0][r] = v.x;
+    sm.qt[c + 1][r] = v.y;
+    sm.qt[c + 2][r] = v.z;
+    sm.qt[c + 3][r] = v.w;
   }
-  float mx = -INFINITY, l = 0.0f;
+  float mrow[4], lrow[4], o[4][CPT];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    mrow[i] = -INFINITY;
+    lrow[i] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) o[i][c] = 0.0f;
+  }
   for (int kt = 0; kt <= qt; ++kt) {
+    const int64_t k0 = (int64_t)kt * 64;
+    __syncthreads();   // the previous tile's readers are done
+    for (int idx = t; idx < 64 * C4; idx += TNT) {
+      const int r = idx / C4, c = (idx % C4) * 4;
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
+      if (k0 + r < a.S) {
+        const int64_t off = (base + k0 + r) * ldk + (int64_t)g * HD + c;
+        kv = *reinterpret_cast<const float4*>(a.K + off);
+        vv = *reinterpret_cast<const float4*>(a.V + off);
+      }
+      sm.kt[c + 0][r] = kv.x;
+      sm.kt[c + 1][r] = kv.y;
+      sm.kt[c + 2][r] = kv.z;
+      sm.kt[c + 3][r] = kv.w;
+      *reinterpret_cast<float4*>(&sm.v[r][c]) = vv;
+    }
     __syncthreads();
-    load_rows<HD>(sm.a, a.K, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
-    load_rows<HD>(sm.b, a.V, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
+    float s[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s[i][j] = 0.0f;
+#pragma unroll 8
+    for (int d = 0; d < HD; ++d) {
+      const float4 x = *reinterpret_cast<const float4*>(&sm.qt[d][ty * 4]);
+      const float4 y = *reinterpret_cast<const float4*>(&sm.kt[d][tx * 4]);
+      const float xa[4] = {x.x, x.y, x.z, x.w}, ya[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[i][j] += xa[i] * ya[j];
+    }
+    float corr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qi = q0 + ty * 4 + i;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t kj = k0 + tx * 4 + j;
+        if (kj > qi || kj >= a.S) s[i][j] = -INFINITY;
+        mx = fmaxf(mx, s[i][j]);
+      }
+#pragma unroll
+      for (int o2 = 1; o2 < 16; o2 <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
+      const float mn = fmaxf(mrow[i], mx);
+      // a row with no valid key so far keeps max -inf: its probabilities are 0
+      const float mref = mn == -INFINITY ? 0.0f : mn;
+      corr[i] = expf(mrow[i] - mref);
+      float rs = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float p = expf(s[i][j] - mref);
+        s[i][j] = p;
+        rs += p;
+      }
+#pragma unroll
+      for (int o2 = 1; o2 < 16; o2 <<= 1) rs += __shfl_xor(rs, o2, 64);
+      lrow[i] = lrow[i] * corr[i] + rs;
+      mrow[i] = mn;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.pt[tx * 4 + j][ty * 4 + i] = s[i][j];
     __syncthreads();
-    if (!valid) continue;
-    int jn = (int)min((int64_t)64, a.S - (int64_t)kt * 64);
-    if (kt == qt) jn = min(jn, qr + 1);
-    for (int j = 0; j < jn; ++j) {
-      float s = 0.0f;
 #pragma unroll
-      for (int x = 0; x < PD; ++x) s += q[x] * sm.a[j][part * PD + x];
-      s = quad_sum(s);
-      const float mn = fmaxf(mx, s);
-      const float corr = expf(mx - mn), p = expf(s - mn);
-      l = l * corr + p;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int x = 0; x < PD; ++x) acc[x] = acc[x] * corr + p * sm.b[j][part * PD + x];
-      mx = mn;
+      for (int c = 0; c < CPT; ++c) o[i][c] *= corr[i];
+#pragma unroll 4
+    for (int k = 0; k < 64; ++k) {
+      const float4 pv = *reinterpret_cast<const float4*>(&sm.pt[k][ty * 4]);
+      const float pa[4] = {pv.x, pv.y, pv.z, pv.w};
+      float vv[CPT];
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) vv[c] = sm.v[k][tx * CPT + c];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) o[i][c] += pa[i] * vv[c];
     }
   }
-  if (!valid) return;
-  const float inv = 1.0f / l;
 #pragma unroll
-  for (int x = 0; x < PD; ++x) a.out[(base + i) * ldq + (int64_t)h * HD + part * PD + x] = acc[x] * inv;
-  if (part == 0) a.lse[(base + i) * a.A + h] = mx + logf(l);
+  for (int i = 0; i < 4; ++i) {
+    const int64_t qi = q0 + ty * 4 + i;
+    if (qi >= a.S) continue;
+    const float inv = 1.0f / lrow[i];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c)
+      a.out[(base + qi) * ldq + (int64_t)h * HD + tx * CPT + c] = o[i][c] * inv;
+    if (tx == 0) a.lse[(base + qi) * a.A + h] = mrow[i] + logf(lrow[i]);
+  }
 }
 
 // dQ_i = scale sum_j P_ij (dP_ij - D_i) k_j, dP_ij = dO_i . v_j,
