@@ -424,122 +424,231 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
   }
 }
 
-// dQ_i = scale sum_j P_ij (dP_ij - D_i) k_j, dP_ij = dO_i . v_j,
-// D_i = dO_i . O_i (also stored for the K / V gradient).
+// Loads rows [row0, row0 + 64) x columns [col0, col0 + HD) of a [M][ld]
+// float matrix transposed into dst[HD][68] (rows past `rows_left` read 0),
+// optionally scaled.
 template <int HD>
-__global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
-  constexpr int PD = HD / 4;
-  __shared__ AttnTile<HD> sm;
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int rep = a.A / a.KV, g = h / rep;
-  const int qr = threadIdx.x >> 2, part = threadIdx.x & 3;
-  const int64_t i = (int64_t)qt * 64 + qr;
-  const bool valid = i < a.S;
-  const int64_t base = (int64_t)b * a.S;
-  const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
-  const int64_t off = (base + (valid ? i : 0)) * ldq + (int64_t)h * HD + part * PD;
-  float q[PD], dout[PD], dq[PD];
-  float Di = 0.0f;
-#pragma unroll
-  for (int x = 0; x < PD; ++x) {
-    q[x] = valid ? a.Q[off + x] * a.scale : 0.0f;
-    dout[x] = valid ? a.dO[off + x] : 0.0f;
-    Di += valid ? dout[x] * a.O[off + x] : 0.0f;
-    dq[x] = 0.0f;
+__device__ __forceinline__ void load_t(float (*dst)[68], const float* src, int64_t row0, int64_t ld,
+                                       int64_t col0, int64_t rows_left, float scale) {
+  constexpr int C4 = HD / 4;
+  for (int idx = threadIdx.x; idx < 64 * C4; idx += TNT) {
+    const int r = idx / C4, c = (idx % C4) * 4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < rows_left) v = f4scale(*reinterpret_cast<const float4*>(src + (row0 + r) * ld + col0 + c), scale);
+    dst[c + 0][r] = v.x;
+    dst[c + 1][r] = v.y;
+    dst[c + 2][r] = v.z;
+    dst[c + 3][r] = v.w;
   }
-  Di = quad_sum(Di);
-  const float lse = valid ? a.lse[(base + i) * a.A + h] : 0.0f;
-  if (valid && part == 0) a.Dv[(base + i) * a.A + h] = Di;
-  for (int kt = 0; kt <= qt; ++kt) {
-    __syncthreads();
-    load_rows<HD>(sm.a, a.K, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
-    load_rows<HD>(sm.b, a.V, base + (int64_t)kt * 64, ldk, (int64_t)g * HD, a.S - (int64_t)kt * 64);
-    __syncthreads();
-    if (!valid) continue;
-    int jn = (int)min((int64_t)64, a.S - (int64_t)kt * 64);
-    if (kt == qt) jn = min(jn, qr + 1);
-    for (int j = 0; j < jn; ++j) {
-      float s = 0.0f, dp = 0.0f;
-#pragma unroll
-      for (int x = 0; x < PD; ++x) {
-        s += q[x] * sm.a[j][part * PD + x];
-        dp += dout[x] * sm.b[j][part * PD + x];
-      }
-      s = quad_sum(s);
-      dp = quad_sum(dp);
-      const float ds = expf(s - lse) * (dp - Di);
-#pragma unroll
-      for (int x = 0; x < PD; ++x) dq[x] += ds * sm.a[j][part * PD + x];
-    }
-  }
-  if (!valid) return;
-#pragma unroll
-  for (int x = 0; x < PD; ++x) a.out[off + x] = dq[x] * a.scale;
 }
 
-// dV_j = sum_{h of the group} sum_{i >= j} P_ij dO_i,
-// dK_j = scale sum_h sum_{i >= j} P_ij (dP_ij - D_i) q_i.
+// 4 x 4 block of sum_d A^T[d][4 ty + i] B^T[d][4 tx + j] over both operands'
+// transposed tiles in LDS.
 template <int HD>
-__global__ __launch_bounds__(TNT) void train_attn_dkv_kernel(TAttnArgs a) {
-  constexpr int PD = HD / 4;
-  __shared__ AttnTile<HD> sm;
-  const int kt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int rep = a.A / a.KV;
-  const int kr = threadIdx.x >> 2, part = threadIdx.x & 3;
-  const int64_t j = (int64_t)kt * 64 + kr;
-  const bool valid = j < a.S;
+__device__ __forceinline__ void tile_dot(const float (*at)[68], const float (*bt)[68], int ty,
+                                         int tx, float (&acc)[4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+#pragma unroll 8
+  for (int d = 0; d < HD; ++d) {
+    const float4 x = *reinterpret_cast<const float4*>(&at[d][ty * 4]);
+    const float4 y = *reinterpret_cast<const float4*>(&bt[d][tx * 4]);
+    const float xa[4] = {x.x, x.y, x.z, x.w}, ya[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] += xa[i] * ya[j];
+  }
+}
+
+// acc[i][c] += sum_r w[r][4 ty + i] m^T[tx CPT + c][r] over the 64 rows r of
+// a 64 x 64 weight block w (LDS, [r][68]) and a transposed operand m^T (LDS).
+template <int HD>
+__device__ __forceinline__ void tile_acc(const float (*w)[68], const float (*mt)[68], int ty,
+                                         int tx, float (&acc)[4][HD / 16]) {
+  constexpr int CPT = HD / 16;
+#pragma unroll 4
+  for (int r = 0; r < 64; ++r) {
+    const float4 wv = *reinterpret_cast<const float4*>(&w[r][ty * 4]);
+    const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
+    float mv[CPT];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) mv[c] = mt[tx * CPT + c][r];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) acc[i][c] += wa[i] * mv[c];
+  }
+}
+
+// Query gradient: one workgroup = 64 query rows of one head.  Per key tile
+// the score block S = (Q scale) K^T and dP = dO V^T are register-tiled
+// products of transposed tiles in LDS; dS = P (dP - D) with P = exp(S - lse)
+// goes through LDS into dQ += dS K (scaled at the end).  D = dO . O per row
+// is formed first and stored for the key / value gradient.
+template <int HD>
+struct DqSmem {
+  float qt[HD][68];
+  float dot[HD][68];
+  float kt[HD][68];
+  float vt[HD][68];
+  float ds[64][68];     // ds[key][query]
+};
+
+template <int HD>
+__global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
+  constexpr int CPT = HD / 16;
+  __shared__ __attribute__((aligned(16))) DqSmem<HD> sm;
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int rep = a.A / a.KV, g = h / rep;
+  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
   const int64_t base = (int64_t)b * a.S;
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
-  const int64_t koff = (base + (valid ? j : 0)) * ldk + (int64_t)g * HD + part * PD;
-  float k[PD], v[PD], dk[PD], dv[PD];
+  const int64_t q0 = (int64_t)qt * 64;
+  load_t<HD>(sm.qt, a.Q, base + q0, ldq, (int64_t)h * HD, a.S - q0, a.scale);
+  load_t<HD>(sm.dot, a.dO, base + q0, ldq, (int64_t)h * HD, a.S - q0, 1.0f);
+  // D and lse of this thread's four rows (D over the thread's columns, then the row)
+  float Dr[4], lse[4];
 #pragma unroll
-  for (int x = 0; x < PD; ++x) {
-    k[x] = valid ? a.K[koff + x] : 0.0f;
-    v[x] = valid ? a.V[koff + x] : 0.0f;
-    dk[x] = 0.0f;
-    dv[x] = 0.0f;
+  for (int i = 0; i < 4; ++i) {
+    const int64_t qi = q0 + ty * 4 + i;
+    float d = 0.0f;
+    if (qi < a.S) {
+      const int64_t off = (base + qi) * ldq + (int64_t)h * HD + tx * CPT;
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) d += a.dO[off + c] * a.O[off + c];
+    }
+#pragma unroll
+    for (int o2 = 1; o2 < 16; o2 <<= 1) d += __shfl_xor(d, o2, 64);
+    Dr[i] = d;
+    lse[i] = qi < a.S ? a.lse[(base + qi) * a.A + h] : 0.0f;
+    if (tx == 0 && qi < a.S) a.Dv[(base + qi) * a.A + h] = d;
   }
+  float acc[4][CPT];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) acc[i][c] = 0.0f;
+  for (int kt = 0; kt <= qt; ++kt) {
+    const int64_t k0 = (int64_t)kt * 64;
+    __syncthreads();
+    load_t<HD>(sm.kt, a.K, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
+    load_t<HD>(sm.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
+    __syncthreads();
+    float s[4][4], dp[4][4];
+    tile_dot<HD>(sm.qt, sm.kt, ty, tx, s);
+    tile_dot<HD>(sm.dot, sm.vt, ty, tx, dp);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qi = q0 + ty * 4 + i;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t kj = k0 + tx * 4 + j;
+        const float p = (kj <= qi && kj < a.S && qi < a.S) ? expf(s[i][j] - lse[i]) : 0.0f;
+        sm.ds[tx * 4 + j][ty * 4 + i] = p * (dp[i][j] - Dr[i]);
+      }
+    }
+    __syncthreads();
+    // dQ[q][d] += sum_k dS[q][k] K[k][d]: rows of ds are keys, K^T is kt
+    tile_acc<HD>(sm.ds, sm.kt, ty, tx, acc);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t qi = q0 + ty * 4 + i;
+    if (qi >= a.S) continue;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c)
+      a.out[(base + qi) * ldq + (int64_t)h * HD + tx * CPT + c] = acc[i][c] * a.scale;
+  }
+}
+
+// Key / value gradient: one workgroup = 64 key rows of one K/V head; for
+// each query head of the group and each query tile at or after the key
+// tile: S^T = K (Q scale)^T and dP^T = V dO^T (register-tiled, transposed
+// tiles in LDS), P^T = exp(S^T - lse), then dV += P^T dO and, through the
+// same LDS block, dK += dS^T (Q scale) with dS^T = P^T (dP^T - D) (the
+// scaled query tile carries the 1/sqrt(d) of dK).
+template <int HD>
+struct DkvSmem {
+  float kt[HD][68];     // K^T of the workgroup's keys
+  float vt[HD][68];     // V^T
+  float qt[HD][68];     // Q^T of the query tile (scaled)
+  float dot[HD][68];    // dO^T of the query tile
+  float w[64][68];      // w[query][key]: P, then dS
+  float lse[64], dv[64];
+};
+
+template <int HD>
+__global__ __launch_bounds__(TNT) void train_attn_dkv_kernel(TAttnArgs a) {
+  constexpr int CPT = HD / 16;
+  __shared__ __attribute__((aligned(16))) DkvSmem<HD> sm;
+  const int kt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int rep = a.A / a.KV;
+  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int64_t base = (int64_t)b * a.S;
+  const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
+  const int64_t k0 = (int64_t)kt * 64;
+  load_t<HD>(sm.kt, a.K, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
+  load_t<HD>(sm.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
+  float gk[4][CPT], gv[4][CPT];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) gk[i][c] = gv[i][c] = 0.0f;
   const int nqt = (int)((a.S + 63) / 64);
   for (int h = g * rep; h < (g + 1) * rep; ++h) {
     for (int qt = kt; qt < nqt; ++qt) {
-      const int64_t rows_left = a.S - (int64_t)qt * 64;
+      const int64_t q0 = (int64_t)qt * 64;
       __syncthreads();
-      load_rows<HD>(sm.a, a.Q, base + (int64_t)qt * 64, ldq, (int64_t)h * HD, rows_left);
-      load_rows<HD>(sm.b, a.dO, base + (int64_t)qt * 64, ldq, (int64_t)h * HD, rows_left);
-      if (threadIdx.x < 64) {
-        const bool in = threadIdx.x < rows_left;
-        const int64_t r = base + (int64_t)qt * 64 + threadIdx.x;
-        sm.s0[threadIdx.x] = in ? a.lse[r * a.A + h] : 0.0f;
-        sm.s1[threadIdx.x] = in ? a.Dv[r * a.A + h] : 0.0f;
+      load_t<HD>(sm.qt, a.Q, base + q0, ldq, (int64_t)h * HD, a.S - q0, a.scale);
+      load_t<HD>(sm.dot, a.dO, base + q0, ldq, (int64_t)h * HD, a.S - q0, 1.0f);
+      if (t < 64) {
+        const bool in = q0 + t < a.S;
+        sm.lse[t] = in ? a.lse[(base + q0 + t) * a.A + h] : 0.0f;
+        sm.dv[t] = in ? a.Dv[(base + q0 + t) * a.A + h] : 0.0f;
       }
       __syncthreads();
-      if (!valid) continue;
-      const int i0 = qt == kt ? kr : 0;
-      const int in = (int)min((int64_t)64, rows_left);
-      for (int ii = i0; ii < in; ++ii) {
-        float s = 0.0f, dp = 0.0f;
+      float s[4][4], dp[4][4];
+      tile_dot<HD>(sm.kt, sm.qt, ty, tx, s);     // [key ty*4+i][query tx*4+j]
+      tile_dot<HD>(sm.vt, sm.dot, ty, tx, dp);
+      float p[4][4];
 #pragma unroll
-        for (int x = 0; x < PD; ++x) {
-          s += sm.a[ii][part * PD + x] * k[x];
-          dp += sm.b[ii][part * PD + x] * v[x];
-        }
-        s = quad_sum(s) * a.scale;
-        dp = quad_sum(dp);
-        const float p = expf(s - sm.s0[ii]);
-        const float ds = p * (dp - sm.s1[ii]);
+      for (int i = 0; i < 4; ++i) {
+        const int64_t ki = k0 + ty * 4 + i;
 #pragma unroll
-        for (int x = 0; x < PD; ++x) {
-          dv[x] += p * sm.b[ii][part * PD + x];
-          dk[x] += ds * sm.a[ii][part * PD + x];
+        for (int j = 0; j < 4; ++j) {
+          const int qj = tx * 4 + j;
+          const int64_t q = q0 + qj;
+          p[i][j] = (q >= ki && q < a.S && ki < a.S) ? expf(s[i][j] - sm.lse[qj]) : 0.0f;
+          sm.w[qj][ty * 4 + i] = p[i][j];
         }
       }
+      __syncthreads();
+      tile_acc<HD>(sm.w, sm.dot, ty, tx, gv);    // dV[k][d] += sum_q P[q][k] dO[q][d]
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int qj = tx * 4 + j;
+          sm.w[qj][ty * 4 + i] = p[i][j] * (dp[i][j] - sm.dv[qj]);
+        }
+      __syncthreads();
+      tile_acc<HD>(sm.w, sm.qt, ty, tx, gk);     // dK[k][d] += sum_q dS[q][k] (Q scale)[q][d]
     }
   }
-  if (!valid) return;
 #pragma unroll
-  for (int x = 0; x < PD; ++x) {
-    a.dK[koff + x] = dk[x] * a.scale;
-    a.dV[koff + x] = dv[x];
+  for (int i = 0; i < 4; ++i) {
+    const int64_t ki = k0 + ty * 4 + i;
+    if (ki >= a.S) continue;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int64_t off = (base + ki) * ldk + (int64_t)g * HD + tx * CPT + c;
+      a.dK[off] = gk[i][c];
+      a.dV[off] = gv[i][c];
+    }
   }
 }
 
