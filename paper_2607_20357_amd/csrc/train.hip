@@ -156,19 +156,25 @@ __global__ __launch_bounds__(TNT) void train_norm_bwd_kernel(const float* X, con
 
 // ------------------------------------------------------------------ matrix products
 // C[M][N] = R + (s . A)[M][K] op(B): BL = 0 reads B as [N][K] (x W^T with
-// W = [out][in]), BL = 1 as [K][N] (dY W).  64 x 64 output tiles, K in steps
-// of 16 staged through LDS, 4 x 4 outputs per thread.  With ASC, A[m][k] is
-// scaled by ascale[(m / S) astride + k / kg] (the unit masks).
-constexpr int GBM = 64, GBN = 64, GBK = 16, GPAD = 4;
+// W = [out][in]), BL = 1 as [K][N] (dY W).  64 x 64 output tiles over four
+// waves (32 x 32 each, 2 x 2 blocks of v_mfma_f32_16x16x4_f32, float32 in
+// and out); K in steps of 16 staged through LDS k-major, so a fragment is one
+// 4-byte read per lane; the next step's operands are in registers while the
+// current one multiplies.  With ASC, A[m][k] is scaled by
+// ascale[(m / S) astride + k / kg] (the unit masks).
+constexpr int GBM = 64, GBN = 64, GBK = 16, GLD = 80;   // LDS row stride (floats)
 
 template <int BL, class TB, bool ASC>
 __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
-  __shared__ __attribute__((aligned(16))) float As[GBK][GBM + GPAD];
-  __shared__ __attribute__((aligned(16))) float Bs[GBK][GBN + GPAD];
-  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  __shared__ __attribute__((aligned(16))) float As[GBK][GLD];   // As[k][m]
+  __shared__ __attribute__((aligned(16))) float Bs[GBK][GLD];   // Bs[k][n]
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wy = wave >> 1, wx = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * GBM, n0 = (int64_t)blockIdx.x * GBN;
   const TB* B = static_cast<const TB*>(a.B);
 
+  // global -> register loads: A row ar, k ak..ak+3; B as [N][K] row bn, k bk..,
+  // or as [K][N] row bk, n bn..
   const int ar = t >> 2, ak = (t & 3) * 4;
   const int64_t arow = m0 + ar;
   const bool aok = arow < a.M;
@@ -176,26 +182,35 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   if constexpr (BL == 0) { bn = t >> 2; bk = (t & 3) * 4; }
   else { bk = t >> 4; bn = (t & 15) * 4; }
   const bool bok = n0 + bn < a.N;
-
-  float acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
-
   const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int64_t k0 = 0; k0 < a.K; k0 += GBK) {
-    float4 av = zero;
+  auto load_a = [&](int64_t k0) {
+    float4 v = zero;
     if (aok) {
-      av = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + ak);
-      if constexpr (ASC) av = f4scale(av, a.ascale[(arow / a.S) * a.astride + (k0 + ak) / a.kg]);
+      v = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + ak);
+      if constexpr (ASC) v = f4scale(v, a.ascale[(arow / a.S) * a.astride + (k0 + ak) / a.kg]);
     }
-    float4 bv = zero;
+    return v;
+  };
+  auto load_b = [&](int64_t k0) {
+    float4 v = zero;
     if (bok) {
-      if constexpr (BL == 0) bv = ld4(B, (n0 + bn) * a.ldb + k0 + bk);
-      else bv = ld4(B, (k0 + bk) * a.ldb + n0 + bn);
+      if constexpr (BL == 0) v = ld4(B, (n0 + bn) * a.ldb + k0 + bk);
+      else v = ld4(B, (k0 + bk) * a.ldb + n0 + bn);
     }
-    __syncthreads();
+    return v;
+  };
+
+  floatx4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // fragment reads: lane l takes row (or column) 16 blk + l % 16 at k = l / 16
+  const int fr = lane & 15, fk = lane >> 4;
+
+  float4 av = load_a(0), bv = load_b(0);
+  for (int64_t k0 = 0; k0 < a.K; k0 += GBK) {
+    __syncthreads();   // the previous step's readers are done
     As[ak + 0][ar] = av.x;
     As[ak + 1][ar] = av.y;
     As[ak + 2][ar] = av.z;
@@ -209,31 +224,40 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
       *reinterpret_cast<float4*>(&Bs[bk][bn]) = bv;
     }
     __syncthreads();
+    if (k0 + GBK < a.K) {
+      av = load_a(k0 + GBK);
+      bv = load_b(k0 + GBK);
+    }
 #pragma unroll
-    for (int k = 0; k < GBK; ++k) {
-      const float4 x = *reinterpret_cast<const float4*>(&As[k][ty * 4]);
-      const float4 y = *reinterpret_cast<const float4*>(&Bs[k][tx * 4]);
-      const float xa[4] = {x.x, x.y, x.z, x.w};
-      const float ya[4] = {y.x, y.y, y.z, y.w};
+    for (int kk = 0; kk < GBK; kk += 4) {
+      float fa[2], fb[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 2; ++i) fa[i] = As[kk + fk][32 * wy + 16 * i + fr];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += xa[i] * ya[j];
+      for (int j = 0; j < 2; ++j) fb[j] = Bs[kk + fk][32 * wx + 16 * j + fr];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
   }
 
-  const int64_t col = n0 + tx * 4;
-  if (col >= a.N) return;
+  // acc[i][j][r] = C[32 wy + 16 i + 4 (lane / 16) + r][32 wx + 16 j + lane % 16]
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t row = m0 + ty * 4 + i;
-    if (row >= a.M) break;
-    float4 o = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
-    if (a.R) {
-      const float4 rv = *reinterpret_cast<const float4*>(a.R + row * a.ldr + col);
-      o = make_float4(rv.x + o.x, rv.y + o.y, rv.z + o.z, rv.w + o.w);
-    }
-    *reinterpret_cast<float4*>(a.C + row * a.ldc + col) = o;
+  for (int j = 0; j < 2; ++j) {
+    const int64_t col = n0 + 32 * wx + 16 * j + fr;
+    if (col >= a.N) continue;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = m0 + 32 * wy + 16 * i + 4 * fk + r;
+        if (row >= a.M) continue;
+        float o = acc[i][j][r];
+        if (a.R) o += a.R[row * a.ldr + col];
+        a.C[row * a.ldc + col] = o;
+      }
   }
 }
 
