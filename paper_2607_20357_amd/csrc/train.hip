@@ -158,11 +158,11 @@ __global__ __launch_bounds__(TNT) void train_norm_bwd_kernel(const float* X, con
 // C[M][N] = R + (s . A)[M][K] op(B): BL = 0 reads B as [N][K] (x W^T with
 // W = [out][in]), BL = 1 as [K][N] (dY W).  64 x 64 output tiles over four
 // waves (32 x 32 each, 2 x 2 blocks of v_mfma_f32_16x16x4_f32, float32 in
-// and out); K in steps of 16 staged through LDS k-major, so a fragment is one
-// 4-byte read per lane; the next step's operands are in registers while the
-// current one multiplies.  With ASC, A[m][k] is scaled by
+// and out); K in steps of 32 staged through LDS k-major, so a fragment is one
+// 4-byte read per lane (K % 16 == 0: a last half step reads as zero); the
+// next step's operands are in registers while the current one multiplies.  With ASC, A[m][k] is scaled by
 // ascale[(m / S) astride + k / kg] (the unit masks).
-constexpr int GBM = 64, GBN = 64, GBK = 16, GLD = 80;   // LDS row stride (floats)
+constexpr int GBM = 64, GBN = 64, GBK = 32, GLD = 80;   // LDS row stride (floats)
 
 template <int BL, class TB, bool ASC>
 __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
@@ -183,21 +183,25 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   else { bk = t >> 4; bn = (t & 15) * 4; }
   const bool bok = n0 + bn < a.N;
   const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-  auto load_a = [&](int64_t k0) {
-    float4 v = zero;
-    if (aok) {
-      v = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + ak);
-      if constexpr (ASC) v = f4scale(v, a.ascale[(arow / a.S) * a.astride + (k0 + ak) / a.kg]);
+  auto load_a = [&](int64_t k0, float4 (&v)[2]) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      v[h2] = zero;
+      if (aok && k0 + 16 * h2 < a.K) {   // K % 32 == 16: the second half of the last step is 0
+        v[h2] = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + 16 * h2 + ak);
+        if constexpr (ASC) v[h2] = f4scale(v[h2], a.ascale[(arow / a.S) * a.astride + (k0 + 16 * h2 + ak) / a.kg]);
+      }
     }
-    return v;
   };
-  auto load_b = [&](int64_t k0) {
-    float4 v = zero;
-    if (bok) {
-      if constexpr (BL == 0) v = ld4(B, (n0 + bn) * a.ldb + k0 + bk);
-      else v = ld4(B, (k0 + bk) * a.ldb + n0 + bn);
+  auto load_b = [&](int64_t k0, float4 (&v)[2]) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      v[h2] = zero;
+      if (bok && k0 + 16 * h2 < a.K) {
+        if constexpr (BL == 0) v[h2] = ld4(B, (n0 + bn) * a.ldb + k0 + 16 * h2 + bk);
+        else v[h2] = ld4(B, (k0 + 16 * h2 + bk) * a.ldb + n0 + bn);
+      }
     }
-    return v;
   };
 
   floatx4 acc[2][2];
@@ -208,25 +212,31 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   // fragment reads: lane l takes row (or column) 16 blk + l % 16 at k = l / 16
   const int fr = lane & 15, fk = lane >> 4;
 
-  float4 av = load_a(0), bv = load_b(0);
+  float4 av[2], bv[2];
+  load_a(0, av);
+  load_b(0, bv);
   for (int64_t k0 = 0; k0 < a.K; k0 += GBK) {
     __syncthreads();   // the previous step's readers are done
-    As[ak + 0][ar] = av.x;
-    As[ak + 1][ar] = av.y;
-    As[ak + 2][ar] = av.z;
-    As[ak + 3][ar] = av.w;
-    if constexpr (BL == 0) {
-      Bs[bk + 0][bn] = bv.x;
-      Bs[bk + 1][bn] = bv.y;
-      Bs[bk + 2][bn] = bv.z;
-      Bs[bk + 3][bn] = bv.w;
-    } else {
-      *reinterpret_cast<float4*>(&Bs[bk][bn]) = bv;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int kb = 16 * h2;
+      As[kb + ak + 0][ar] = av[h2].x;
+      As[kb + ak + 1][ar] = av[h2].y;
+      As[kb + ak + 2][ar] = av[h2].z;
+      As[kb + ak + 3][ar] = av[h2].w;
+      if constexpr (BL == 0) {
+        Bs[kb + bk + 0][bn] = bv[h2].x;
+        Bs[kb + bk + 1][bn] = bv[h2].y;
+        Bs[kb + bk + 2][bn] = bv[h2].z;
+        Bs[kb + bk + 3][bn] = bv[h2].w;
+      } else {
+        *reinterpret_cast<float4*>(&Bs[kb + bk][bn]) = bv[h2];
+      }
     }
     __syncthreads();
     if (k0 + GBK < a.K) {
-      av = load_a(k0 + GBK);
-      bv = load_b(k0 + GBK);
+      load_a(k0 + GBK, av);
+      load_b(k0 + GBK, bv);
     }
 #pragma unroll
     for (int kk = 0; kk < GBK; kk += 4) {
