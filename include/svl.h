@@ -25,7 +25,8 @@
  *   stream).  All device work is enqueued on it; device outputs are valid once
  *   the stream reaches that point.  No call synchronises the stream, except
  *   svl_count_positive and svl_prefill_controlled (host outputs that the
- *   host plans from).
+ *   host plans from) and svl_workspace_status (a host copy of a status
+ *   word).
  * Dtypes.  `svl_config.dtype` selects the storage type of weights and of the
  *   vision / text hidden states: SVL_F32 (float) or SVL_BF16 (bfloat16).  The
  *   residual stream `resid` is always float32.  SVL_BF16 runs 16-bit MFMA
@@ -352,6 +353,22 @@ svl_status svl_budget_loss(const svl_config *cfg, const svl_budget_loss_params *
                            const float *gate_logits, const float *gate_noise,
                            uint8_t *token_mask, uint8_t *unit_mask, float *ratio, float *loss,
                            float *grad_logits, float *grad_gate, void *stream);
+
+/* ---- status of the last prefill on a workspace ---------------------------
+ * With fp16 activations (SVL_COMPUTE_F16) a value outside fp16's range
+ * becomes inf when it is converted, and the inf (or the NaN it produces)
+ * reaches the output rows; the call itself still returns SVL_OK.  At its
+ * end every svl_prefill and svl_prefill_cache clears a status word in the
+ * last four bytes of its workspace buffer (ws + (ws_bytes & ~3) - 4) and
+ * sets it to SVL_STATUS_NONFINITE if any of its output values (resid rows
+ * 0 .. sum S_b - 1) is inf or NaN, whatever the cause (fp16 overflow, or
+ * non-finite inputs or weights).  svl_workspace_status copies that word to
+ * *status (host) once `stream` has reached it: it synchronises the stream.
+ * After other calls on the same buffer the word is undefined.
+ * Errors: SVL_E_NULL (ws or status NULL), SVL_E_ALIGN, SVL_E_WORKSPACE
+ * (ws_bytes < 256), SVL_E_HIP. */
+#define SVL_STATUS_NONFINITE 1u
+svl_status svl_workspace_status(const void *ws, size_t ws_bytes, uint32_t *status, void *stream);
 
 /* ---- training-time masked decoder ----------------------------------------
  * The prediction side of a training step (Sec. 3.1 Eq. (6); Sec. 3.2).  The

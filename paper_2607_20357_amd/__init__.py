@@ -12,5 +12,6 @@ from .binding import (  # noqa: F401
     svl_decode_step, svl_decode_step_noalloc, svl_kv_cache_bytes, svl_layer_forward, svl_prefill, svl_prefill_cache,
     svl_prefill_controlled, svl_select_tokens, svl_timing_enable, svl_timing_read,
     svl_workspace_bytes, alloc_train_workspace, svl_train_params, svl_train_step,
+    SVL_STATUS_NONFINITE, svl_workspace_status,
     svl_train_workspace_bytes,
 )

@@ -130,6 +130,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.svl_train_step.argtypes = [cfgp, ctypes.POINTER(svl_layer_weights),
                                    ctypes.POINTER(svl_train_params), i32, i32, i32, P, P, P, P, P,
                                    P, P, P, P, P, P, P, P, sz, P]
+    lib.svl_workspace_status.argtypes = [P, sz, ctypes.POINTER(ctypes.c_uint32), P]
     lib.svl_workspace_bytes.argtypes = [cfgp, i32, i32]
     lib.svl_workspace_bytes.restype = sz
     lib.svl_count_flops.argtypes = [cfgp, i32, ctypes.POINTER(i32), P, P, P,
@@ -143,7 +144,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
               "svl_timing_enable", "svl_timing_read", "svl_count_positive", "svl_budget_project",
               "svl_prefill_cache", "svl_decode_step", "svl_decode_step_noalloc",
               "svl_prefill_controlled",
-              "svl_budget_loss", "svl_train_step"):
+              "svl_budget_loss", "svl_train_step", "svl_workspace_status"):
         getattr(lib, f).restype = i32
     _lib = lib
     return lib
@@ -335,6 +336,19 @@ def svl_workspace_bytes(cfg: svl_config, batch: int, total_rows: int) -> int:
     if n == 0:
         raise SvlError(2, "svl_workspace_bytes: invalid configuration")
     return int(n)
+
+
+SVL_STATUS_NONFINITE = 1
+
+
+def svl_workspace_status(ws: torch.Tensor, stream=None) -> int:
+    """Status word of the last svl_prefill / svl_prefill_cache on `ws`
+    (SVL_STATUS_NONFINITE: an output value was inf or NaN); synchronises the
+    stream."""
+    out = ctypes.c_uint32(0)
+    _check(load_library().svl_workspace_status(_dev(ws, "ws"), _nbytes(ws), ctypes.byref(out),
+                                               _stream(stream)))
+    return int(out.value)
 
 
 def alloc_workspace(cfg: svl_config, batch: int, total_rows: int, device="cuda") -> torch.Tensor:

@@ -126,6 +126,13 @@ struct WsLayout {
 // the 16-bit MFMA path); the partial region holds the float32 split-K slices.
 // pos_rows: RoPE table rows (positions) when they exceed R (decode: max_len).
 // Decode (pos_rows > 0) never splits K, so its layout has no partial region.
+// The status word: the last four bytes of the caller's workspace buffer
+// (inside the 256 bytes every layout reserves at its end, or past the
+// layout when the buffer is larger).
+uint32_t* status_word(void* ws, size_t ws_bytes) {
+  return reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + ((ws_bytes & ~size_t(3)) - 4));
+}
+
 WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows = 0) {
   const int64_t es = c.dtype == SVL_BF16 ? 2 : 4;
   const int64_t prow = std::max<int64_t>(padded_rows_bound(c, B, R), 16);
@@ -145,6 +152,7 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows =
   L.qkv = take(prow * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
   L.attn_out = take(prow * (int64_t)c.n_heads * c.head_dim * es);
   L.h = take(prow * (int64_t)c.d_ffn * es);
+  take(256);   // the last bytes of the buffer hold the call's status word (svl_workspace_status)
   L.total = off;
   return L;
 }
@@ -710,6 +718,12 @@ static svl_status prefill_impl(const svl_config* cfg, const svl_layer_weights* l
   }
   hipError_t e = ex.norm(t_plan.final_norm, nullptr);
   if (e != hipSuccess) return hip_fail(e, "final residual launch");
+  // the status word: cleared, then set if an output value is inf or NaN
+  uint32_t* status = status_word(ws, ws_bytes);
+  if ((e = launch_fill_i32(reinterpret_cast<int32_t*>(status), 0, 1, ex.st)) != hipSuccess)
+    return hip_fail(e, "status clear");
+  if ((e = launch_nonfinite(resid, (int64_t)R * cfg->d_model, status, ex.st)) != hipSuccess)
+    return hip_fail(e, "status scan");
   return SVL_OK;
 }
 
@@ -732,6 +746,20 @@ svl_status svl_prefill_cache(const svl_config* cfg, const svl_layer_weights* lay
   if (!kv_cache) return fail(SVL_E_NULL, "kv_cache is NULL");
   return prefill_impl(cfg, layers, batch, scores, vision, text, layer_mask, head_mask, ffn_mask,
                       kept_idx, resid, cu_seqlens, nullptr, ws, ws_bytes, stream, kv_cache, max_len);
+}
+
+svl_status svl_workspace_status(const void* ws, size_t ws_bytes, uint32_t* status, void* stream) {
+  if (!ws || !status) return fail(SVL_E_NULL, "ws and status are required");
+  if (!aligned16(ws)) return fail(SVL_E_ALIGN, "workspace not 16-byte aligned");
+  if (ws_bytes < 256) return fail(SVL_E_WORKSPACE, "workspace of %zu bytes holds no status word", ws_bytes);
+  const uint32_t* w = status_word(const_cast<void*>(ws), ws_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t v = 0;
+  hipError_t e = hipMemcpyAsync(&v, w, sizeof(v), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "status read");
+  *status = v;
+  return SVL_OK;
 }
 
 size_t svl_kv_cache_bytes(const svl_config* cfg, int32_t batch, int32_t max_len) {

@@ -106,6 +106,18 @@ __global__ void rope_table_kernel(float2* table, int max_pos, int half, double t
   table[idx] = make_float2((float)cs, (float)sn);
 }
 
+// Sets *flag when one of x[0..4 n4) is inf or NaN (x 16-byte aligned);
+// every thread that finds one stores the same value.
+__global__ void nonfinite_kernel(const float4* x, int64_t n4, uint32_t* flag) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  bool bad = false;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    const float4 v = x[i];
+    bad = bad || !isfinite(v.x) || !isfinite(v.y) || !isfinite(v.z) || !isfinite(v.w);
+  }
+  if (bad) *flag = SVL_STATUS_NONFINITE;
+}
+
 __global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -340,6 +352,14 @@ hipError_t launch_rope_table(float2* table, int32_t max_pos, int32_t head_dim, f
   if (n <= 0) return hipSuccess;
   rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(table, max_pos, half,
                                                                    (double)theta);
+  return hipGetLastError();
+}
+
+hipError_t launch_nonfinite(const float* x, int64_t n, uint32_t* flag, hipStream_t st) {
+  const int64_t n4 = n / 4;
+  if (n4 <= 0) return hipSuccess;
+  const int64_t blocks = (n4 + 255) / 256 < 2048 ? (n4 + 255) / 256 : 2048;
+  nonfinite_kernel<<<(unsigned)blocks, 256, 0, st>>>(reinterpret_cast<const float4*>(x), n4, flag);
   return hipGetLastError();
 }
 

@@ -216,6 +216,8 @@ hipError_t launch_budget_rows(const float* eb, const int32_t* cu, int32_t B, int
 hipError_t launch_compact_rows(const CompactArgs& a, int32_t rows, hipStream_t st);
 hipError_t launch_budget_loss(const BudgetLossArgs& a, int32_t B, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t st);
+// *flag = SVL_STATUS_NONFINITE if one of x[0..n) (n % 4 == 0) is inf or NaN
+hipError_t launch_nonfinite(const float* x, int64_t n, uint32_t* flag, hipStream_t st);
 
 // Shared by the C-ABI sources: sets the per-thread message of svl_last_error
 // and returns st; validates a config as every entry point does.

@@ -479,3 +479,24 @@ def test_train_step_rejects_bad_arguments():
     sizes = [lib.svl_train_workspace_bytes(ctypes.byref(cfg), ctypes.byref(prm()), b, 8, 3)
              for b in (1, 2, 4)]
     assert sizes[0] < sizes[1] < sizes[2]
+
+
+def test_workspace_status_rejects_bad_arguments():
+    """Host-side checks of svl_workspace_status (no copy is issued)."""
+    lib = svl.load_library()
+    dev = 16 * 4096 * 100
+    out = ctypes.c_uint32(7)
+    assert lib.svl_workspace_status(None, 4096, ctypes.byref(out), None) == 1
+    assert lib.svl_workspace_status(dev, 4096, None, None) == 1
+    assert lib.svl_workspace_status(dev + 4, 4096, ctypes.byref(out), None) == 7
+    assert lib.svl_workspace_status(dev, 255, ctypes.byref(out), None) == 4
+    assert out.value == 7
+
+
+def test_every_workspace_layout_reserves_the_status_word():
+    """svl_workspace_bytes grows by the 256 bytes that hold the status word at
+    the end of the buffer, for every workload shape."""
+    for name, w in WORKLOADS.items():
+        cfg = svl.make_config(w.shape)
+        n = svl.svl_workspace_bytes(cfg, w.batch, w.batch * (w.n_vision + w.n_text))
+        assert n >= 256 and n % 256 == 0, name
