@@ -812,6 +812,9 @@ def main():
         flops = svl.svl_count_flops(cfg, seqlens, lm_run, hm_run, fm_run)
         bytes_, launches = gemm_bytes(shape, seqlens, lm_run, hm_run, fm_run)
     gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
+    gemm_bytes_total = sum(bytes_.values())
+    gemm_t_mfma = gemm_flops / (BF16_PEAK_TFLOPS * 1e12)
+    gemm_floor = max(gemm_t_mfma, gemm_bytes_total / (HBM_PEAK_GBS * 1e9))
     eq8 = eq8_flops(shape, seqlens, lm_run, hm_run, w.n_vision, w.n_text)
     gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / args.steps
     attn_ms = ktime["attention"][0] / args.steps
@@ -872,6 +875,14 @@ def main():
         "mfma_util_attn_pct": round(100 * flops["attn"] / (attn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 3)
         if attn_ms > 0 else None,
         "gemm_ms_per_step": round(gemm_ms, 4),
+        # the GEMMs' floor is the larger of their MFMA time at the dense peak
+        # and their algorithmic bytes at 8 TB/s; the ceiling of the MFMA
+        # fraction is that MFMA time over the floor (HBM-bound launches
+        # cannot reach 100 %), the roofline fraction the floor over the
+        # measured GEMM time
+        "mfma_util_gemm_ceiling_pct": round(100 * gemm_t_mfma / gemm_floor, 2),
+        "gemm_roofline_frac": round(gemm_floor / (gemm_ms * 1e-3), 4),
+        "gemm_algorithmic_bytes_per_step": int(gemm_bytes_total),
         "per_kernel": per_kernel,
         "roofline": {
             "kernel": "gemm_mfma_kernel<EPI_SWIGLU> (gate/up projection + SwiGLU)",
