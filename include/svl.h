@@ -358,10 +358,11 @@ svl_status svl_budget_loss(const svl_config *cfg, const svl_budget_loss_params *
  * With fp16 activations (SVL_COMPUTE_F16) a value outside fp16's range
  * becomes inf when it is converted, and the inf (or the NaN it produces)
  * reaches the output rows; the call itself still returns SVL_OK.  At its
- * end every svl_prefill and svl_prefill_cache clears a status word in the
- * last four bytes of its workspace buffer (ws + (ws_bytes & ~3) - 4) and
- * sets it to SVL_STATUS_NONFINITE if any of its output values (resid rows
- * 0 .. sum S_b - 1) is inf or NaN, whatever the cause (fp16 overflow, or
+ * end every svl_prefill, svl_prefill_cache and svl_prefill_controlled clears
+ * a status word in the last four bytes of its workspace buffer
+ * (ws + (ws_bytes & ~3) - 4) and sets it to SVL_STATUS_NONFINITE if any of
+ * its output values (resid rows 0 .. sum S_b - 1, S_b the final lengths) is
+ * inf or NaN, whatever the cause (fp16 overflow, or
  * non-finite inputs or weights).  svl_workspace_status copies that word to
  * *status (host) once `stream` has reached it: it synchronises the stream.
  * After other calls on the same buffer the word is undefined.

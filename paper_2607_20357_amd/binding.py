@@ -342,7 +342,8 @@ SVL_STATUS_NONFINITE = 1
 
 
 def svl_workspace_status(ws: torch.Tensor, stream=None) -> int:
-    """Status word of the last svl_prefill / svl_prefill_cache on `ws`
+    """Status word of the last svl_prefill / svl_prefill_cache /
+    svl_prefill_controlled on `ws`
     (SVL_STATUS_NONFINITE: an output value was inf or NaN); synchronises the
     stream."""
     out = ctypes.c_uint32(0)

@@ -957,6 +957,7 @@ static CtrlLayout ctrl_layout(const svl_config& c, const svl_controller& k, int3
   L.htil = take(4LL * B * D);
   L.glog = take(4LL * B * nl);
   L.rcopy = take(4LL * Rmax * D);
+  take(256);   // the last bytes of the buffer hold the call's status word (svl_workspace_status)
   L.total = off;
   return L;
 }
@@ -1196,6 +1197,12 @@ svl_status svl_prefill_controlled(const svl_config* cfg, const svl_layer_weights
     e = ex2.layer(t_plan.layers[l - P], layers[l], l);
   if (e == hipSuccess) e = ex2.norm(t_plan.final_norm, nullptr);
   if (e != hipSuccess) return hip_fail(e, "layer launch");
+  // the status word: cleared, then set if an output value is inf or NaN
+  uint32_t* status = status_word(ws, ws_bytes);
+  if ((e = launch_fill_i32(reinterpret_cast<int32_t*>(status), 0, 1, st)) != hipSuccess)
+    return hip_fail(e, "status clear");
+  if ((e = launch_nonfinite(resid, (int64_t)R2 * D, status, st)) != hipSuccess)
+    return hip_fail(e, "status scan");
 
   cu_seqlens[0] = 0;
   for (int32_t b = 0; b < B; ++b) {

@@ -44,6 +44,8 @@ def _run(w, seed, prefix, units, budget, shift, pe_dim=64, hidden=128, vocab=0):
     out = svl.svl_prefill_controlled(cfg, svl.LayerTable(layers), ctrl, logits, inp.vision,
                                      inp.text, budget, vocab, kept, resid, ws)
     torch.cuda.synchronize()
+    # finite inputs and weights: the call's status word is clear
+    assert svl.svl_workspace_status(ws) == 0
 
     ref = oc.prefill_controlled(shape, lambda l: host_layer(layers[l]), host_controller(draw), z,
                                 W.as_f32(inp.vision), W.as_f32(inp.text), budget, vocab)
