@@ -162,7 +162,10 @@ __global__ __launch_bounds__(TNT) void train_norm_bwd_kernel(const float* X, con
 // 4-byte read per lane (K % 16 == 0: a last half step reads as zero); the
 // next step's operands are in registers while the current one multiplies.  With ASC, A[m][k] is scaled by
 // ascale[(m / S) astride + k / kg] (the unit masks).
-constexpr int GBM = 64, GBN = 64, GBK = 32, GLD = 80;   // LDS row stride (floats)
+// LDS row stride (floats): measured over 68-96 on the headline-shape training
+// step, 68 and 76 take 313 ms per step against 331 ms for 80 and 72 (fewer
+// bank conflicts on the transposed stores and the fragment reads)
+constexpr int GBM = 64, GBN = 64, GBK = 32, GLD = 68;
 
 template <int BL, class TB, bool ASC>
 __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
