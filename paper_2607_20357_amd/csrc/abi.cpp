@@ -318,11 +318,13 @@ struct Exec {
       a.ldo = A * d;
       a.rope = reinterpret_cast<const float2*>(ws + L.rope);
       a.scale = 1.0f / std::sqrt((float)d);
+      // active K/V heads per group: the cache append and the grouped-K/V
+      // prefill attention read them
+      a.kvhead_table = at<int32_t>(P.attn.kvheads_off);
+      a.max_kv_cnt = P.attn.max_kv_cnt;
       if (cache) {
         a.cache = cache + (size_t)l * batch * KV * 2 * (size_t)max_len * d * 2;
         a.max_len = max_len;
-        a.kvhead_table = at<int32_t>(P.attn.kvheads_off);
-        a.max_kv_cnt = P.attn.max_kv_cnt;
         // prefill: this call's K / V rows into the cache (decode attention
         // appends its one row itself)
         if (!decode) {

@@ -234,6 +234,28 @@ static void check_prefill(const Case& c) {
             }
       }
     }
+    // ---- attention tiles: each group's query tiles times its active query
+    // heads, numbered consecutively; the group covers its sample's rows
+    if (LP.attn.ntiles > 0) {
+      const AttnGroup* ag = at<AttnGroup>(plan, LP.attn.groups_off);
+      const int32_t* heads = at<int32_t>(plan, LP.attn.heads_off);
+      const int bq = LP.attn.bq;
+      CHECK(bq == ATTN_BQ || bq == ATTN_BQ_SHORT, "layer %d attention bq %d", l, bq);
+      int tiles = 0;
+      for (int gi = 0; gi < LP.attn.ngroups; ++gi) {
+        const AttnGroup& g = ag[gi];
+        CHECK(g.tile0 == tiles, "layer %d attention group %d tile0 %d != %d", l, gi, g.tile0, tiles);
+        CHECK(g.sample >= 0 && g.sample < B && g.S == c.seq[g.sample] && g.row0 == pcu[g.sample],
+              "layer %d attention group %d rows", l, gi);
+        CHECK(g.nqt == (g.S + bq - 1) / bq, "layer %d attention group %d nqt %d", l, gi, g.nqt);
+        CHECK(g.h_cnt >= 1 && g.kv_cnt >= 1, "layer %d attention group %d empty", l, gi);
+        for (int i = 0; i < g.h_cnt; ++i)
+          CHECK(m.head_mask[g.sample * A + heads[g.h_off + i]] != 0,
+                "layer %d group %d lists inactive head %d", l, gi, heads[g.h_off + i]);
+        tiles += g.nqt * g.h_cnt;
+      }
+      CHECK(tiles == LP.attn.ntiles, "layer %d attention tiles %d != %d", l, LP.attn.ntiles, tiles);
+    }
   }
 }
 
