@@ -44,6 +44,8 @@ def _decode_case(w, seed, steps, extra=3):
     cu = svl.svl_prefill_cache(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
                                inp.head_mask, inp.ffn_mask, kept, resid, cache, max_len, ws)
     torch.cuda.synchronize()
+    # finite inputs and weights: the call's status word is clear
+    assert svl.svl_workspace_status(ws) == 0
     # the cache writes leave the prefill itself unchanged
     _, cu2, plain, _ = gpu_prefill(w, inp, layers, table=table)
     np.testing.assert_array_equal(cu, cu2)
