@@ -338,12 +338,19 @@ struct FwdSmem {
 
 template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
-  constexpr int CPT = HD / 16;   // output columns per thread
+  // 64 queries x 64 keys per tile on v_mfma_f32_16x16x4_f32: wave w owns
+  // queries 16 w .. 16 w + 15 against the tile's 64 keys (four 16 x 16
+  // score blocks, A = Q from Q^T in LDS, B = K^T), then O += P V with P
+  // passed through the wave's own columns of P^T in LDS (A operand) and V
+  // rows (B operand).  Lane l holds rows 4 (l / 16) + r, r < 4, of every
+  // block, so a row's statistics stay in the 16 lanes that share l / 16.
+  constexpr int NBO = HD / 16;   // 16-column blocks of the output
   constexpr int C4 = HD / 4;
   __shared__ __attribute__((aligned(16))) FwdSmem<HD> sm;
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int rep = a.A / a.KV, g = h / rep;
-  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
   const int64_t base = (int64_t)b * a.S;
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
   const int64_t q0 = (int64_t)qt * 64;
@@ -357,107 +364,117 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
     sm.qt[c + 2][r] = v.z;
     sm.qt[c + 3][r] = v.w;
   }
-  float mrow[4], lrow[4], o[4][CPT];
+  float mrow[4], lrow[4];
+  floatx4 o[NBO];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    mrow[i] = -INFINITY;
-    lrow[i] = 0.0f;
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) o[i][c] = 0.0f;
+  for (int r = 0; r < 4; ++r) {
+    mrow[r] = -INFINITY;
+    lrow[r] = 0.0f;
   }
+#pragma unroll
+  for (int n = 0; n < NBO; ++n) o[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int qw = 16 * wave;   // the wave's first query of the tile
+  // K / V of a key tile: thread pieces idx = t + TNT e (row idx / C4, 4
+  // columns from (idx % C4) * 4), loaded into registers one tile ahead
+  constexpr int KE = 64 * C4 / TNT;
+  static_assert(64 * C4 % TNT == 0, "whole pieces per thread");
+  float4 kreg[KE], vreg[KE];
+  auto load_kv = [&](int64_t k0) {
+#pragma unroll
+    for (int e = 0; e < KE; ++e) {
+      const int idx = t + TNT * e, r = idx / C4, c = (idx % C4) * 4;
+      kreg[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      vreg[e] = kreg[e];
+      if (k0 + r < a.S) {
+        const int64_t off = (base + k0 + r) * ldk + (int64_t)g * HD + c;
+        kreg[e] = *reinterpret_cast<const float4*>(a.K + off);
+        vreg[e] = *reinterpret_cast<const float4*>(a.V + off);
+      }
+    }
+  };
+  load_kv(0);
   for (int kt = 0; kt <= qt; ++kt) {
     const int64_t k0 = (int64_t)kt * 64;
     __syncthreads();   // the previous tile's readers are done
-    for (int idx = t; idx < 64 * C4; idx += TNT) {
-      const int r = idx / C4, c = (idx % C4) * 4;
-      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
-      if (k0 + r < a.S) {
-        const int64_t off = (base + k0 + r) * ldk + (int64_t)g * HD + c;
-        kv = *reinterpret_cast<const float4*>(a.K + off);
-        vv = *reinterpret_cast<const float4*>(a.V + off);
-      }
-      sm.kt[c + 0][r] = kv.x;
-      sm.kt[c + 1][r] = kv.y;
-      sm.kt[c + 2][r] = kv.z;
-      sm.kt[c + 3][r] = kv.w;
-      *reinterpret_cast<float4*>(&sm.v[r][c]) = vv;
+#pragma unroll
+    for (int e = 0; e < KE; ++e) {
+      const int idx = t + TNT * e, r = idx / C4, c = (idx % C4) * 4;
+      sm.kt[c + 0][r] = kreg[e].x;
+      sm.kt[c + 1][r] = kreg[e].y;
+      sm.kt[c + 2][r] = kreg[e].z;
+      sm.kt[c + 3][r] = kreg[e].w;
+      *reinterpret_cast<float4*>(&sm.v[r][c]) = vreg[e];
     }
     __syncthreads();
-    float s[4][4];
+    if (kt < qt) load_kv(k0 + 64);
+    floatx4 sc[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) s[i][j] = 0.0f;
+    for (int j = 0; j < 4; ++j) sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-    for (int d = 0; d < HD; ++d) {
-      const float4 x = *reinterpret_cast<const float4*>(&sm.qt[d][ty * 4]);
-      const float4 y = *reinterpret_cast<const float4*>(&sm.kt[d][tx * 4]);
-      const float xa[4] = {x.x, x.y, x.z, x.w}, ya[4] = {y.x, y.y, y.z, y.w};
+    for (int d = 0; d < HD; d += 4) {
+      const float qa = sm.qt[d + lg][qw + lr];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s[i][j] += xa[i] * ya[j];
+      for (int j = 0; j < 4; ++j)
+        sc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, sm.kt[d + lg][16 * j + lr], sc[j], 0, 0, 0);
     }
+    // sc[j][r] = score of query qw + 4 lg + r and key 16 j + lr of the tile
     float corr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t qi = q0 + ty * 4 + i;
+    for (int r = 0; r < 4; ++r) {
+      const int64_t qi = q0 + qw + 4 * lg + r;
       float mx = -INFINITY;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int64_t kj = k0 + tx * 4 + j;
-        if (kj > qi || kj >= a.S) s[i][j] = -INFINITY;
-        mx = fmaxf(mx, s[i][j]);
+        const int64_t kj = k0 + 16 * j + lr;
+        if (kj > qi || kj >= a.S) sc[j][r] = -INFINITY;
+        mx = fmaxf(mx, sc[j][r]);
       }
 #pragma unroll
       for (int o2 = 1; o2 < 16; o2 <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
-      const float mn = fmaxf(mrow[i], mx);
+      const float mn = fmaxf(mrow[r], mx);
       // a row with no valid key so far keeps max -inf: its probabilities are 0
       const float mref = mn == -INFINITY ? 0.0f : mn;
-      corr[i] = expf(mrow[i] - mref);
+      corr[r] = expf(mrow[r] - mref);
       float rs = 0.0f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p = expf(s[i][j] - mref);
-        s[i][j] = p;
+        const float p = expf(sc[j][r] - mref);
+        sc[j][r] = p;
         rs += p;
       }
 #pragma unroll
       for (int o2 = 1; o2 < 16; o2 <<= 1) rs += __shfl_xor(rs, o2, 64);
-      lrow[i] = lrow[i] * corr[i] + rs;
-      mrow[i] = mn;
+      lrow[r] = lrow[r] * corr[r] + rs;
+      mrow[r] = mn;
     }
+    // P^T: pt[key][query], the wave's own 16 query columns
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(&sm.pt[16 * j + lr][qw + 4 * lg]) =
+          make_float4(sc[j][0], sc[j][1], sc[j][2], sc[j][3]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.pt[tx * 4 + j][ty * 4 + i] = s[i][j];
-    __syncthreads();
+    for (int n = 0; n < NBO; ++n)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) o[i][c] *= corr[i];
+      for (int r = 0; r < 4; ++r) o[n][r] *= corr[r];
+    // O += P V (the P^T writes above are the wave's own; LDS keeps a wave's order)
 #pragma unroll 4
-    for (int k = 0; k < 64; ++k) {
-      const float4 pv = *reinterpret_cast<const float4*>(&sm.pt[k][ty * 4]);
-      const float pa[4] = {pv.x, pv.y, pv.z, pv.w};
-      float vv[CPT];
+    for (int k = 0; k < 64; k += 4) {
+      const float pa = sm.pt[k + lg][qw + lr];
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) vv[c] = sm.v[k][tx * CPT + c];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) o[i][c] += pa[i] * vv[c];
+      for (int n = 0; n < NBO; ++n)
+        o[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, sm.v[k + lg][16 * n + lr], o[n], 0, 0, 0);
     }
   }
+  // o[n][r] = O of query qw + 4 lg + r, column 16 n + lr
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t qi = q0 + ty * 4 + i;
+  for (int r = 0; r < 4; ++r) {
+    const int64_t qi = q0 + qw + 4 * lg + r;
     if (qi >= a.S) continue;
-    const float inv = 1.0f / lrow[i];
+    const float inv = 1.0f / lrow[r];
 #pragma unroll
-    for (int c = 0; c < CPT; ++c)
-      a.out[(base + qi) * ldq + (int64_t)h * HD + tx * CPT + c] = o[i][c] * inv;
-    if (tx == 0) a.lse[(base + qi) * a.A + h] = mrow[i] + logf(lrow[i]);
+    for (int n = 0; n < NBO; ++n)
+      a.out[(base + qi) * ldq + (int64_t)h * HD + 16 * n + lr] = o[n][r] * inv;
+    if (lr == 0) a.lse[(base + qi) * a.A + h] = mrow[r] + logf(lrow[r]);
   }
 }
 
