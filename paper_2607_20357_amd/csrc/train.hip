@@ -553,68 +553,93 @@ struct DqSmem {
 
 template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
-  constexpr int CPT = HD / 16;
+  // v_mfma_f32_16x16x4_f32: wave w owns queries 16 w .. 16 w + 15 of the
+  // tile; S = (Q scale) K^T and dP = dO V^T as four 16 x 16 blocks each (A
+  // from the transposed query tiles, B from K^T / V^T), dS = P (dP - D)
+  // through the wave's own columns of ds[key][query] into dQ += dS K.  Lane
+  // l holds rows 4 (l / 16) + r, r < 4, of every block.
+  constexpr int NBO = HD / 16;
+  constexpr int CPT = HD / 16;   // columns per lane of the D reduction
   __shared__ __attribute__((aligned(16))) DqSmem<HD> sm;
   const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int rep = a.A / a.KV, g = h / rep;
-  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
   const int64_t base = (int64_t)b * a.S;
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
   const int64_t q0 = (int64_t)qt * 64;
+  const int qw = 16 * wave;
   load_t<HD>(sm.qt, a.Q, base + q0, ldq, (int64_t)h * HD, a.S - q0, a.scale);
   load_t<HD>(sm.dot, a.dO, base + q0, ldq, (int64_t)h * HD, a.S - q0, 1.0f);
-  // D and lse of this thread's four rows (D over the thread's columns, then the row)
+  // D = dO . O and lse of the lane's four rows (each of the 16 lanes of a
+  // row sums HD / 16 of its columns)
   float Dr[4], lse[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t qi = q0 + ty * 4 + i;
+  for (int r = 0; r < 4; ++r) {
+    const int64_t qi = q0 + qw + 4 * lg + r;
     float d = 0.0f;
     if (qi < a.S) {
-      const int64_t off = (base + qi) * ldq + (int64_t)h * HD + tx * CPT;
+      const int64_t off = (base + qi) * ldq + (int64_t)h * HD + lr * CPT;
 #pragma unroll
       for (int c = 0; c < CPT; ++c) d += a.dO[off + c] * a.O[off + c];
     }
 #pragma unroll
     for (int o2 = 1; o2 < 16; o2 <<= 1) d += __shfl_xor(d, o2, 64);
-    Dr[i] = d;
-    lse[i] = qi < a.S ? a.lse[(base + qi) * a.A + h] : 0.0f;
-    if (tx == 0 && qi < a.S) a.Dv[(base + qi) * a.A + h] = d;
+    Dr[r] = d;
+    lse[r] = qi < a.S ? a.lse[(base + qi) * a.A + h] : 0.0f;
+    if (lr == 0 && qi < a.S) a.Dv[(base + qi) * a.A + h] = d;
   }
-  float acc[4][CPT];
+  floatx4 acc[NBO];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) acc[i][c] = 0.0f;
+  for (int n = 0; n < NBO; ++n) acc[n] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int kt = 0; kt <= qt; ++kt) {
     const int64_t k0 = (int64_t)kt * 64;
     __syncthreads();
     load_t<HD>(sm.kt, a.K, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
     load_t<HD>(sm.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
     __syncthreads();
-    float s[4][4], dp[4][4];
-    tile_dot<HD>(sm.qt, sm.kt, ty, tx, s);
-    tile_dot<HD>(sm.dot, sm.vt, ty, tx, dp);
+    floatx4 sc[4], dp[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t qi = q0 + ty * 4 + i;
+    for (int jb = 0; jb < 4; ++jb) sc[jb] = dp[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int d = 0; d < HD; d += 4) {
+      const float qa = sm.qt[d + lg][qw + lr], da = sm.dot[d + lg][qw + lr];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t kj = k0 + tx * 4 + j;
-        const float p = (kj <= qi && kj < a.S && qi < a.S) ? expf(s[i][j] - lse[i]) : 0.0f;
-        sm.ds[tx * 4 + j][ty * 4 + i] = p * (dp[i][j] - Dr[i]);
+      for (int jb = 0; jb < 4; ++jb) {
+        sc[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, sm.kt[d + lg][16 * jb + lr], sc[jb], 0, 0, 0);
+        dp[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(da, sm.vt[d + lg][16 * jb + lr], dp[jb], 0, 0, 0);
       }
     }
-    __syncthreads();
-    // dQ[q][d] += sum_k dS[q][k] K[k][d]: rows of ds are keys, K^T is kt
-    tile_acc<HD>(sm.ds, sm.kt, ty, tx, acc);
+    // dS of query qw + 4 lg + r and key 16 jb + lr, into ds[key][query]
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+      float4 w;
+      float* wv = reinterpret_cast<float*>(&w);
+      const int64_t kj = k0 + 16 * jb + lr;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t qi = q0 + qw + 4 * lg + r;
+        const float p = (kj <= qi && kj < a.S && qi < a.S) ? expf(sc[jb][r] - lse[r]) : 0.0f;
+        wv[r] = p * (dp[jb][r] - Dr[r]);
+      }
+      *reinterpret_cast<float4*>(&sm.ds[16 * jb + lr][qw + 4 * lg]) = w;
+    }
+    // dQ[q][d] += sum_k dS[q][k] K[k][d] (the ds writes above are the wave's own)
+#pragma unroll 4
+    for (int k = 0; k < 64; k += 4) {
+      const float pa = sm.ds[k + lg][qw + lr];
+#pragma unroll
+      for (int n = 0; n < NBO; ++n)
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, sm.kt[16 * n + lr][k + lg], acc[n], 0, 0, 0);
+    }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t qi = q0 + ty * 4 + i;
+  for (int r = 0; r < 4; ++r) {
+    const int64_t qi = q0 + qw + 4 * lg + r;
     if (qi >= a.S) continue;
 #pragma unroll
-    for (int c = 0; c < CPT; ++c)
-      a.out[(base + qi) * ldq + (int64_t)h * HD + tx * CPT + c] = acc[i][c] * a.scale;
+    for (int n = 0; n < NBO; ++n)
+      a.out[(base + qi) * ldq + (int64_t)h * HD + 16 * n + lr] = acc[n][r] * a.scale;
   }
 }
 
@@ -636,21 +661,25 @@ struct DkvSmem {
 
 template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_dkv_kernel(TAttnArgs a) {
-  constexpr int CPT = HD / 16;
+  // v_mfma_f32_16x16x4_f32: wave w owns keys 16 w .. 16 w + 15 of the tile;
+  // S^T = K (Q scale)^T and dP^T = V dO^T as four 16 x 16 blocks each, P^T
+  // and then dS^T through the wave's own columns of w[query][key] into
+  // dV += P^T dO and dK += dS^T (Q scale).
+  constexpr int NBO = HD / 16;
   __shared__ __attribute__((aligned(16))) DkvSmem<HD> sm;
   const int kt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int rep = a.A / a.KV;
-  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
   const int64_t base = (int64_t)b * a.S;
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
   const int64_t k0 = (int64_t)kt * 64;
+  const int kw = 16 * wave;
   load_t<HD>(sm.kt, a.K, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
   load_t<HD>(sm.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
-  float gk[4][CPT], gv[4][CPT];
+  floatx4 gk[NBO], gv[NBO];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) gk[i][c] = gv[i][c] = 0.0f;
+  for (int n = 0; n < NBO; ++n) gk[n] = gv[n] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int nqt = (int)((a.S + 63) / 64);
   for (int h = g * rep; h < (g + 1) * rep; ++h) {
     for (int qt = kt; qt < nqt; ++qt) {
@@ -664,44 +693,72 @@ __global__ __launch_bounds__(TNT) void train_attn_dkv_kernel(TAttnArgs a) {
         sm.dv[t] = in ? a.Dv[(base + q0 + t) * a.A + h] : 0.0f;
       }
       __syncthreads();
-      float s[4][4], dp[4][4];
-      tile_dot<HD>(sm.kt, sm.qt, ty, tx, s);     // [key ty*4+i][query tx*4+j]
-      tile_dot<HD>(sm.vt, sm.dot, ty, tx, dp);
-      float p[4][4];
+      floatx4 st[4], dpt[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t ki = k0 + ty * 4 + i;
+      for (int jb = 0; jb < 4; ++jb) st[jb] = dpt[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+      for (int d = 0; d < HD; d += 4) {
+        const float ka = sm.kt[d + lg][kw + lr], va = sm.vt[d + lg][kw + lr];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int qj = tx * 4 + j;
-          const int64_t q = q0 + qj;
-          p[i][j] = (q >= ki && q < a.S && ki < a.S) ? expf(s[i][j] - sm.lse[qj]) : 0.0f;
-          sm.w[qj][ty * 4 + i] = p[i][j];
+        for (int jb = 0; jb < 4; ++jb) {
+          st[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, sm.qt[d + lg][16 * jb + lr], st[jb], 0, 0, 0);
+          dpt[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, sm.dot[d + lg][16 * jb + lr], dpt[jb], 0, 0, 0);
         }
       }
-      __syncthreads();
-      tile_acc<HD>(sm.w, sm.dot, ty, tx, gv);    // dV[k][d] += sum_q P[q][k] dO[q][d]
-      __syncthreads();
+      // P^T of key kw + 4 lg + r and query 16 jb + lr, into w[query][key]
+      float4 pw[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int jb = 0; jb < 4; ++jb) {
+        const int qj = 16 * jb + lr;
+        const int64_t q = q0 + qj;
+        const float lq = sm.lse[qj];
+        float* pv = reinterpret_cast<float*>(&pw[jb]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int qj = tx * 4 + j;
-          sm.w[qj][ty * 4 + i] = p[i][j] * (dp[i][j] - sm.dv[qj]);
+        for (int r = 0; r < 4; ++r) {
+          const int64_t ki = k0 + kw + 4 * lg + r;
+          pv[r] = (q >= ki && q < a.S && ki < a.S) ? expf(st[jb][r] - lq) : 0.0f;
         }
-      __syncthreads();
-      tile_acc<HD>(sm.w, sm.qt, ty, tx, gk);     // dK[k][d] += sum_q dS[q][k] (Q scale)[q][d]
+        *reinterpret_cast<float4*>(&sm.w[qj][kw + 4 * lg]) = pw[jb];
+      }
+      // dV[k][c] += sum_q P^T[k][q] dO[q][c]
+#pragma unroll 4
+      for (int qq = 0; qq < 64; qq += 4) {
+        const float pa = sm.w[qq + lg][kw + lr];
+#pragma unroll
+        for (int n = 0; n < NBO; ++n)
+          gv[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, sm.dot[16 * n + lr][qq + lg], gv[n], 0, 0, 0);
+      }
+      // dS^T = P^T (dP^T - D) over the same columns (after this wave's reads above)
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const int qj = 16 * jb + lr;
+        const float dq = sm.dv[qj];
+        const float* pv = reinterpret_cast<const float*>(&pw[jb]);
+        float4 w;
+        float* wv = reinterpret_cast<float*>(&w);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) wv[r] = pv[r] * (dpt[jb][r] - dq);
+        *reinterpret_cast<float4*>(&sm.w[qj][kw + 4 * lg]) = w;
+      }
+      // dK[k][c] += sum_q dS^T[k][q] (Q scale)[q][c]
+#pragma unroll 4
+      for (int qq = 0; qq < 64; qq += 4) {
+        const float sa = sm.w[qq + lg][kw + lr];
+#pragma unroll
+        for (int n = 0; n < NBO; ++n)
+          gk[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(sa, sm.qt[16 * n + lr][qq + lg], gk[n], 0, 0, 0);
+      }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t ki = k0 + ty * 4 + i;
+  for (int r = 0; r < 4; ++r) {
+    const int64_t ki = k0 + kw + 4 * lg + r;
     if (ki >= a.S) continue;
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int64_t off = (base + ki) * ldk + (int64_t)g * HD + tx * CPT + c;
-      a.dK[off] = gk[i][c];
-      a.dV[off] = gv[i][c];
+    for (int n = 0; n < NBO; ++n) {
+      const int64_t off = (base + ki) * ldk + (int64_t)g * HD + 16 * n + lr;
+      a.dK[off] = gk[n][r];
+      a.dV[off] = gv[n][r];
     }
   }
 }
