@@ -824,18 +824,23 @@ __global__ __launch_bounds__(TNT) void train_attn_mask_bwd_kernel(float* dOm, co
   }
 }
 
-// dM[b][l][u] = sum over the sample's rows of both partial sums (float64, row order).
-__global__ void train_mask_reduce_kernel(const float* pa, const float* pf, int32_t B, int32_t S,
-                                         int32_t U, int32_t L, int32_t l, float* dM) {
-  const int q = blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= B * U) return;
-  const int b = q / U, u = q % U;
+// dM[b][l][u] = sum over the sample's rows of both partial sums, in float64: one
+// workgroup per (b, u), each thread a stride of rows, then a fixed-order tree.
+__global__ __launch_bounds__(TNT) void train_mask_reduce_kernel(const float* pa, const float* pf,
+                                                                int32_t S, int32_t U, int32_t L,
+                                                                int32_t l, float* dM) {
+  __shared__ double red[TNT / 64];
+  const int b = blockIdx.x / U, u = blockIdx.x % U;
   double s = 0.0;
-  for (int64_t i = 0; i < S; ++i) {
+  for (int64_t i = threadIdx.x; i < S; i += TNT) {
     const int64_t r = ((int64_t)b * S + i) * U + u;
     s += (double)pa[r] + (double)pf[r];
   }
-  dM[((int64_t)b * L + l) * U + u] = (float)s;
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    dM[((int64_t)b * L + l) * U + u] = (float)((red[0] + red[1]) + (red[2] + red[3]));
 }
 
 // dL/dz_i = (dX0_i . v_i) y (1 - y) / tau_tok, one workgroup per vision token.
@@ -989,7 +994,7 @@ hipError_t launch_train_attn_mask_bwd(float* dOm, const float* O, const float* m
 hipError_t launch_train_mask_reduce(const float* pa, const float* pf, int32_t B, int32_t S,
                                     int32_t U, int32_t L, int32_t l, float* dM, hipStream_t st) {
   if (B * U <= 0) return hipSuccess;
-  train_mask_reduce_kernel<<<blocks((int64_t)B * U), TNT, 0, st>>>(pa, pf, B, S, U, L, l, dM);
+  train_mask_reduce_kernel<<<(unsigned)(B * U), TNT, 0, st>>>(pa, pf, S, U, L, l, dM);
   return hipGetLastError();
 }
 
