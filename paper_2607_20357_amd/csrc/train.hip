@@ -295,39 +295,12 @@ __global__ void train_rope_kernel(float* X, int64_t ld, int32_t nheads, int32_t 
 
 // ------------------------------------------------------------------ attention
 // One workgroup: 64 rows (queries, or keys for the K/V gradient) of one head
-// of one sample; four threads per row, each holding a quarter of the head's
-// dimensions; the other operand's rows stream through LDS 64 at a time.
-template <int HD>
-struct AttnTile {
-  float a[64][HD];
-  float b[64][HD];
-  float s0[64], s1[64];
-};
+// of one sample, four waves of 16 rows each on fp32 MFMA; the other
+// operand's rows go through LDS 64 at a time.
 
-template <int HD>
-__device__ __forceinline__ void load_rows(float (*dst)[HD], const float* src, int64_t row0,
-                                          int64_t ld, int64_t col0, int64_t rows_left) {
-  constexpr int C4 = HD / 4;
-  for (int q = threadIdx.x; q < 64 * C4; q += TNT) {
-    const int r = q / C4, c = (q % C4) * 4;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < rows_left) v = *reinterpret_cast<const float4*>(src + (row0 + r) * ld + col0 + c);
-    *reinterpret_cast<float4*>(&dst[r][c]) = v;
-  }
-}
-
-__device__ __forceinline__ float quad_sum(float v) {
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  return v;
-}
-
-// Forward: one workgroup = 64 query rows of one head.  The 64 x 64 score
-// block of each key tile is a register-tiled product (4 x 4 scores per
-// thread) of Q^T and K^T held in LDS; the probabilities go through LDS
-// (transposed) into the P V product (4 rows x HD/16 columns per thread).
-// The online softmax keeps each row's running max and sum in the 16
-// threads that share the row.
+// Forward: one workgroup = 64 query rows of one head against the key tiles
+// up to its own, with an online softmax; writes O and the log-sum-exp of
+// every row for the backward.
 template <int HD>
 struct FwdSmem {
   float qt[HD][68];     // Q^T of the query tile, scaled by 1/sqrt(d)
@@ -496,52 +469,10 @@ __device__ __forceinline__ void load_t(float (*dst)[68], const float* src, int64
   }
 }
 
-// 4 x 4 block of sum_d A^T[d][4 ty + i] B^T[d][4 tx + j] over both operands'
-// transposed tiles in LDS.
-template <int HD>
-__device__ __forceinline__ void tile_dot(const float (*at)[68], const float (*bt)[68], int ty,
-                                         int tx, float (&acc)[4][4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
-#pragma unroll 8
-  for (int d = 0; d < HD; ++d) {
-    const float4 x = *reinterpret_cast<const float4*>(&at[d][ty * 4]);
-    const float4 y = *reinterpret_cast<const float4*>(&bt[d][tx * 4]);
-    const float xa[4] = {x.x, x.y, x.z, x.w}, ya[4] = {y.x, y.y, y.z, y.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] += xa[i] * ya[j];
-  }
-}
-
-// acc[i][c] += sum_r w[r][4 ty + i] m^T[tx CPT + c][r] over the 64 rows r of
-// a 64 x 64 weight block w (LDS, [r][68]) and a transposed operand m^T (LDS).
-template <int HD>
-__device__ __forceinline__ void tile_acc(const float (*w)[68], const float (*mt)[68], int ty,
-                                         int tx, float (&acc)[4][HD / 16]) {
-  constexpr int CPT = HD / 16;
-#pragma unroll 4
-  for (int r = 0; r < 64; ++r) {
-    const float4 wv = *reinterpret_cast<const float4*>(&w[r][ty * 4]);
-    const float wa[4] = {wv.x, wv.y, wv.z, wv.w};
-    float mv[CPT];
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) mv[c] = mt[tx * CPT + c][r];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) acc[i][c] += wa[i] * mv[c];
-  }
-}
-
 // Query gradient: one workgroup = 64 query rows of one head.  Per key tile
-// the score block S = (Q scale) K^T and dP = dO V^T are register-tiled
-// products of transposed tiles in LDS; dS = P (dP - D) with P = exp(S - lse)
-// goes through LDS into dQ += dS K (scaled at the end).  D = dO . O per row
-// is formed first and stored for the key / value gradient.
+// S = (Q scale) K^T and dP = dO V^T, dS = P (dP - D) with P = exp(S - lse),
+// then dQ += dS K (scaled at the end).  D = dO . O per row is formed first
+// and stored for the key / value gradient.
 template <int HD>
 struct DqSmem {
   float qt[HD][68];
@@ -645,8 +576,7 @@ __global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
 
 // Key / value gradient: one workgroup = 64 key rows of one K/V head; for
 // each query head of the group and each query tile at or after the key
-// tile: S^T = K (Q scale)^T and dP^T = V dO^T (register-tiled, transposed
-// tiles in LDS), P^T = exp(S^T - lse), then dV += P^T dO and, through the
+// tile: S^T = K (Q scale)^T and dP^T = V dO^T, P^T = exp(S^T - lse), then dV += P^T dO and, through the
 // same LDS block, dK += dS^T (Q scale) with dS^T = P^T (dP^T - D) (the
 // scaled query tile carries the 1/sqrt(d) of dK).
 template <int HD>

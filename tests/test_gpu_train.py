@@ -14,6 +14,8 @@ eps^(-1/2): they differ from the kept tokens' by orders, and a normwise
 measure over all tokens would see only them.)
 
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -135,6 +137,15 @@ def test_train_scaled_gqa_bf16():
                  n_kv_heads=2, d_ffn=1024, batch=2, n_vision=160, n_text=48,
                  name="gqa7b_train_scaled")
     _run(w, 7, 0, 4)
+
+
+def test_train_head_dim_32_gqa():
+    """32-dimensional heads (8 query heads over 4 K/V heads, two per group)
+    and 130 rows, three 64-row tiles with a ragged last one."""
+    base = _tiny()
+    shape = dataclasses.replace(base.shape, n_heads=8, n_kv_heads=4, head_dim=32)
+    w = dataclasses.replace(base, shape=shape, n_vision=100, n_text=30, name="tiny_hd32_train")
+    _run(w, 9, 1, 4)
 
 
 def test_train_headline_width():
