@@ -186,13 +186,18 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   else { bk = t >> 4; bn = (t & 15) * 4; }
   const bool bok = n0 + bn < a.N;
   const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  // the row's unit masks (its sample's), found once; a k's unit is a 32-bit
+  // quotient (K < 2^31), the four k of a piece share it (kg % 4 == 0)
+  const float* srow = nullptr;
+  if constexpr (ASC) srow = a.ascale + (aok ? (arow / a.S) * a.astride : 0);
   auto load_a = [&](int64_t k0, float4 (&v)[2]) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       v[h2] = zero;
       if (aok && k0 + 16 * h2 < a.K) {   // K % 32 == 16: the second half of the last step is 0
         v[h2] = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + 16 * h2 + ak);
-        if constexpr (ASC) v[h2] = f4scale(v[h2], a.ascale[(arow / a.S) * a.astride + (k0 + 16 * h2 + ak) / a.kg]);
+        if constexpr (ASC)
+          v[h2] = f4scale(v[h2], srow[(uint32_t)(k0 + 16 * h2 + ak) / (uint32_t)a.kg]);
       }
     }
   };
