@@ -161,7 +161,8 @@ __global__ __launch_bounds__(TNT) void train_norm_bwd_kernel(const float* X, con
 // and out); K in steps of 32 staged through LDS k-major, so a fragment is one
 // 4-byte read per lane (K % 16 == 0: a last half step reads as zero); the
 // next step's operands are in registers while the current one multiplies.  With ASC, A[m][k] is scaled by
-// ascale[(m / S) astride + k / kg] (the unit masks).
+// ascale[(m / S) astride + k / kg] (the unit masks).  blockIdx.z is the K
+// piece: with more than one, each writes its own float32 slice (no R).
 // LDS row stride (floats): measured over 68-96 on the headline-shape training
 // step, 68 and 76 take 313 ms per step against 331 ms for 80 and 72 (fewer
 // bank conflicts on the transposed stores and the fragment reads)
@@ -175,6 +176,12 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   const int wy = wave >> 1, wx = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * GBM, n0 = (int64_t)blockIdx.x * GBN;
   const TB* B = static_cast<const TB*>(a.B);
+  const int64_t kb = (int64_t)blockIdx.z * a.kpiece;
+  const int64_t ke = kb + a.kpiece < a.K ? kb + a.kpiece : a.K;
+  const bool split = gridDim.z > 1;
+  float* C = split ? a.part + (int64_t)blockIdx.z * a.M * a.N : a.C;
+  const int64_t ldc = split ? a.N : a.ldc;
+  const float* R = split ? nullptr : a.R;
 
   // global -> register loads: A row ar, k ak..ak+3; B as [N][K] row bn, k bk..,
   // or as [K][N] row bk, n bn..
@@ -194,7 +201,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       v[h2] = zero;
-      if (aok && k0 + 16 * h2 < a.K) {   // K % 32 == 16: the second half of the last step is 0
+      if (aok && k0 + 16 * h2 < ke) {   // K % 32 == 16: the second half of the last step is 0
         v[h2] = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + 16 * h2 + ak);
         if constexpr (ASC)
           v[h2] = f4scale(v[h2], srow[(uint32_t)(k0 + 16 * h2 + ak) / (uint32_t)a.kg]);
@@ -205,7 +212,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       v[h2] = zero;
-      if (bok && k0 + 16 * h2 < a.K) {
+      if (bok && k0 + 16 * h2 < ke) {
         if constexpr (BL == 0) v[h2] = ld4(B, (n0 + bn) * a.ldb + k0 + 16 * h2 + bk);
         else v[h2] = ld4(B, (k0 + 16 * h2 + bk) * a.ldb + n0 + bn);
       }
@@ -221,9 +228,9 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   const int fr = lane & 15, fk = lane >> 4;
 
   float4 av[2], bv[2];
-  load_a(0, av);
-  load_b(0, bv);
-  for (int64_t k0 = 0; k0 < a.K; k0 += GBK) {
+  load_a(kb, av);
+  load_b(kb, bv);
+  for (int64_t k0 = kb; k0 < ke; k0 += GBK) {
     __syncthreads();   // the previous step's readers are done
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
@@ -242,7 +249,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
       }
     }
     __syncthreads();
-    if (k0 + GBK < a.K) {
+    if (k0 + GBK < ke) {
       load_a(k0 + GBK, av);
       load_b(k0 + GBK, bv);
     }
@@ -273,10 +280,29 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
         const int64_t row = m0 + 32 * wy + 16 * i + 4 * fk + r;
         if (row >= a.M) continue;
         float o = acc[i][j][r];
-        if (a.R) o += a.R[row * a.ldr + col];
-        a.C[row * a.ldc + col] = o;
+        if (R) o += R[row * a.ldr + col];
+        C[row * ldc + col] = o;
       }
   }
+}
+
+// C = R + the K pieces' slices added in piece order, four columns per thread.
+__global__ void train_splitk_reduce_kernel(const float* part, int32_t ns, int64_t M, int64_t N,
+                                           const float* R, int64_t ldr, float* C, int64_t ldc) {
+  const int64_t n4 = N / 4;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= M * n4) return;
+  const int64_t m = q / n4, c = (q % n4) * 4;
+  float4 s = *reinterpret_cast<const float4*>(part + m * N + c);
+  for (int z = 1; z < ns; ++z) {
+    const float4 p = *reinterpret_cast<const float4*>(part + (z * M + m) * N + c);
+    s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
+  }
+  if (R) {
+    const float4 r = *reinterpret_cast<const float4*>(R + m * ldr + c);
+    s.x = r.x + s.x; s.y = r.y + s.y; s.z = r.z + s.z; s.w = r.w + s.w;
+  }
+  *reinterpret_cast<float4*>(C + m * ldc + c) = s;
 }
 
 // ------------------------------------------------------------------ RoPE
@@ -860,9 +886,15 @@ hipError_t launch_train_norm_bwd(const float* X, const void* gain, const float* 
 
 hipError_t launch_train_gemm(const TGemmArgs& a, int32_t bl, bool bf16, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((a.N + GBN - 1) / GBN), (unsigned)((a.M + GBM - 1) / GBM));
+  const int32_t ns = a.ksplit > 1 ? a.ksplit : 1;
+  if (ns > 1 && (!a.part || a.kpiece % GBK || a.kpiece * (ns - 1) >= a.K || a.kpiece * ns < a.K))
+    return hipErrorInvalidValue;
+  TGemmArgs g = a;
+  if (ns == 1) g.kpiece = a.K;
+  const dim3 grid((unsigned)((a.N + GBN - 1) / GBN), (unsigned)((a.M + GBM - 1) / GBM),
+                  (unsigned)ns);
   const bool asc = a.ascale != nullptr;
-#define SVL_TGEMM(BLV, TB, ASCV) train_gemm_kernel<BLV, TB, ASCV><<<grid, TNT, 0, st>>>(a)
+#define SVL_TGEMM(BLV, TB, ASCV) train_gemm_kernel<BLV, TB, ASCV><<<grid, TNT, 0, st>>>(g)
   if (bl == 0) {
     if (bf16) { if (asc) SVL_TGEMM(0, uint16_t, true); else SVL_TGEMM(0, uint16_t, false); }
     else { if (asc) SVL_TGEMM(0, float, true); else SVL_TGEMM(0, float, false); }
@@ -871,6 +903,11 @@ hipError_t launch_train_gemm(const TGemmArgs& a, int32_t bl, bool bf16, hipStrea
     else SVL_TGEMM(1, float, false);
   }
 #undef SVL_TGEMM
+  if (ns == 1) return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  train_splitk_reduce_kernel<<<blocks(a.M * (a.N / 4)), TNT, 0, st>>>(a.part, ns, a.M, a.N, a.R,
+                                                                       a.ldr, a.C, a.ldc);
   return hipGetLastError();
 }
 

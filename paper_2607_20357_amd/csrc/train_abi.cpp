@@ -29,6 +29,26 @@ svl_status err(svl_status st, const char* fmt, ...) {
   return set_error(st, buf);
 }
 
+// K pieces of a product of M x N over K: a launch of fewer than 1024 64 x 64
+// tiles takes 2-4 pieces of at least 512 of K each, so that it holds about
+// 1280 workgroups, five per CU (640 tiles leave half the CUs one workgroup
+// short); ns = 1 keeps K whole.
+struct KSplit {
+  int32_t ns;
+  int64_t kpiece;
+};
+
+KSplit k_split(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((N + 63) / 64) * ((M + 63) / 64);
+  int64_t ns = 1;
+  if (tiles < 1024) ns = std::min<int64_t>({4, K / 512, (1280 + tiles - 1) / tiles});
+  if (ns < 2) return {1, K};
+  const int64_t kp = ((K + ns - 1) / ns + 31) / 32 * 32;
+  ns = (K + kp - 1) / kp;
+  if (ns < 2) return {1, K};
+  return {(int32_t)ns, kp};
+}
+
 // Byte offsets of the workspace regions (each 256-byte aligned).
 struct TrainLayout {
   int64_t xs;                          // X_0 .. X_{L-1}, [L][M][D]
@@ -36,6 +56,7 @@ struct TrainLayout {
   int64_t rope;                        // (cos, sin)[S][d/2]
   int64_t u, r1, q, k, v, o, lse, x1, u2, r2, ag, ae, hh;   // one layer's forward
   int64_t dxa, dxb, dx1, du, dh, dO, dq, dk, dv, dvec, pa, pf;  // its backward
+  int64_t kpart, kpart_floats;         // the K pieces' slices of one product
   int64_t total;
 };
 
@@ -81,6 +102,13 @@ TrainLayout train_layout(const svl_config& c, int32_t U, int32_t B, int32_t N, i
   t.dvec = take(M * A);
   t.pa = take(M * U);
   t.pf = take(M * U);
+  // every (N, K) the layer passes multiply
+  const int64_t shapes[][2] = {{A * d, D}, {KV * d, D}, {D, A * d}, {D, KV * d}, {F, D}, {D, F}};
+  for (const auto& nk : shapes) {
+    const KSplit ks = k_split(M, nk[0], nk[1]);
+    if (ks.ns > 1) t.kpart_floats = std::max(t.kpart_floats, ks.ns * M * nk[0]);
+  }
+  t.kpart = take(t.kpart_floats);
   t.total = off;
   return t;
 }
@@ -148,6 +176,14 @@ struct TrainRun {
     g.M = M;
     g.N = N_;
     g.K = K;
+    const KSplit ks = k_split(M, N_, K);
+    g.ksplit = 1;
+    g.kpiece = K;
+    if (ks.ns > 1 && ks.ns * M * N_ <= Lw.kpart_floats) {
+      g.ksplit = ks.ns;
+      g.kpiece = ks.kpiece;
+      g.part = f(Lw.kpart);
+    }
     return launch_train_gemm(g, bl, bf16, st);
   }
 

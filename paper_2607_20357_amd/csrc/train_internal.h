@@ -38,6 +38,12 @@ struct TGemmArgs {
   int64_t astride;
   int32_t S, kg;
   int64_t M, N, K;     // K % 16 == 0, N % 4 == 0, kg % 4 == 0
+  // split K: ksplit pieces of kpiece (a multiple of 32; the last one shorter)
+  // write float32 slices [ksplit][M][N] at part, then C = R + their sum
+  // (slices in order); ksplit = 1 writes C directly
+  int32_t ksplit;
+  int64_t kpiece;
+  float* part;
 };
 
 // Attention of one layer over B samples of S rows (buffers [B S][heads d]).
