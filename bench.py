@@ -773,8 +773,10 @@ def main():
     if (not args.no_bf16_line and args.compute == "f16" and shape.dtype == "bf16"
             and args.threshold_budget is None and args.controller is None):
         # the same step with bf16 activations and bf16 MFMA products
-        cfg16 = cfg
+        cfg16, ws16 = cfg, ws
         cfg = svl.make_config(shape, compute="bf16")
+        # bf16 activations add a plane of the normed rows' low bf16 parts
+        ws = svl.alloc_workspace(cfg, B, R, dev)
         for _ in range(max(1, args.warmup)):
             step()
         torch.cuda.synchronize()
@@ -788,7 +790,7 @@ def main():
         tok = B * (w.n_vision + w.n_text)
         bf16_line = {"compute": "bf16 activations, bf16 MFMA", "ms_per_step": round(ms_b, 4),
                      "value": round(tok / (ms_b * 1e-3), 1), "unit": "tokens/s"}
-        cfg = cfg16
+        cfg, ws = cfg16, ws16
         print(f"# bf16 compute: {ms_b:.4f} ms/step", file=sys.stderr, flush=True)
 
     # second pass, same steps, every launch bracketed by HIP events on `stream`

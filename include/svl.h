@@ -74,8 +74,13 @@ typedef enum { SVL_F32 = 0, SVL_BF16 = 1 } svl_dtype;
  * ones become fp16 subnormals, absolute error at most 2^-25) and keeps
  * activations in fp16 (11-bit significand): weights and activations must lie
  * inside the fp16 range.  SVL_COMPUTE_BF16 keeps bf16 activations (8-bit
- * significand, full bf16 range).  Both accumulate in float32 and keep the
- * residual stream in float32. */
+ * significand, full bf16 range) and multiplies them by bf16 MFMA; the
+ * RMS-normed rows enter the QKV and gate/up products of a prefill as two
+ * bf16 terms, hi = bf16(x) and lo = bf16(x - hi), both multiplied by the
+ * same weights (about 16 significant bits for those operands; twice the
+ * products, and a workspace plane of the low terms).  Decode steps take the
+ * hi terms only.  Both modes accumulate in float32 and keep the residual
+ * stream in float32. */
 typedef enum { SVL_COMPUTE_F16 = 0, SVL_COMPUTE_BF16 = 1 } svl_compute;
 
 /* Decoder shape (LLaMA block: pre-RMSNorm, rotate-half RoPE, causal

@@ -117,7 +117,7 @@ svl_status check_mask(const uint8_t* m, int64_t n, const char* what) {
 
 // ------------------------------------------------------------------ workspace
 struct WsLayout {
-  int64_t plan, rope, partial, xn, qkv, attn_out, h, total;
+  int64_t plan, rope, partial, xn, xn_lo, qkv, attn_out, h, total;
   int64_t partial_slice;   // floats per split-K slice of the output / down projections (R x d_model)
   int64_t prows;           // padded activation rows
 };
@@ -131,6 +131,13 @@ struct WsLayout {
 // layout when the buffer is larger).
 uint32_t* status_word(void* ws, size_t ws_bytes) {
   return reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + ((ws_bytes & ~size_t(3)) - 4));
+}
+
+// bf16 activations (bf16 storage, SVL_COMPUTE_BF16) carry the normed rows
+// as two bf16 terms, hi = bf16(x) and lo = bf16(x - hi), into the QKV and
+// gate/up products (both multiplied by bf16 MFMA, summed in float32).
+bool lo_parts(const svl_config& c) {
+  return c.dtype == SVL_BF16 && c.compute == SVL_COMPUTE_BF16;
 }
 
 WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows = 0) {
@@ -149,6 +156,9 @@ WsLayout ws_layout(const svl_config& c, int32_t B, int32_t R, int32_t pos_rows =
   L.partial_slice = (int64_t)R * c.d_model;
   L.prows = prow;
   L.xn = take(prow * c.d_model * es);
+  // bf16 activations: the normed rows' low bf16 parts, for the QKV and
+  // gate/up products
+  L.xn_lo = take(lo_parts(c) ? prow * c.d_model * 2 : 0);
   L.qkv = take(prow * (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim * es);
   L.attn_out = take(prow * (int64_t)c.n_heads * c.head_dim * es);
   L.h = take(prow * (int64_t)c.d_ffn * es);
@@ -206,6 +216,9 @@ struct Exec {
     a.ntiles = g.ntiles;
     a.chunks = chunks;
     a.A = A; a.lda = lda;
+    // the normed rows' low parts (QKV and gate/up products of bf16 activations)
+    if (!decode && lo_parts(c) && A == ws + L.xn && (epi == EPI_QKV || epi == EPI_SWIGLU))
+      a.A2 = ws + L.xn_lo;
     for (int i = 0; i < 3; ++i) { a.W[i] = W[i]; a.w_rows[i] = w_rows[i]; }
     a.ldw = ldw;
     a.out = out; a.ldo = ldo;
@@ -277,6 +290,7 @@ struct Exec {
     a.pslice = L.partial_slice;
     a.gain = gain;
     a.out = ws + L.xn;
+    a.out2 = !decode && lo_parts(c) ? ws + L.xn_lo : nullptr;
     a.D = c.d_model;
     a.eps = c.rms_eps;
     const int out_kind = c.dtype != SVL_BF16 ? 0 : (c.compute == SVL_COMPUTE_F16 ? 2 : 1);

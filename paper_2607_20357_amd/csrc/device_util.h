@@ -90,6 +90,13 @@ __device__ __forceinline__ uint32_t pack_act2(float lo, float hi) {
   }
 }
 
+// Low bf16 parts of two values whose high parts are the bf16 word `hi`
+// (pack_act2<false>(lo_val, hi_val)): bf16(v - bf16(v)) each, so the two
+// words together carry v to about 16 significant bits.
+__device__ __forceinline__ uint32_t bf16_low2(float v0, float v1, uint32_t hi) {
+  return pack_bf16x2(v0 - bf16_bits_to_f32(hi & 0xffffu), v1 - bf16_bits_to_f32(hi >> 16));
+}
+
 // Two bf16 values (one 32-bit word) -> the same two values as fp16.  Exact
 // for magnitudes in [2^-14, 65504]; smaller ones become fp16 subnormals
 // (absolute error at most 2^-25).

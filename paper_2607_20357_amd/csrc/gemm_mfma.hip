@@ -115,7 +115,11 @@ using Phase = std::integral_constant<int, P>;
 // waves per SIMD), or 4 x 4 (one wave per SIMD; each LDS operand feeds twice
 // the MFMAs, the accumulators sit in the AGPRs, and two workgroups share a
 // CU: the output / down projections of launches with more tiles than CUs).
-template <int EPI, int NB, bool F16, int NWAVE>
+// HILO (bf16 products of QKV / gate-up): every A fragment comes with its low
+// bf16 part from A2, multiplied right after it against the same weight
+// fragment, so the activations enter the products with about 16 significant
+// bits; two A chunks in flight instead of four keep the registers.
+template <int EPI, int NB, bool F16, int NWAVE, bool HILO = false>
 __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   constexpr int NT = NWAVE * 64;
   constexpr int RB = BM / (16 * NWAVE);         // 16-row blocks per wave
@@ -130,7 +134,9 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
 #else
   constexpr int NWS = NB <= (NWAVE == 8 ? 6 : 3) ? 2 : 1;   // weight register stages
 #endif
-  constexpr int NSA = NWAVE == 8 ? NSA8 : 2;    // A chunks in flight (register slot = chunk % NSA)
+  static_assert(!HILO || (!F16 && NWAVE == 8), "low parts: bf16 products, 8-wave tiles");
+  constexpr int NSA = HILO ? 2 : (NWAVE == 8 ? NSA8 : 2);   // A chunks in flight (slot = chunk % NSA)
+  constexpr int AU = HILO ? 4 : 2;              // A fragments per row block and chunk
   static_assert(KS % NSA == 0, "a stage holds whole rounds of A slots");
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
   __shared__ int32_t s_k0[MAX_CHUNKS];          // the tile's chunk offsets (no vmcnt waits)
@@ -157,6 +163,9 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   const __amdgpu_buffer_rsrc_t rsA =
       make_rsrc(static_cast<const uint16_t*>(a.A) + (size_t)rb0 * kblocks * 1024,
                 (uint32_t)((mcnt + 15) / 16) * blk_bytes);
+  const __amdgpu_buffer_rsrc_t rsA2 =
+      make_rsrc(static_cast<const uint16_t*>(HILO ? a.A2 : a.A) + (size_t)rb0 * kblocks * 1024,
+                HILO ? (uint32_t)((mcnt + 15) / 16) * blk_bytes : 0u);
   uint32_t voA[RB];
 #pragma unroll
   for (int i = 0; i < RB; ++i) voA[i] = (uint32_t)(RB * wave + i) * blk_bytes + lane * 16u;
@@ -203,19 +212,23 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   __syncthreads();   // s_k0 ready
 
   const int last = nk - 1;
-  uint4 sa[NSA][RB][2], sw[NWS][WLD];
+  uint4 sa[NSA][RB][AU], sw[NWS][WLD];
   // A loads and MFMAs of the wave's NRB row blocks that hold rows of the
   // tile (the pipeline is instantiated per NRB, so a wave past the tile's
   // rows issues no loads for them and the waits stay exact).  NRB < 0: all RB
   // blocks are loaded (out-of-range rows read zero) and the MFMAs branch on
   // rowblk, which keeps the widest tiles within the registers.
-  auto loadA = [&](auto nrb, int c, uint4 (&ra)[RB][2]) __attribute__((always_inline)) {
+  auto loadA = [&](auto nrb, int c, uint4 (&ra)[RB][AU]) __attribute__((always_inline)) {
     constexpr int NRB = decltype(nrb)::value < 0 ? RB : decltype(nrb)::value;
     const uint32_t soA = (uint32_t)__builtin_amdgcn_readfirstlane(s_k0[c]) * 32u;
 #pragma unroll
     for (int i = 0; i < NRB; ++i) {
       ra[i][0] = load16(rsA, voA[i], soA);
       ra[i][1] = load16(rsA, voA[i] + 1024u, soA);
+      if constexpr (HILO) {
+        ra[i][2] = load16(rsA2, voA[i], soA);
+        ra[i][3] = load16(rsA2, voA[i] + 1024u, soA);
+      }
     }
   };
   // weight stage S: chunks S*KS .. S*KS + KS-1 (past the last: the last again);
@@ -247,7 +260,7 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   // swizzle of rows j*16 + lane%16 depends on lane%16 only
   const int fl = (2 * (lane >> 4)) ^ swz(lane & 15);
   const uint16_t* Bl = Bs + (lane & 15) * LDS_STRIDE;
-  auto compute = [&](auto nrb, int buf, int q, const uint4 (&ra)[RB][2]) __attribute__((always_inline)) {
+  auto compute = [&](auto nrb, int buf, int q, const uint4 (&ra)[RB][AU]) __attribute__((always_inline)) {
     constexpr bool DYN = decltype(nrb)::value < 0;
     constexpr int NRB = DYN ? RB : decltype(nrb)::value;
     const uint16_t* B = Bl + buf * (BN * LDS_STRIDE);
@@ -265,7 +278,10 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
       for (int i = 0; i < NRB; ++i)
         if (!DYN || rowblk[i])
 #pragma unroll
-          for (int j = 0; j < NB; ++j) acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
+          for (int j = 0; j < NB; ++j) {
+            acc[i][j] = mfma16x16x32<F16>(ra[i][ks], bfr[j], acc[i][j]);
+            if constexpr (HILO) acc[i][j] = mfma16x16x32<F16>(ra[i][2 + ks], bfr[j], acc[i][j]);
+          }
     }
   };
 
@@ -490,22 +506,22 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   }
 }
 
-template <int EPI, int NB, bool F16, int NWAVE = 8>
+template <int EPI, int NB, bool F16, int NWAVE = 8, bool HILO = false>
 hipError_t launch(const MmArgs& a, hipStream_t st) {
   const unsigned grid = (unsigned)((a.ntiles + 7) / 8 * 8);
-  gemm_mfma_kernel<EPI, NB, F16, NWAVE><<<grid, NWAVE * 64, 0, st>>>(a);
+  gemm_mfma_kernel<EPI, NB, F16, NWAVE, HILO><<<grid, NWAVE * 64, 0, st>>>(a);
   return hipGetLastError();
 }
 
-template <int EPI, bool F16>
+template <int EPI, bool F16, bool HILO = false>
 hipError_t by_nb(const MmArgs& a, int32_t nb, hipStream_t st) {
   switch (nb) {
-    case 2: return launch<EPI, 2, F16>(a, st);
-    case 3: return launch<EPI, 3, F16>(a, st);
-    case 4: return launch<EPI, 4, F16>(a, st);
-    case 5: return launch<EPI, 5, F16>(a, st);
-    case 6: return launch<EPI, 6, F16>(a, st);
-    case 8: return launch<EPI, 8, F16>(a, st);
+    case 2: return launch<EPI, 2, F16, 8, HILO>(a, st);
+    case 3: return launch<EPI, 3, F16, 8, HILO>(a, st);
+    case 4: return launch<EPI, 4, F16, 8, HILO>(a, st);
+    case 5: return launch<EPI, 5, F16, 8, HILO>(a, st);
+    case 6: return launch<EPI, 6, F16, 8, HILO>(a, st);
+    case 8: return launch<EPI, 8, F16, 8, HILO>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -518,6 +534,12 @@ hipError_t dispatch(const MmArgs& a, int32_t epi, int32_t nb, int32_t waves, hip
     return hipErrorInvalidValue;
   }
   if (waves != 8) return hipErrorInvalidValue;
+  if constexpr (!F16) {
+    // bf16 products with the activations' low parts (QKV and gate/up)
+    if (a.A2 && epi == EPI_QKV) return by_nb<EPI_QKV, false, true>(a, nb, st);
+    if (a.A2 && epi == EPI_SWIGLU) return by_nb<EPI_SWIGLU, false, true>(a, nb, st);
+  }
+  if (a.A2) return hipErrorInvalidValue;   // low parts only for bf16 QKV / gate-up
   switch (epi) {
     case EPI_QKV: return by_nb<EPI_QKV, F16>(a, nb, st);
     case EPI_SWIGLU: return by_nb<EPI_SWIGLU, F16>(a, nb, st);

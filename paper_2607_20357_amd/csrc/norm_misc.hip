@@ -78,12 +78,17 @@ __global__ __launch_bounds__(NT) void resid_norm_kernel(NormArgs a) {
                           bf16_bits_to_f32(gw.y & 0xffffu), bf16_bits_to_f32(gw.y >> 16),
                           bf16_bits_to_f32(gw.z & 0xffffu), bf16_bits_to_f32(gw.z >> 16),
                           bf16_bits_to_f32(gw.w & 0xffffu), bf16_bits_to_f32(gw.w >> 16)};
-      const uint4 o = make_uint4(pack_act2<OUT == 2>(v0.x * inv * g[0], v0.y * inv * g[1]),
-                                 pack_act2<OUT == 2>(v0.z * inv * g[2], v0.w * inv * g[3]),
-                                 pack_act2<OUT == 2>(v1.x * inv * g[4], v1.y * inv * g[5]),
-                                 pack_act2<OUT == 2>(v1.z * inv * g[6], v1.w * inv * g[7]));
-      *reinterpret_cast<uint4*>(out + (a.rowmajor ? (int64_t)prow * D + 8 * c
-                                                  : packed_index((int64_t)prow, 8 * c, D))) = o;
+      const float y[8] = {v0.x * inv * g[0], v0.y * inv * g[1], v0.z * inv * g[2],
+                          v0.w * inv * g[3], v1.x * inv * g[4], v1.y * inv * g[5],
+                          v1.z * inv * g[6], v1.w * inv * g[7]};
+      const uint4 o = make_uint4(pack_act2<OUT == 2>(y[0], y[1]), pack_act2<OUT == 2>(y[2], y[3]),
+                                 pack_act2<OUT == 2>(y[4], y[5]), pack_act2<OUT == 2>(y[6], y[7]));
+      const int64_t at = a.rowmajor ? (int64_t)prow * D + 8 * c : packed_index((int64_t)prow, 8 * c, D);
+      *reinterpret_cast<uint4*>(out + at) = o;
+      if (OUT == 1 && a.out2)
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.out2) + at) =
+            make_uint4(bf16_low2(y[0], y[1], o.x), bf16_low2(y[2], y[3], o.y),
+                       bf16_low2(y[4], y[5], o.z), bf16_low2(y[6], y[7], o.w));
     }
   } else {
     const float4* gain = reinterpret_cast<const float4*>(a.gain);
@@ -206,11 +211,15 @@ __global__ __launch_bounds__(NTR) void resid_norm_reg_kernel(NormArgs a) {
       const uint2 gw = gv[i];
       const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
       const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
-      const uint2 o = make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
-                                 pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) +
-                                (a.rowmajor ? (int64_t)prow * a.D + 4 * c
-                                            : packed_index((int64_t)prow, 4 * c, a.D))) = o;
+      const float y0 = v[i].x * inv * g0, y1 = v[i].y * inv * g1;
+      const float y2 = v[i].z * inv * g2, y3 = v[i].w * inv * g3;
+      const uint2 o = make_uint2(pack_act2<OUT == 2>(y0, y1), pack_act2<OUT == 2>(y2, y3));
+      const int64_t at = a.rowmajor ? (int64_t)prow * a.D + 4 * c
+                                    : packed_index((int64_t)prow, 4 * c, a.D);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + at) = o;
+      if (OUT == 1 && a.out2)
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out2) + at) =
+            make_uint2(bf16_low2(y0, y1, o.x), bf16_low2(y2, y3, o.y));
     } else {
       const float4 g = gv[i];
       reinterpret_cast<float4*>(static_cast<float*>(a.out) + prow * a.D)[c] =
@@ -288,27 +297,34 @@ __global__ __launch_bounds__(NT8) void resid_norm8_kernel(NormArgs a) {
   for (int i = 0; i < VMAX; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
   ss = warp_sum(ss);
   const float inv = rsqrtf(ss / (float)a.D + a.eps);
-  if (valid) {
+  // pass 0: the output; pass 1 (bf16 output with out2): the low parts
+  const int npass = (OUT == 1 && a.out2) ? 2 : 1;   // uniform across the workgroup
+  for (int pass = 0; pass < npass; ++pass) {
+    if (pass) __syncthreads();   // the first pass's pieces are read
+    if (valid) {
 #pragma unroll
-    for (int i = 0; i < VMAX; ++i) {
-      if (i >= vpt) continue;
-      const int c = lane + 64 * i;                 // columns 4c .. 4c+3
-      const uint2 gw = gv[i];
-      const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
-      const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
-      *reinterpret_cast<uint2*>(stage + (c >> 1) * 144 + wave * 16 + (c & 1) * 8) =
-          make_uint2(pack_act2<OUT == 2>(v[i].x * inv * g0, v[i].y * inv * g1),
-                     pack_act2<OUT == 2>(v[i].z * inv * g2, v[i].w * inv * g3));
+      for (int i = 0; i < VMAX; ++i) {
+        if (i >= vpt) continue;
+        const int c = lane + 64 * i;                 // columns 4c .. 4c+3
+        const uint2 gw = gv[i];
+        const float g0 = bf16_bits_to_f32(gw.x & 0xffffu), g1 = bf16_bits_to_f32(gw.x >> 16);
+        const float g2 = bf16_bits_to_f32(gw.y & 0xffffu), g3 = bf16_bits_to_f32(gw.y >> 16);
+        const float y0 = v[i].x * inv * g0, y1 = v[i].y * inv * g1;
+        const float y2 = v[i].z * inv * g2, y3 = v[i].w * inv * g3;
+        uint2 o = make_uint2(pack_act2<OUT == 2>(y0, y1), pack_act2<OUT == 2>(y2, y3));
+        if (pass) o = make_uint2(bf16_low2(y0, y1, o.x), bf16_low2(y2, y3, o.y));
+        *reinterpret_cast<uint2*>(stage + (c >> 1) * 144 + wave * 16 + (c & 1) * 8) = o;
+      }
     }
-  }
-  __syncthreads();
-  // piece p: row w = p % 8 of the group, columns 8 (p / 8) .. + 7
-  uint16_t* out = static_cast<uint16_t*>(a.out);
-  for (int p = threadIdx.x; p < a.D; p += NT8) {
-    const int w = p & 7, kg = p >> 3;
-    if (base + w < sg.nrows)
-      *reinterpret_cast<uint4*>(out + packed_index((int64_t)sg.prow0 + base + w, 8 * kg, a.D)) =
-          *reinterpret_cast<const uint4*>(stage + kg * 144 + w * 16);
+    __syncthreads();
+    // piece p: row w = p % 8 of the group, columns 8 (p / 8) .. + 7
+    uint16_t* out = static_cast<uint16_t*>(pass ? a.out2 : a.out);
+    for (int p = threadIdx.x; p < a.D; p += NT8) {
+      const int w = p & 7, kg = p >> 3;
+      if (base + w < sg.nrows)
+        *reinterpret_cast<uint4*>(out + packed_index((int64_t)sg.prow0 + base + w, 8 * kg, a.D)) =
+            *reinterpret_cast<const uint4*>(stage + kg * 144 + w * 16);
+    }
   }
 }
 

@@ -46,6 +46,9 @@ struct MmArgs {
   int32_t ntiles;
   const KChunk* chunks;
   const void* A;         // fragment-packed activations, K = lda
+  const void* A2;        // bf16 products of QKV / gate-up: the low bf16 parts of
+                         // the same activations (A2 = bf16(x - A)), same layout,
+                         // multiplied after A against the same weights; or nullptr
   int32_t lda;
   const void* W[3];      // bf16 weight matrices [rows][ldw] (gate/up: W[0] gate, W[1] up)
   int32_t w_rows[3];     // their row counts (load range)
@@ -122,6 +125,7 @@ struct NormArgs {
   int64_t pslice;
   const void* gain;    // [D], weight dtype
   void* out;           // normed rows: fragment-packed (16-bit) or row-major (float32)
+  void* out2;          // bf16 packed output: the low parts bf16(x - out), or nullptr
   int32_t D;
   float eps;
 };

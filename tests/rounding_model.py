@@ -27,8 +27,18 @@ POINTS = ("xn", "qkv", "p", "o", "h")
 _SUBPOINTS = {"xn": ("xn_attn", "xn_ffn")}
 
 
-def _round(x: torch.Tensor, dt: Optional[torch.dtype]) -> torch.Tensor:
-    return x if dt is None else x.to(dt).to(torch.float32)
+# "bf16x2": a value carried as two bf16 terms, hi = bf16(x) and
+# lo = bf16(x - hi), whose products are summed in float32
+_HILO = "bf16x2"
+
+
+def _round(x: torch.Tensor, dt) -> torch.Tensor:
+    if dt is None:
+        return x
+    if dt == _HILO:
+        hi = x.to(torch.bfloat16).to(torch.float32)
+        return hi + (x - hi).to(torch.bfloat16).to(torch.float32)
+    return x.to(dt).to(torch.float32)
 
 
 def _rms(x: torch.Tensor, g: torch.Tensor, eps: float) -> torch.Tensor:
@@ -51,14 +61,14 @@ def _rope(a: torch.Tensor, cs) -> torch.Tensor:
     return torch.cat([a1 * c - a2 * s, a2 * c + a1 * s], dim=-1)
 
 
-_DT = {"bf16": torch.bfloat16, "f16": torch.float16, None: None}
+_DT = {"bf16": torch.bfloat16, "f16": torch.float16, _HILO: _HILO, None: None}
 
 
 class RoundedPrefill:
     """Runs the decoder layers of one sample's packed sequence in float32 with
     the rounding points `points` (a subset of POINTS) rounded to `act`
-    ("bf16", "f16" or None for none), or with `points` a dict giving each
-    rounded point its own type.  Variants share the weights: call `layer`
+    ("bf16", "f16", "bf16x2" or None for none), or with `points` a dict
+    giving each rounded point its own type.  Variants share the weights: call `layer`
     with each layer's float32 weights in turn."""
 
     def __init__(self, shape, x0: np.ndarray, act: Optional[str], points):
