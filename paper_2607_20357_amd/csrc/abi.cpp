@@ -63,10 +63,22 @@ hipError_t timed(int cls, hipStream_t st, F&& f) {
     a = g_timing.take();
     b = g_timing.take();
   }
-  if (!a || !b) return f();
-  hipEventRecord(a, st);
+  // an event that fails to record goes back to the pool and the launch runs
+  // untimed (timing is a diagnostic; the launch's own status is returned)
+  auto give_back = [&] {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    if (a) g_timing.pool.push_back(a);
+    if (b) g_timing.pool.push_back(b);
+  };
+  if (!a || !b || hipEventRecord(a, st) != hipSuccess) {
+    give_back();
+    return f();
+  }
   hipError_t r = f();
-  hipEventRecord(b, st);
+  if (hipEventRecord(b, st) != hipSuccess) {
+    give_back();
+    return r;
+  }
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.recs.push_back({cls, a, b});
   return r;
