@@ -51,7 +51,8 @@ def _run(w, seed, prefix, units, tau_tok=0.7, tau_comp=1.3, drop_first=False, no
     rng = np.random.default_rng(seed + 101)
     nl = (L - prefix) * units
     z = rng.normal(0.3, 1.5, (B, N)).astype(np.float32)
-    z[:, 0] = -20.0 if drop_first else 20.0
+    if N:
+        z[:, 0] = -20.0 if drop_first else 20.0
     g = rng.normal(0.6, 1.5, (B, nl)).astype(np.float32)
     xi = rng.logistic(0, 1, (B, N)).astype(np.float32) if noise else None
     xg = rng.logistic(0, 1, (B, nl)).astype(np.float32) if noise else None
@@ -146,6 +147,17 @@ def test_train_head_dim_32_gqa():
     shape = dataclasses.replace(base.shape, n_heads=8, n_kv_heads=4, head_dim=32)
     w = dataclasses.replace(base, shape=shape, n_vision=100, n_text=30, name="tiny_hd32_train")
     _run(w, 9, 1, 4)
+
+
+@pytest.mark.parametrize("n_vision,n_text,prefix", [(0, 40, 1), (60, 0, 1), (40, 24, 2)])
+def test_train_edge_shapes(n_vision, n_text, prefix):
+    """No vision tokens (no token logits or gradients), no text tokens, and a
+    prefix covering every layer (no gate logits or gradients)."""
+    w = dataclasses.replace(_tiny(), n_vision=n_vision, n_text=n_text,
+                            name=f"tiny_train_n{n_vision}_t{n_text}_p{prefix}")
+    got = _run(w, 10, prefix, 4)
+    assert got["token_mask"].shape == (2, n_vision)
+    assert got["unit_mask"].shape == (2, (w.shape.n_layers - prefix) * 4)
 
 
 def test_train_headline_width():
