@@ -176,8 +176,8 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   const int wy = wave >> 1, wx = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * GBM, n0 = (int64_t)blockIdx.x * GBN;
   const TB* B = static_cast<const TB*>(a.B);
-  const int64_t kb = (int64_t)blockIdx.z * a.kpiece;
-  const int64_t ke = kb + a.kpiece < a.K ? kb + a.kpiece : a.K;
+  const int64_t k_lo = (int64_t)blockIdx.z * a.kpiece;   // this piece's K range
+  const int64_t k_hi = k_lo + a.kpiece < a.K ? k_lo + a.kpiece : a.K;
   const bool split = gridDim.z > 1;
   float* C = split ? a.part + (int64_t)blockIdx.z * a.M * a.N : a.C;
   const int64_t ldc = split ? a.N : a.ldc;
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       v[h2] = zero;
-      if (aok && k0 + 16 * h2 < ke) {   // K % 32 == 16: the second half of the last step is 0
+      if (aok && k0 + 16 * h2 < k_hi) {   // K % 32 == 16: the second half of the last step is 0
         v[h2] = *reinterpret_cast<const float4*>(a.A + arow * a.lda + k0 + 16 * h2 + ak);
         if constexpr (ASC)
           v[h2] = f4scale(v[h2], srow[(uint32_t)(k0 + 16 * h2 + ak) / (uint32_t)a.kg]);
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       v[h2] = zero;
-      if (bok && k0 + 16 * h2 < ke) {
+      if (bok && k0 + 16 * h2 < k_hi) {
         if constexpr (BL == 0) v[h2] = ld4(B, (n0 + bn) * a.ldb + k0 + 16 * h2 + bk);
         else v[h2] = ld4(B, (k0 + 16 * h2 + bk) * a.ldb + n0 + bn);
       }
@@ -228,9 +228,9 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
   const int fr = lane & 15, fk = lane >> 4;
 
   float4 av[2], bv[2];
-  load_a(kb, av);
-  load_b(kb, bv);
-  for (int64_t k0 = kb; k0 < ke; k0 += GBK) {
+  load_a(k_lo, av);
+  load_b(k_lo, bv);
+  for (int64_t k0 = k_lo; k0 < k_hi; k0 += GBK) {
     __syncthreads();   // the previous step's readers are done
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
@@ -249,7 +249,7 @@ __global__ __launch_bounds__(TNT) void train_gemm_kernel(TGemmArgs a) {
       }
     }
     __syncthreads();
-    if (k0 + GBK < ke) {
+    if (k0 + GBK < k_hi) {
       load_a(k0 + GBK, av);
       load_b(k0 + GBK, bv);
     }
