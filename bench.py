@@ -45,7 +45,9 @@ def parse():
     p.add_argument("--compute", choices=("f16", "bf16"), default="f16",
                    help="activation / matrix-input type of the 16-bit path (fp16 or bf16 MFMA)")
     p.add_argument("--no-bf16-line", action="store_true",
-                   help="skip the extra timing of the headline with bf16 activations")
+                   help="skip the extra prefill timings of the default run: the headline "
+                        "with bf16 activations and the compute-bound ragged batch of 8 (the "
+                        "counter runs skip them, so only the headline's GEMMs are counted)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-train-line", action="store_true",
                    help="skip the training-step timing (svl_train_step) of the default run")
@@ -639,6 +641,64 @@ def train_line(w, seed, dev, steps=2, warmup=1):
             "fp32_peak_tflops": FP32_PEAK_TFLOPS, "frac_fp32_peak": round(tf / FP32_PEAK_TFLOPS, 4)}
 
 
+COMPUTE_BOUND = "llava7b_b8_ragged"
+
+
+def compute_bound_line(headline, table, compute: str, seed: int, dev, steps: int = 5,
+                       warmup: int = 2) -> dict:
+    """GEMM MFMA fraction of the compute-bound ragged batch of 8 (same 7B shape,
+    so the headline's weights, which depend only on shape and seed, serve it
+    unchanged): executed GEMM FLOPs over the GEMM launches' event time at the
+    dense peak."""
+    import torch
+
+    import paper_2607_20357_amd as svl
+    import workloads as W
+
+    w = W.get_workload(COMPUTE_BOUND)
+    if w.shape != headline.shape:
+        return {"workload": COMPUTE_BOUND, "skipped": "shape differs from the headline's"}
+    inp = W.draw_inputs(w, seed, device=dev)
+    cfg = svl.make_config(w.shape, compute=compute)
+    B, N = inp.scores.shape
+    seqlens = (inp.keep + w.n_text).astype(np.int64)
+    R = int(seqlens.sum())
+    scores = torch.from_numpy(inp.scores).to(dev)
+    kept = torch.empty((B, N), dtype=torch.int32, device=dev)
+    resid = torch.empty((R, w.shape.d_model), dtype=torch.float32, device=dev)
+    ws = svl.alloc_workspace(cfg, B, R, dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        svl.svl_prefill(cfg, table, inp.keep, scores, inp.vision, inp.text, inp.layer_mask,
+                        inp.head_mask, inp.ffn_mask, kept, resid, ws, stream=stream,
+                        want_flops=False)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    svl.svl_timing_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    svl.svl_timing_enable(False)
+    ktime = {k: svl.svl_timing_read(k) for k in svl.KCLASS}
+    flops = svl.svl_count_flops(cfg, seqlens, inp.layer_mask, inp.head_mask, inp.ffn_mask)
+    gemm_flops = flops["q"] + flops["kv"] + flops["o"] + flops["ffn"]
+    gemm_ms = sum(ktime[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / steps
+    return {"workload": COMPUTE_BOUND, "batch": B, "kept_tokens": R, "ms_per_step": round(ms, 3),
+            "gemm_ms_per_step": round(gemm_ms, 3),
+            "mfma_util_gemm_pct": round(100 * gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2),
+            "mfma_util_prefill_pct": round(100 * flops["total"] / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2)}
+
+
 def main():
     args = parse()
     if args.train:
@@ -886,6 +946,7 @@ def main():
         "mfma_util_gemm_pct": round(100 * gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2),
         "mfma_util_attn_pct": round(100 * flops["attn"] / (attn_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 3)
         if attn_ms > 0 else None,
+        "mfma_util_prefill_pct": round(100 * flops["total"] / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 2),
         "gemm_ms_per_step": round(gemm_ms, 4),
         # the GEMMs' floor is the larger of their MFMA time at the dense peak
         # and their algorithmic bytes at 8 TB/s; the ceiling of the MFMA
@@ -927,6 +988,9 @@ def main():
                     "+ row compaction + remaining layers"}
     if bf16_line is not None:
         result["bf16_compute"] = bf16_line
+    if not args.no_bf16_line and default_mode and w.name == W.HEADLINE:
+        # the compute-bound counterpart of the headline's MFMA fraction
+        result["compute_bound"] = compute_bound_line(w, table, args.compute, args.seed, dev)
     if not args.no_train_line and default_mode and w.name == W.HEADLINE:
         result["train_step"] = train_line(w, args.seed, dev)
     if not args.no_cpu_baseline and default_mode:
