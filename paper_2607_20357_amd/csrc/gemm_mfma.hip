@@ -118,7 +118,7 @@ using Phase = std::integral_constant<int, P>;
 // HILO (bf16 products of QKV / gate-up): every A fragment comes with its low
 // bf16 part from A2, multiplied right after it against the same weight
 // fragment, so the activations enter the products with about 16 significant
-// bits; two A chunks in flight instead of four keep the registers.
+// bits.
 template <int EPI, int NB, bool F16, int NWAVE, bool HILO = false>
 __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   constexpr int NT = NWAVE * 64;
@@ -135,7 +135,10 @@ __global__ __launch_bounds__(NWAVE * 64) void gemm_mfma_kernel(MmArgs a) {
   constexpr int NWS = NB <= (NWAVE == 8 ? 6 : 3) ? 2 : 1;   // weight register stages
 #endif
   static_assert(!HILO || (!F16 && NWAVE == 8), "low parts: bf16 products, 8-wave tiles");
-  constexpr int NSA = HILO ? 2 : (NWAVE == 8 ? NSA8 : 2);   // A chunks in flight (slot = chunk % NSA)
+  // A chunks in flight (register slot = chunk % NSA); with the low terms the
+  // tiles of up to 4 blocks keep four within the registers (211-256 VGPRs,
+  // 5.60 -> 5.30-5.52 ms per bf16 headline step), wider ones two
+  constexpr int NSA = HILO ? (NB <= 4 ? 4 : 2) : (NWAVE == 8 ? NSA8 : 2);
   constexpr int AU = HILO ? 4 : 2;              // A fragments per row block and chunk
   static_assert(KS % NSA == 0, "a stage holds whole rounds of A slots");
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * BN * LDS_STRIDE];
