@@ -24,10 +24,10 @@ def _row_err(g, o):
     return float(np.abs(g - o).max() / den) if den > 0 else float(np.abs(g).max())
 
 
-def _decode_case(w, seed, steps, extra=3):
+def _decode_case(w, seed, steps, extra=3, compute="f16"):
     dev = "cuda"
     shape = w.shape
-    cfg = svl.make_config(shape)
+    cfg = svl.make_config(shape, compute=compute)
     inp = W.draw_inputs(w, seed, device=dev)
     layers = [W.draw_layer_weights(w, l, seed, device=dev) for l in range(shape.n_layers)]
     table = svl.LayerTable(layers)
@@ -47,7 +47,7 @@ def _decode_case(w, seed, steps, extra=3):
     # finite inputs and weights: the call's status word is clear
     assert svl.svl_workspace_status(ws) == 0
     # the cache writes leave the prefill itself unchanged
-    _, cu2, plain, _ = gpu_prefill(w, inp, layers, table=table)
+    _, cu2, plain, _ = gpu_prefill(w, inp, layers, table=table, compute=compute)
     np.testing.assert_array_equal(cu, cu2)
     np.testing.assert_array_equal(resid.cpu().numpy(), plain)
 
@@ -83,6 +83,17 @@ def test_decode_ragged_batch():
     w = W.scaled(W.get_workload("llava7b_b8_ragged"), n_layers=4, d_model=512, n_heads=4,
                  n_kv_heads=4, d_ffn=1024, name="dec8")
     errs = _decode_case(w, 7, steps=3)
+    print(f"max rel err over rows: {max(errs):.2e}", flush=True)
+    assert max(errs) <= tol_for(w.shape), errs
+
+
+def test_decode_ragged_batch_bf16():
+    """The ragged batch with bf16 activations: a bf16 cache and bf16 products
+    (the cache-filling prefill carries the normed rows' low bf16 terms into
+    its QKV and gate/up products, the decode steps the high terms only)."""
+    w = W.scaled(W.get_workload("llava7b_b8_ragged"), n_layers=4, d_model=512, n_heads=4,
+                 n_kv_heads=4, d_ffn=1024, name="dec8_bf16")
+    errs = _decode_case(w, 7, steps=3, compute="bf16")
     print(f"max rel err over rows: {max(errs):.2e}", flush=True)
     assert max(errs) <= tol_for(w.shape), errs
 
