@@ -23,11 +23,12 @@ from oracle import controller as oc
 pytestmark = pytest.mark.gpu
 
 
-def _run(w, seed, prefix, units, budget, shift, pe_dim=64, hidden=128, vocab=0):
-    print(f"controlled {w.name} seed={seed} P={prefix} units={units} b={budget}", flush=True)
+def _run(w, seed, prefix, units, budget, shift, pe_dim=64, hidden=128, vocab=0, compute="f16"):
+    print(f"controlled {w.name} seed={seed} P={prefix} units={units} b={budget} "
+          f"compute={compute}", flush=True)
     dev = "cuda"
     shape = w.shape
-    cfg = svl.make_config(shape)
+    cfg = svl.make_config(shape, compute=compute)
     inp = W.draw_inputs(w, seed, device=dev)
     layers = [W.draw_layer_weights(w, l, seed, device=dev) for l in range(shape.n_layers)]
     draw = W.draw_controller(w, seed, device=dev, prefix=prefix, units=units, pe_dim=pe_dim,
@@ -121,6 +122,14 @@ def test_controlled_bf16_ragged_batch():
     out, ref = _run(w, 4, prefix=1, units=4, budget=0.4, shift=-0.2)
     # some samples are trimmed at the prefix boundary, others keep every token
     assert (ref.keep < ref.counts).any() and (ref.keep == ref.counts).any()
+
+
+def test_controlled_bf16_activations():
+    """The ragged batch of the test above with bf16 activations and products
+    (the normed rows' low bf16 terms in the QKV and gate/up products)."""
+    w = W.scaled(W.get_workload("llava7b_b8_ragged"), n_layers=4, d_model=512, n_heads=8,
+                 n_kv_heads=8, d_ffn=1024, batch=4, n_vision=200, n_text=24, name="ctrl_b4_bf16")
+    _run(w, 4, prefix=1, units=4, budget=0.4, shift=-0.2, compute="bf16")
 
 
 def test_controlled_bf16_gqa_layer_controller():
