@@ -334,17 +334,22 @@ __global__ void train_rope_kernel(float* X, int64_t ld, int32_t nheads, int32_t 
 // every row for the backward.
 template <int HD>
 struct FwdSmem {
-  float qt[HD][68];     // Q^T of the query tile, scaled by 1/sqrt(d)
-  float kt[HD][68];     // K^T of the key tile
+  // one region in turn: Q^T of the query tile (scaled by 1/sqrt(d), read
+  // once into registers), then per key tile K^T, then P^T (pt[key][query])
+  // once every wave has its scores; 69 KB at d = 128, two workgroups per CU
+  union {
+    float qt[HD][68];
+    float kt[HD][68];
+    float pt[64][68];
+  } u;
   float v[64][HD + 4];  // V rows of the key tile
-  float pt[64][68];     // P^T: pt[key][query]
 };
 
 template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
   // 64 queries x 64 keys per tile on v_mfma_f32_16x16x4_f32: wave w owns
   // queries 16 w .. 16 w + 15 against the tile's 64 keys (four 16 x 16
-  // score blocks, A = Q from Q^T in LDS, B = K^T), then O += P V with P
+  // score blocks, A = the wave's Q fragments in registers, B = K^T), then O += P V with P
   // passed through the wave's own columns of P^T in LDS (A operand) and V
   // rows (B operand).  Lane l holds rows 4 (l / 16) + r, r < 4, of every
   // block, so a row's statistics stay in the 16 lanes that share l / 16.
@@ -363,11 +368,17 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
     const int r = idx / C4, c = (idx % C4) * 4;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (q0 + r < a.S) v = f4scale(*reinterpret_cast<const float4*>(a.Q + (base + q0 + r) * ldq + (int64_t)h * HD + c), a.scale);
-    sm.qt[c + 0][r] = v.x;
-    sm.qt[c + 1][r] = v.y;
-    sm.qt[c + 2][r] = v.z;
-    sm.qt[c + 3][r] = v.w;
+    sm.u.qt[c + 0][r] = v.x;
+    sm.u.qt[c + 1][r] = v.y;
+    sm.u.qt[c + 2][r] = v.z;
+    sm.u.qt[c + 3][r] = v.w;
   }
+  __syncthreads();
+  const int qw = 16 * wave;   // the wave's first query of the tile
+  // the wave's A fragments of the score products: qf[i] = Q^T[4 i + lg][qw + lr]
+  float qf[HD / 4];
+#pragma unroll
+  for (int i = 0; i < HD / 4; ++i) qf[i] = sm.u.qt[4 * i + lg][qw + lr];
   float mrow[4], lrow[4];
   floatx4 o[NBO];
 #pragma unroll
@@ -377,7 +388,6 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
   }
 #pragma unroll
   for (int n = 0; n < NBO; ++n) o[n] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int qw = 16 * wave;   // the wave's first query of the tile
   // K / V of a key tile: thread pieces idx = t + TNT e (row idx / C4, 4
   // columns from (idx % C4) * 4), loaded into registers one tile ahead
   constexpr int KE = 64 * C4 / TNT;
@@ -399,14 +409,14 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
   load_kv(0);
   for (int kt = 0; kt <= qt; ++kt) {
     const int64_t k0 = (int64_t)kt * 64;
-    __syncthreads();   // the previous tile's readers are done
+    __syncthreads();   // the previous tile's readers (and the Q^T readers) are done
 #pragma unroll
     for (int e = 0; e < KE; ++e) {
       const int idx = t + TNT * e, r = idx / C4, c = (idx % C4) * 4;
-      sm.kt[c + 0][r] = kreg[e].x;
-      sm.kt[c + 1][r] = kreg[e].y;
-      sm.kt[c + 2][r] = kreg[e].z;
-      sm.kt[c + 3][r] = kreg[e].w;
+      sm.u.kt[c + 0][r] = kreg[e].x;
+      sm.u.kt[c + 1][r] = kreg[e].y;
+      sm.u.kt[c + 2][r] = kreg[e].z;
+      sm.u.kt[c + 3][r] = kreg[e].w;
       *reinterpret_cast<float4*>(&sm.v[r][c]) = vreg[e];
     }
     __syncthreads();
@@ -414,12 +424,12 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
     floatx4 sc[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) sc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
+#pragma unroll
     for (int d = 0; d < HD; d += 4) {
-      const float qa = sm.qt[d + lg][qw + lr];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        sc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, sm.kt[d + lg][16 * j + lr], sc[j], 0, 0, 0);
+        sc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[d / 4], sm.u.kt[d + lg][16 * j + lr], sc[j],
+                                                     0, 0, 0);
     }
     // sc[j][r] = score of query qw + 4 lg + r and key 16 j + lr of the tile
     float corr[4];
@@ -451,10 +461,12 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
       lrow[r] = lrow[r] * corr[r] + rs;
       mrow[r] = mn;
     }
-    // P^T: pt[key][query], the wave's own 16 query columns
+    // P^T: pt[key][query], the wave's own 16 query columns, in K^T's place
+    // once every wave has read K^T
+    __syncthreads();
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(&sm.pt[16 * j + lr][qw + 4 * lg]) =
+      *reinterpret_cast<float4*>(&sm.u.pt[16 * j + lr][qw + 4 * lg]) =
           make_float4(sc[j][0], sc[j][1], sc[j][2], sc[j][3]);
 #pragma unroll
     for (int n = 0; n < NBO; ++n)
@@ -463,7 +475,7 @@ __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
     // O += P V (the P^T writes above are the wave's own; LDS keeps a wave's order)
 #pragma unroll 4
     for (int k = 0; k < 64; k += 4) {
-      const float pa = sm.pt[k + lg][qw + lr];
+      const float pa = sm.u.pt[k + lg][qw + lr];
 #pragma unroll
       for (int n = 0; n < NBO; ++n)
         o[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, sm.v[k + lg][16 * n + lr], o[n], 0, 0, 0);
