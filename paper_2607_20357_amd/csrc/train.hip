@@ -518,18 +518,22 @@ __device__ __forceinline__ void load_t(float (*dst)[68], const float* src, int64
 // and stored for the key / value gradient.
 template <int HD>
 struct DqSmem {
-  float qt[HD][68];
-  float dot[HD][68];
+  // first the query tile's Q^T (scaled) in kt and dO^T in vt, read once into
+  // registers; then per key tile K^T and V^T, and dS (ds[key][query]) in
+  // V^T's place once every wave has its dP: 69 KB at d = 128, two
+  // workgroups per CU
   float kt[HD][68];
-  float vt[HD][68];
-  float ds[64][68];     // ds[key][query]
+  union {
+    float vt[HD][68];
+    float ds[64][68];
+  } u;
 };
 
 template <int HD>
-__global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
+__global__ __launch_bounds__(TNT, 2) void train_attn_dq_kernel(TAttnArgs a) {   // 2 waves per SIMD
   // v_mfma_f32_16x16x4_f32: wave w owns queries 16 w .. 16 w + 15 of the
   // tile; S = (Q scale) K^T and dP = dO V^T as four 16 x 16 blocks each (A
-  // from the transposed query tiles, B from K^T / V^T), dS = P (dP - D)
+  // the wave's Q / dO fragments in registers, B from K^T / V^T), dS = P (dP - D)
   // through the wave's own columns of ds[key][query] into dQ += dS K.  Lane
   // l holds rows 4 (l / 16) + r, r < 4, of every block.
   constexpr int NBO = HD / 16;
@@ -543,8 +547,16 @@ __global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
   const int64_t ldq = (int64_t)a.A * HD, ldk = (int64_t)a.KV * HD;
   const int64_t q0 = (int64_t)qt * 64;
   const int qw = 16 * wave;
-  load_t<HD>(sm.qt, a.Q, base + q0, ldq, (int64_t)h * HD, a.S - q0, a.scale);
-  load_t<HD>(sm.dot, a.dO, base + q0, ldq, (int64_t)h * HD, a.S - q0, 1.0f);
+  load_t<HD>(sm.kt, a.Q, base + q0, ldq, (int64_t)h * HD, a.S - q0, a.scale);
+  load_t<HD>(sm.u.vt, a.dO, base + q0, ldq, (int64_t)h * HD, a.S - q0, 1.0f);
+  __syncthreads();
+  // the wave's A fragments: qf[i] = (Q scale)^T[4 i + lg][qw + lr], df[i] the same of dO
+  float qf[HD / 4], df[HD / 4];
+#pragma unroll
+  for (int i = 0; i < HD / 4; ++i) {
+    qf[i] = sm.kt[4 * i + lg][qw + lr];
+    df[i] = sm.u.vt[4 * i + lg][qw + lr];
+  }
   // D = dO . O and lse of the lane's four rows (each of the 16 lanes of a
   // row sums HD / 16 of its columns)
   float Dr[4], lse[4];
@@ -568,22 +580,24 @@ __global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
   for (int n = 0; n < NBO; ++n) acc[n] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int kt = 0; kt <= qt; ++kt) {
     const int64_t k0 = (int64_t)kt * 64;
-    __syncthreads();
+    __syncthreads();   // the previous tile's (and the query fragments') readers are done
     load_t<HD>(sm.kt, a.K, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
-    load_t<HD>(sm.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
+    load_t<HD>(sm.u.vt, a.V, base + k0, ldk, (int64_t)g * HD, a.S - k0, 1.0f);
     __syncthreads();
     floatx4 sc[4], dp[4];
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) sc[jb] = dp[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+#pragma unroll
     for (int d = 0; d < HD; d += 4) {
-      const float qa = sm.qt[d + lg][qw + lr], da = sm.dot[d + lg][qw + lr];
 #pragma unroll
       for (int jb = 0; jb < 4; ++jb) {
-        sc[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa, sm.kt[d + lg][16 * jb + lr], sc[jb], 0, 0, 0);
-        dp[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(da, sm.vt[d + lg][16 * jb + lr], dp[jb], 0, 0, 0);
+        sc[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[d / 4], sm.kt[d + lg][16 * jb + lr], sc[jb],
+                                                      0, 0, 0);
+        dp[jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(df[d / 4], sm.u.vt[d + lg][16 * jb + lr],
+                                                      dp[jb], 0, 0, 0);
       }
     }
+    __syncthreads();   // every wave has read V^T: dS goes in its place
     // dS of query qw + 4 lg + r and key 16 jb + lr, into ds[key][query]
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) {
@@ -596,12 +610,12 @@ __global__ __launch_bounds__(TNT) void train_attn_dq_kernel(TAttnArgs a) {
         const float p = (kj <= qi && kj < a.S && qi < a.S) ? expf(sc[jb][r] - lse[r]) : 0.0f;
         wv[r] = p * (dp[jb][r] - Dr[r]);
       }
-      *reinterpret_cast<float4*>(&sm.ds[16 * jb + lr][qw + 4 * lg]) = w;
+      *reinterpret_cast<float4*>(&sm.u.ds[16 * jb + lr][qw + 4 * lg]) = w;
     }
     // dQ[q][d] += sum_k dS[q][k] K[k][d] (the ds writes above are the wave's own)
 #pragma unroll 4
     for (int k = 0; k < 64; k += 4) {
-      const float pa = sm.ds[k + lg][qw + lr];
+      const float pa = sm.u.ds[k + lg][qw + lr];
 #pragma unroll
       for (int n = 0; n < NBO; ++n)
         acc[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, sm.kt[16 * n + lr][k + lg], acc[n], 0, 0, 0);
