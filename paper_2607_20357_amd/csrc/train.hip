@@ -349,9 +349,9 @@ template <int HD>
 __global__ __launch_bounds__(TNT) void train_attn_fwd_kernel(TAttnArgs a) {
   // 64 queries x 64 keys per tile on v_mfma_f32_16x16x4_f32: wave w owns
   // queries 16 w .. 16 w + 15 against the tile's 64 keys (four 16 x 16
-  // score blocks, A = the wave's Q fragments in registers, B = K^T), then O += P V with P
-  // passed through the wave's own columns of P^T in LDS (A operand) and V
-  // rows (B operand).  Lane l holds rows 4 (l / 16) + r, r < 4, of every
+  // score blocks, A = the wave's Q fragments in registers, B = K^T), then
+  // O += P V with P passed through the wave's own columns of P^T in LDS
+  // (A operand) and V rows (B operand).  Lane l holds rows 4 (l / 16) + r, r < 4, of every
   // block, so a row's statistics stay in the 16 lanes that share l / 16.
   constexpr int NBO = HD / 16;   // 16-column blocks of the output
   constexpr int C4 = HD / 4;
@@ -533,7 +533,8 @@ template <int HD>
 __global__ __launch_bounds__(TNT, 2) void train_attn_dq_kernel(TAttnArgs a) {   // 2 waves per SIMD
   // v_mfma_f32_16x16x4_f32: wave w owns queries 16 w .. 16 w + 15 of the
   // tile; S = (Q scale) K^T and dP = dO V^T as four 16 x 16 blocks each (A
-  // the wave's Q / dO fragments in registers, B from K^T / V^T), dS = P (dP - D)
+  // the wave's Q / dO fragments in registers, B from K^T / V^T), then
+  // dS = P (dP - D)
   // through the wave's own columns of ds[key][query] into dQ += dS K.  Lane
   // l holds rows 4 (l / 16) + r, r < 4, of every block.
   constexpr int NBO = HD / 16;
