@@ -534,9 +534,8 @@ __global__ __launch_bounds__(TNT, 2) void train_attn_dq_kernel(TAttnArgs a) {   
   // v_mfma_f32_16x16x4_f32: wave w owns queries 16 w .. 16 w + 15 of the
   // tile; S = (Q scale) K^T and dP = dO V^T as four 16 x 16 blocks each (A
   // the wave's Q / dO fragments in registers, B from K^T / V^T), then
-  // dS = P (dP - D)
-  // through the wave's own columns of ds[key][query] into dQ += dS K.  Lane
-  // l holds rows 4 (l / 16) + r, r < 4, of every block.
+  // dS = P (dP - D) through the wave's own columns of ds[key][query] into
+  // dQ += dS K.  Lane l holds rows 4 (l / 16) + r, r < 4, of every block.
   constexpr int NBO = HD / 16;
   constexpr int CPT = HD / 16;   // columns per lane of the D reduction
   __shared__ __attribute__((aligned(16))) DqSmem<HD> sm;
